@@ -1,0 +1,313 @@
+"""Plain CPU oracle of the keyed Poisson race (test infrastructure only).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s ``cpu_baseline``
+leg may import this package.  It shares no code with the HIP library
+(``paper_2609_21858_amd``) and never imports it; the two meet only through the
+seeded input generator in ``workloads.py``.
+
+The arithmetic lives in ``psd_oracle.c`` (double precision, exhaustive); this
+module adds the block-level orchestration in plain Python:
+
+* draft path k of a speculative block drafts depth s with the race of its own
+  slot k over its draft row, keyed by the context (key, t, last m tokens of
+  prefix || x^(k)_{<s}) -- Sec. 3.3 / Sec. 4 algorithms and the non-identical
+  proposal construction (Prop. "heterogeneous PML bound");
+* the target chain races all K slots at every depth s = 0..gamma, keyed by the
+  context of its own chain prefix || y_{<s} (stopping-time drafter invariance,
+  Prop. on stopping-time invariance: the chain never looks at the drafts);
+* the walk emits target tokens while they belong to the drafts of the still
+  active paths, then the bonus token (Alg. "Multi-Draft ... (Formal)").
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "psd_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+LAYOUT_TREE = 0
+LAYOUT_FLAT = 1
+NEAR_TIE = 1e-6  # gap (natural-log score units = relative gap of E/p) below which either token is accepted
+
+
+def build() -> str:
+    """Compile the oracle with gcc into oracle/liboracle.so."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-o", _LIB, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    return _LIB
+
+
+class _RaceResult(ctypes.Structure):
+    _fields_ = [
+        ("token", ctypes.c_int32),
+        ("slot", ctypes.c_int32),
+        ("best", ctypes.c_double),
+        ("second", ctypes.c_double),
+        ("lse", ctypes.c_double),
+    ]
+
+
+_lib_handle = None
+
+
+def _lib():
+    global _lib_handle
+    if _lib_handle is not None:
+        return _lib_handle
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    f32p = ctypes.POINTER(ctypes.c_float)
+    f64p = ctypes.POINTER(ctypes.c_double)
+    lib.oracle_philox.argtypes = [u32p, u32p, u32p]
+    lib.oracle_philox.restype = None
+    lib.oracle_fold.argtypes = [u32p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, u32p]
+    lib.oracle_fold.restype = None
+    lib.oracle_context_key.argtypes = [ctypes.c_uint64, ctypes.c_int64, i32p, ctypes.c_int, u32p]
+    lib.oracle_context_key.restype = None
+    lib.oracle_uniform.argtypes = [ctypes.c_uint32]
+    lib.oracle_uniform.restype = ctypes.c_double
+    lib.oracle_clocks.argtypes = [u32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, f64p]
+    lib.oracle_clocks.restype = ctypes.c_int
+    lib.oracle_clock.argtypes = [u32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    lib.oracle_clock.restype = ctypes.c_double
+    lib.oracle_lse.argtypes = [f32p, ctypes.c_int, ctypes.c_float]
+    lib.oracle_lse.restype = ctypes.c_double
+    lib.oracle_race.argtypes = [f32p, ctypes.c_int, ctypes.c_float, u32p, ctypes.c_int, ctypes.c_int,
+                                ctypes.c_int, ctypes.POINTER(_RaceResult)]
+    lib.oracle_race.restype = ctypes.c_int
+    lib.oracle_detect_term.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_int, i32p, ctypes.c_int64]
+    lib.oracle_detect_term.restype = ctypes.c_double
+    lib.oracle_detect_sequence.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                           ctypes.c_int, i32p, ctypes.c_int, ctypes.c_int, i32p, f64p]
+    lib.oracle_detect_sequence.restype = ctypes.c_double
+    _lib_handle = lib
+    return lib
+
+
+def _u32(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.uint32))
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+
+
+def _i32(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _f32(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+# ---------------------------------------------------------------- primitives
+
+def philox(ctr, key):
+    """Philox4x32-10 block: 4 counter words, 2 key words -> 4 words."""
+    c, cp = _u32(ctr)
+    k, kp = _u32(key)
+    out, op = _u32(np.zeros(4, np.uint32))
+    _lib().oracle_philox(cp, kp, op)
+    return [int(x) for x in out]
+
+
+def fold(kappa, a, b, tag):
+    k, kp = _u32(kappa)
+    out, op = _u32(np.zeros(2, np.uint32))
+    _lib().oracle_fold(kp, a & 0xFFFFFFFF, b & 0xFFFFFFFF, tag & 0xFFFFFFFF, op)
+    return (int(out[0]), int(out[1]))
+
+
+def context_key(key: int, t: int, window) -> tuple:
+    """kappa = H(key, absolute position t, window of previous tokens, oldest first)."""
+    w, wp = _i32(window if len(window) else np.zeros(1, np.int32))
+    out, op = _u32(np.zeros(2, np.uint32))
+    _lib().oracle_context_key(ctypes.c_uint64(key & 0xFFFFFFFFFFFFFFFF), int(t), wp, len(window), op)
+    return (int(out[0]), int(out[1]))
+
+
+def uniform(word: int) -> float:
+    return _lib().oracle_uniform(word & 0xFFFFFFFF)
+
+
+def clocks(kappa, slot: int, V: int, layout: int = LAYOUT_TREE) -> np.ndarray:
+    """All V clocks E_slot[v] of the keyed source kappa (double)."""
+    k, kp = _u32(kappa)
+    out = np.empty(V, np.float64)
+    rc = _lib().oracle_clocks(kp, slot, V, layout, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise ValueError("oracle_clocks: bad arguments")
+    return out
+
+
+def clock(kappa, slot: int, V: int, v: int, layout: int = LAYOUT_TREE) -> float:
+    """One clock E_slot[v] (tree walk root -> token, or one flat word)."""
+    k, kp = _u32(kappa)
+    return _lib().oracle_clock(kp, slot, V, layout, v)
+
+
+def lse(logits, T: float) -> float:
+    x, xp = _f32(logits)
+    return _lib().oracle_lse(xp, x.size, T)
+
+
+def race(logits, T: float, kappa, slot0: int, nslots: int, layout: int = LAYOUT_TREE) -> dict:
+    """Exhaustive race of one row over slots [slot0, slot0+nslots)."""
+    x, xp = _f32(logits)
+    k, kp = _u32(kappa)
+    res = _RaceResult()
+    rc = _lib().oracle_race(xp, x.size, T, kp, slot0, nslots, layout, ctypes.byref(res))
+    if rc != 0:
+        raise ValueError("oracle_race failed (%d)" % rc)
+    return {"token": res.token, "slot": res.slot, "best": res.best, "second": res.second, "lse": res.lse}
+
+
+def token_score(logits, T: float, kappa, slot0: int, nslots: int, v: int, layout: int = LAYOUT_TREE) -> float:
+    """Score min_j ln E_j[v] - l_v/T of one token (used to classify near-ties)."""
+    x = float(np.float32(logits[v]))
+    if x == -np.inf:
+        return np.inf
+    e = min(clock(kappa, j, len(logits), v, layout) for j in range(slot0, slot0 + nslots))
+    return float(np.log(e) - np.float64(x) / np.float64(np.float32(T)))
+
+
+def detect_term(key: int, m: int, K: int, V: int, tokens, t: int, layout: int = LAYOUT_TREE) -> float:
+    tk, tp = _i32(tokens)
+    return _lib().oracle_detect_term(ctypes.c_uint64(key), m, K, V, layout, tp, int(t))
+
+
+def detect_sequence(key: int, m: int, K: int, V: int, tokens, n0: int, layout: int = LAYOUT_TREE):
+    """(S_A, M, per-token A_t) of one sequence, scored positions t in [n0, n)."""
+    tk, tp = _i32(tokens)
+    per = np.empty(tk.size, np.float64)
+    cnt = ctypes.c_int32(0)
+    S = _lib().oracle_detect_sequence(ctypes.c_uint64(key), m, K, V, layout, tp, tk.size, n0,
+                                      ctypes.byref(cnt), per.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    return S, int(cnt.value), per
+
+
+# ---------------------------------------------------------------- block level
+
+def window_of(prefix, path, m: int):
+    """Last m tokens of prefix || path, oldest first, padded with -1 in front."""
+    seq = list(prefix) + list(path)
+    w = seq[-m:] if m > 0 else []
+    return [-1] * (m - len(w)) + [int(a) for a in w]
+
+
+def walk(draft_tokens, chain, K: int, gamma: int, per_path: bool = False):
+    """Realised-path walk of one speculative block.
+
+    draft_tokens[k][s]: drafts of path k.  chain[s] (shared target rows) or
+    chain[k][s] (per-path target rows, the row of the lowest active path is read).
+    Emit the target token of the current depth; stop after it if it is not among
+    the drafts of the active paths (correction); otherwise narrow the active set to
+    the paths that drafted it.  All gamma accepted -> emit the bonus token.
+    Returns the emitted tokens (tau = len)."""
+    active = list(range(K))
+    out = []
+    for s in range(gamma):
+        y = int(chain[min(active)][s]) if per_path else int(chain[s])
+        out.append(y)
+        proposals = {int(draft_tokens[k][s]) for k in active}
+        if y < 0 or y not in proposals:
+            return out
+        active = [k for k in active if int(draft_tokens[k][s]) == y]
+    out.append(int(chain[min(active)][gamma]) if per_path else int(chain[gamma]))
+    return out
+
+
+def _check(tag, got, res, logits, T, kappa, slot0, nslots, layout, stats):
+    """Compare a GPU-chosen token with the oracle race: exact, near-tie or mismatch."""
+    if got == res["token"]:
+        stats["exact"] += 1
+        return
+    if res["token"] >= 0 and got >= 0:
+        s_got = token_score(logits, T, kappa, slot0, nslots, got, layout)
+        if s_got - res["best"] < NEAR_TIE:
+            stats["near_tie"] += 1
+            return
+    stats["mismatch"] += 1
+    stats["mismatches"].append((tag, got, res["token"], res["best"], res["second"]))
+
+
+def verify_block(*, key, K, gamma, m, T_target, T_draft, prefix, start_pos, target_logits,
+                 draft_logits=None, draft_tokens=None, target_rows=1, layout=LAYOUT_TREE,
+                 gpu=None, seqs=None):
+    """Oracle of one speculative block for sequences `seqs` (default all).
+
+    target_logits: float32 [B][gamma+1][V] (target_rows=1) or [B][K][gamma+1][V].
+    draft_logits:  float32 [B][K][gamma][V], or None when draft_tokens [B][K][gamma]
+    are given.  gpu: optional dict of the HIP results (draft_tokens, target_tokens,
+    out_tokens, out_len, target_lse, draft_lse); when given, every race is run in
+    the GPU's context (teacher forcing) and classified exact / near-tie / mismatch,
+    so a near-tie cannot derail the rest of the comparison.
+    Returns a dict with the oracle's tokens, LSEs and the comparison counts."""
+    B = target_logits.shape[0]
+    V = target_logits.shape[-1]
+    seqs = list(range(B)) if seqs is None else list(seqs)
+    stats = {"exact": 0, "near_tie": 0, "mismatch": 0, "mismatches": []}
+    out = {"draft_tokens": {}, "target_tokens": {}, "out_tokens": {}, "out_len": {},
+           "draft_lse": {}, "target_lse": {}, "stats": stats}
+    per_path = target_rows != 1
+    for b in range(B):
+        if b not in seqs:
+            continue
+        pre = [int(a) for a in prefix[b]]
+        t0 = int(start_pos[b])
+        # --- drafts: path k races slot k, sequential over depth
+        drafts = np.zeros((K, gamma), np.int64)
+        for k in range(K):
+            for s in range(gamma):
+                if draft_logits is None:
+                    drafts[k, s] = int(draft_tokens[b][k][s])
+                    continue
+                ctx_path = (gpu["draft_tokens"][b][k][:s] if gpu is not None else drafts[k, :s])
+                kappa = context_key(key, t0 + s, window_of(pre, ctx_path, m))
+                row = draft_logits[b][k][s]
+                res = race(row, T_draft, kappa, k, 1, layout)
+                out["draft_lse"][(b, k, s)] = res["lse"]
+                if gpu is not None:
+                    _check(("draft", b, k, s), int(gpu["draft_tokens"][b][k][s]), res, row, T_draft, kappa,
+                           k, 1, layout, stats)
+                    drafts[k, s] = int(gpu["draft_tokens"][b][k][s])
+                else:
+                    drafts[k, s] = res["token"]
+        out["draft_tokens"][b] = drafts
+        # --- target: all K slots; shared chain or one chain per path
+        chains = []
+        paths = range(K) if per_path else [None]
+        for k in paths:
+            chain = np.zeros(gamma + 1, np.int64)
+            for s in range(gamma + 1):
+                if per_path:
+                    ctx_path = drafts[k, :s]
+                    row = target_logits[b][k][s]
+                    gtok = None if gpu is None else int(gpu["target_tokens"][b][k][s])
+                else:
+                    ctx_path = (gpu["target_tokens"][b][:s] if gpu is not None else chain[:s])
+                    row = target_logits[b][s]
+                    gtok = None if gpu is None else int(gpu["target_tokens"][b][s])
+                kappa = context_key(key, t0 + s, window_of(pre, ctx_path, m))
+                res = race(row, T_target, kappa, 0, K, layout)
+                out["target_lse"][(b, k, s) if per_path else (b, s)] = res["lse"]
+                if gtok is not None:
+                    _check(("target", b, k, s), gtok, res, row, T_target, kappa, 0, K, layout, stats)
+                    chain[s] = gtok
+                else:
+                    chain[s] = res["token"]
+            chains.append(chain)
+        chain_arr = np.stack(chains) if per_path else chains[0]
+        out["target_tokens"][b] = chain_arr
+        emitted = walk(drafts, chain_arr, K, gamma, per_path)
+        out["out_tokens"][b] = emitted
+        out["out_len"][b] = len(emitted)
+    return out
