@@ -1,0 +1,254 @@
+// psd_api.cpp -- C ABI of libpsd: argument validation, workspace sizing and launches.
+// Every argument is checked before anything is enqueued; no exception crosses the ABI.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/psd.h"
+#include "psd_launch.hpp"
+#include "psd_layout.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+psd_status fail(psd_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+psd_status hip_fail(hipError_t e, const char* where) {
+    return fail(PSD_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+psd_status check_params(const psd_params* p) {
+    if (!p) return fail(PSD_E_ARG, "params is NULL");
+    if (p->vocab < 1 || p->vocab > PSD_MAX_VOCAB) return fail(PSD_E_ARG, "vocab %d outside [1, %d]", p->vocab, PSD_MAX_VOCAB);
+    if (p->num_drafts < 1 || p->num_drafts > PSD_MAX_DRAFTS)
+        return fail(PSD_E_ARG, "num_drafts %d outside [1, %d]", p->num_drafts, PSD_MAX_DRAFTS);
+    if (p->ctx_window < 0 || p->ctx_window > PSD_MAX_WINDOW)
+        return fail(PSD_E_ARG, "ctx_window %d outside [0, %d]", p->ctx_window, PSD_MAX_WINDOW);
+    if (!(p->temp_target > 0.f) || !isfinite(p->temp_target))
+        return fail(PSD_E_ARG, "temp_target must be finite and > 0");
+    if (!(p->temp_draft > 0.f) || !isfinite(p->temp_draft)) return fail(PSD_E_ARG, "temp_draft must be finite and > 0");
+    if (p->dtype != PSD_F32 && p->dtype != PSD_BF16) return fail(PSD_E_ARG, "unknown dtype %d", p->dtype);
+    if (p->clocks != PSD_CLOCKS_TREE && p->clocks != PSD_CLOCKS_FLAT)
+        return fail(PSD_E_ARG, "unknown clock layout %d", p->clocks);
+    if (p->mode == PSD_MODE_MPFR) return fail(PSD_E_UNSUPPORTED, "mode MPFR (identical drafters) is not implemented");
+    if (p->mode != PSD_MODE_HET) return fail(PSD_E_ARG, "unknown mode %d", p->mode);
+    return PSD_OK;
+}
+
+psd_status check_block(const psd_params* p, const psd_block* b) {
+    if (!b) return fail(PSD_E_ARG, "block is NULL");
+    if (b->batch < 1) return fail(PSD_E_ARG, "batch %d < 1", b->batch);
+    if (b->gamma < 1 || b->gamma > PSD_MAX_GAMMA) return fail(PSD_E_ARG, "gamma %d outside [1, %d]", b->gamma, PSD_MAX_GAMMA);
+    if (!b->start_pos) return fail(PSD_E_ARG, "start_pos is NULL");
+    if (p->ctx_window > 0 && !b->prefix_tokens) return fail(PSD_E_ARG, "prefix_tokens is NULL with ctx_window > 0");
+    const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
+    const long items = (long)L.n_rows * L.nseg;
+    if (items > 0x7FFFFFFFL) return fail(PSD_E_ARG, "block too large (%ld work items)", items);
+    if (!b->workspace) return fail(PSD_E_WORKSPACE, "workspace is NULL");
+    if (b->workspace_bytes < L.total)
+        return fail(PSD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", b->workspace_bytes, L.total);
+    if (((uintptr_t)b->workspace & 255u) != 0) return fail(PSD_E_WORKSPACE, "workspace must be 256-byte aligned");
+    return PSD_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+psd::RaceArgs base_args(const psd_params* p, const psd_block* b) {
+    psd::RaceArgs a;
+    memset(&a, 0, sizeof a);
+    a.prefix = b->prefix_tokens;
+    a.start_pos = b->start_pos;
+    a.ws = (unsigned char*)b->workspace;
+    a.L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
+    a.key = p->key;
+    a.V = p->vocab;
+    a.K = p->num_drafts;
+    a.m = p->ctx_window;
+    a.B = b->batch;
+    a.gamma = b->gamma;
+    a.T_target = p->temp_target;
+    a.T_draft = p->temp_draft;
+    a.inv_T_target = 1.0f / p->temp_target;
+    a.inv_T_draft = 1.0f / p->temp_draft;
+    return a;
+}
+
+// Depth-major item table: at depth d, draft rows (if d is drafted) then target rows.
+void build_depths(psd::RaceArgs& a, int n_depth) {
+    int first = 0;
+    a.n_depth = n_depth;
+    for (int d = 0; d < n_depth; ++d) {
+        const int nd = (a.s_count > 0 && d >= a.s_begin && d < a.s_begin + a.s_count) ? a.B * a.K : 0;
+        const int nt = (a.target_rows > 0 && d <= a.gamma) ? a.B * a.target_rows : 0;
+        a.depth_first[d] = first;
+        a.depth_nd[d] = nd;
+        a.depth_nt[d] = nt;
+        first += (nd + nt) * a.L.nseg;
+    }
+    a.n_items = first;
+}
+
+psd_status run_race(const psd_params* p, psd::RaceArgs& a, hipStream_t stream) {
+    const size_t es = p->dtype == PSD_BF16 ? 2 : 4;
+    bool vec = ((size_t)p->vocab * es) % 16 == 0;
+    if (a.draft_logits) vec = vec && aligned16(a.draft_logits);
+    if (a.target_logits) vec = vec && aligned16(a.target_logits);
+    hipError_t e = psd::launch_race(a, p->dtype == PSD_BF16, vec, p->clocks, stream);
+    if (e != hipSuccess) return hip_fail(e, "race kernel launch");
+    return PSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t psd_abi_version(void) { return PSD_ABI_VERSION; }
+
+const char* psd_last_error(void) { return g_err; }
+
+size_t psd_workspace_bytes(const psd_params* params, int32_t batch, int32_t gamma) {
+    if (!params || params->vocab < 1 || params->vocab > PSD_MAX_VOCAB || params->num_drafts < 1 ||
+        params->num_drafts > PSD_MAX_DRAFTS || batch < 1 || gamma < 1 || gamma > PSD_MAX_GAMMA ||
+        (params->dtype != PSD_F32 && params->dtype != PSD_BF16))
+        return 0;
+    return psd::ws_layout(batch, params->num_drafts, gamma, params->vocab, params->dtype == PSD_BF16).total;
+}
+
+psd_status psd_workspace_clear(void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!workspace) return fail(PSD_E_ARG, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(PSD_E_WORKSPACE, "workspace must be 256-byte aligned");
+    // The control region starts the workspace; clearing everything below the token slots of the
+    // largest layout that fits is enough, but clearing the whole buffer is simplest and cheap.
+    hipError_t e = psd::launch_fill_zero((uint32_t*)workspace, workspace_bytes / 4, stream);
+    if (e != hipSuccess) return hip_fail(e, "workspace clear");
+    return PSD_OK;
+}
+
+psd_status psd_workspace_errors(const void* workspace, hipStream_t stream, uint32_t* out_bits) {
+    if (!workspace || !out_bits) return fail(PSD_E_ARG, "NULL argument");
+    uint32_t ctrl[16];
+    hipError_t e = hipMemcpyAsync(ctrl, workspace, sizeof ctrl, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e, "workspace error read");
+    *out_bits = ctrl[2];
+    return PSD_OK;
+}
+
+psd_status psd_draft(const psd_params* params, const psd_block* block, int32_t s_begin, int32_t s_count,
+                     const void* draft_logits, int32_t* draft_tokens, float* draft_lse, hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    if ((st = check_block(params, block)) != PSD_OK) return st;
+    if (s_begin < 0 || s_count < 1 || s_begin + s_count > block->gamma)
+        return fail(PSD_E_ARG, "draft depths [%d, %d) outside [0, gamma=%d)", s_begin, s_begin + s_count, block->gamma);
+    if (!draft_logits) return fail(PSD_E_ARG, "draft_logits is NULL");
+    if (!draft_tokens) return fail(PSD_E_ARG, "draft_tokens is NULL");
+    psd::RaceArgs a = base_args(params, block);
+    a.draft_logits = draft_logits;
+    a.draft_tokens = draft_tokens;
+    a.draft_lse = draft_lse;
+    a.s_begin = s_begin;
+    a.s_count = s_count;
+    a.target_rows = 0;
+    build_depths(a, s_begin + s_count);
+    a.seq_rows = 0;
+    return run_race(params, a, stream);
+}
+
+psd_status psd_verify(const psd_params* params, const psd_block* block, int32_t target_rows,
+                      const void* target_logits, const void* draft_logits, int32_t* draft_tokens,
+                      int32_t* out_tokens, int32_t* out_len, float* target_lse, float* draft_lse,
+                      int32_t* target_tokens, hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    if ((st = check_block(params, block)) != PSD_OK) return st;
+    if (target_rows != 1 && target_rows != params->num_drafts)
+        return fail(PSD_E_ARG, "target_rows must be 1 or num_drafts (%d), got %d", params->num_drafts, target_rows);
+    if (!target_logits) return fail(PSD_E_ARG, "target_logits is NULL");
+    if (!draft_tokens) return fail(PSD_E_ARG, "draft_tokens is NULL");
+    if (!out_tokens || !out_len) return fail(PSD_E_ARG, "out_tokens / out_len is NULL");
+    if (!draft_logits && draft_lse) return fail(PSD_E_ARG, "draft_lse requires draft_logits");
+    psd::RaceArgs a = base_args(params, block);
+    a.target_logits = target_logits;
+    a.draft_logits = draft_logits;
+    a.draft_tokens = draft_tokens;
+    a.out_tokens = out_tokens;
+    a.out_len = out_len;
+    a.target_lse = target_lse;
+    a.draft_lse = draft_lse;
+    a.target_tokens = target_tokens;
+    a.s_begin = 0;
+    a.s_count = draft_logits ? block->gamma : 0;
+    a.target_rows = target_rows;
+    build_depths(a, block->gamma + 1);
+    a.seq_rows = a.K * a.s_count + target_rows * (block->gamma + 1);
+    return run_race(params, a, stream);
+}
+
+psd_status psd_detect(const psd_params* params, int32_t n_seq, int32_t seq_len, const int32_t* tokens,
+                      const int32_t* n0, double* out_score, int32_t* out_count, float* out_per_token,
+                      hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    if (n_seq < 0 || seq_len < 0) return fail(PSD_E_ARG, "negative n_seq / seq_len");
+    if (n_seq > 0 && (!tokens || !n0 || !out_score || !out_count))
+        return fail(PSD_E_ARG, "tokens / n0 / out_score / out_count is NULL");
+    psd::DetectArgs a;
+    a.tokens = tokens;
+    a.n0 = n0;
+    a.out_score = out_score;
+    a.out_count = out_count;
+    a.out_per_token = out_per_token;
+    a.key = params->key;
+    a.n_seq = n_seq;
+    a.seq_len = seq_len;
+    a.V = params->vocab;
+    a.K = params->num_drafts;
+    a.m = params->ctx_window;
+    hipError_t e = psd::launch_detect(a, params->clocks, stream);
+    if (e != hipSuccess) return hip_fail(e, "detect kernel launch");
+    return PSD_OK;
+}
+
+psd_status psd_philox(int32_t n, const uint32_t* ctr, const uint32_t* key, uint32_t* out, hipStream_t stream) {
+    if (n < 0) return fail(PSD_E_ARG, "n < 0");
+    if (n > 0 && (!ctr || !key || !out)) return fail(PSD_E_ARG, "NULL argument");
+    hipError_t e = psd::launch_philox(n, ctr, key, out, stream);
+    if (e != hipSuccess) return hip_fail(e, "philox kernel launch");
+    return PSD_OK;
+}
+
+psd_status psd_context_keys(const psd_params* params, int32_t n, const int64_t* t, const int32_t* windows,
+                            uint32_t* out_kappa, hipStream_t stream) {
+    if (!params) return fail(PSD_E_ARG, "params is NULL");
+    if (params->ctx_window < 0 || params->ctx_window > PSD_MAX_WINDOW) return fail(PSD_E_ARG, "bad ctx_window");
+    if (n < 0) return fail(PSD_E_ARG, "n < 0");
+    if (n > 0 && (!t || !out_kappa || (params->ctx_window > 0 && !windows))) return fail(PSD_E_ARG, "NULL argument");
+    hipError_t e = psd::launch_context_keys(params->key, params->ctx_window, n, t, windows, out_kappa, stream);
+    if (e != hipSuccess) return hip_fail(e, "context key kernel launch");
+    return PSD_OK;
+}
+
+psd_status psd_clock_values(const psd_params* params, int32_t n, const uint32_t* kappa, const int32_t* slot,
+                            const int32_t* token, double* out, hipStream_t stream) {
+    if (!params) return fail(PSD_E_ARG, "params is NULL");
+    if (params->vocab < 1 || params->vocab > PSD_MAX_VOCAB) return fail(PSD_E_ARG, "bad vocab");
+    if (params->clocks != PSD_CLOCKS_TREE && params->clocks != PSD_CLOCKS_FLAT) return fail(PSD_E_ARG, "bad clocks");
+    if (n < 0) return fail(PSD_E_ARG, "n < 0");
+    if (n > 0 && (!kappa || !slot || !token || !out)) return fail(PSD_E_ARG, "NULL argument");
+    hipError_t e = psd::launch_clock_values(params->clocks, params->vocab, n, kappa, slot, token, out, stream);
+    if (e != hipSuccess) return hip_fail(e, "clock kernel launch");
+    return PSD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,30 @@
+// psd_launch.hpp -- host-side launchers of the HIP kernels (internal to libpsd).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "psd_layout.hpp"
+
+namespace psd {
+
+struct DetectArgs {
+    const int32_t* tokens;  // [n_seq][seq_len]
+    const int32_t* n0;      // [n_seq]
+    double* out_score;      // [n_seq]
+    int32_t* out_count;     // [n_seq]
+    float* out_per_token;   // nullable [n_seq][seq_len]
+    uint64_t key;
+    int n_seq, seq_len, V, K, m;
+};
+
+hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
+size_t race_shared_bytes(int ng);
+hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream);
+hipError_t launch_philox(int n, const uint32_t* ctr, const uint32_t* key, uint32_t* out, hipStream_t stream);
+hipError_t launch_context_keys(uint64_t key, int m, int n, const int64_t* t, const int32_t* windows,
+                               uint32_t* out, hipStream_t stream);
+hipError_t launch_clock_values(int layout, int V, int n, const uint32_t* kappa, const int32_t* slot,
+                               const int32_t* token, double* out, hipStream_t stream);
+hipError_t launch_fill_zero(uint32_t* p, size_t n_words, hipStream_t stream);
+
+}  // namespace psd

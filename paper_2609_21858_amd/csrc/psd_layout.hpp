@@ -1,0 +1,89 @@
+// psd_layout.hpp -- workspace layout and kernel arguments of the fused race kernel
+// (host and device).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace psd {
+
+constexpr int kBlock = 256;             // threads per workgroup (4 wave64)
+constexpr int kSegTokensBf16 = 16384;   // tokens per work item: 32 KiB of bf16
+constexpr int kSegTokensF32 = 8192;     // 32 KiB of float32
+constexpr int kMaxDepth = 33;           // gamma + 1 <= 33
+
+inline int seg_tokens(int dtype_bf16) { return dtype_bf16 ? kSegTokensBf16 : kSegTokensF32; }
+
+// Row identifiers (independent of the call):
+//   draft (b, k, s)            : (b*K + k)*gamma + s
+//   target shared (b, s)       : D + b*(gamma+1) + s                 D = B*K*gamma
+//   target per path (b, k, s)  : D + (b*K + k)*(gamma+1) + s
+struct WsLayout {
+    size_t ctrl;     // uint32[16]: [0] ticket, [1] finished workgroups, [2] error bits
+    size_t row_cnt;  // uint32[n_rows]: finished segments per row
+    size_t flag;     // uint32[n_rows]: row token published
+    size_t seq_cnt;  // uint32[B]: finished rows per sequence
+    size_t ctrl_end; // [0, ctrl_end) is cleared after every call
+    size_t tok;      // int32[n_rows]: race winner per row
+    size_t part;     // float2[n_rows][nseg]: per-segment (max, sum) in log2 units
+    size_t gmax;     // float[n_rows][ng]: max logit of every 128-token group
+    size_t total;
+    int n_rows, nseg, ng;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline WsLayout ws_layout(int B, int K, int gamma, int V, int dtype_bf16) {
+    WsLayout L;
+    const long D = (long)B * K * gamma;
+    L.n_rows = (int)(D + (long)B * K * (gamma + 1));
+    L.nseg = (V + seg_tokens(dtype_bf16) - 1) / seg_tokens(dtype_bf16);
+    L.ng = (V + 127) / 128;
+    size_t o = 0;
+    L.ctrl = o;
+    o = align256(o + 16 * 4);
+    L.row_cnt = o;
+    o = align256(o + (size_t)L.n_rows * 4);
+    L.flag = o;
+    o = align256(o + (size_t)L.n_rows * 4);
+    L.seq_cnt = o;
+    o = align256(o + (size_t)B * 4);
+    L.ctrl_end = o;
+    L.tok = o;
+    o = align256(o + (size_t)L.n_rows * 4);
+    L.part = o;
+    o = align256(o + (size_t)L.n_rows * L.nseg * 8);
+    L.gmax = o;
+    o = align256(o + (size_t)L.n_rows * L.ng * 4);
+    L.total = o;
+    return L;
+}
+
+struct RaceArgs {
+    const void* draft_logits;   // [B][K][s_count][V] or null
+    const void* target_logits;  // [B][gamma+1][V] or [B][K][gamma+1][V] or null
+    const int32_t* prefix;      // [B][m]
+    const int64_t* start_pos;   // [B]
+    int32_t* draft_tokens;      // [B][K][gamma]
+    int32_t* out_tokens;        // [B][gamma+1] or null
+    int32_t* out_len;           // [B] or null
+    float* target_lse;          // nullable
+    float* draft_lse;           // nullable
+    int32_t* target_tokens;     // nullable
+    unsigned char* ws;          // workspace base
+    WsLayout L;
+    uint64_t key;
+    int V, K, m, B, gamma;
+    float T_target, T_draft;    // temperatures
+    float inv_T_target, inv_T_draft;
+    int s_begin, s_count;       // draft depths computed in this call (s_count = 0: none)
+    int target_rows;            // 0: no target rows, 1: shared, K: per path
+    int n_items;                // rows * nseg
+    int n_depth;
+    int depth_first[kMaxDepth]; // first item of depth d
+    int depth_nd[kMaxDepth];    // draft rows at depth d
+    int depth_nt[kMaxDepth];    // target rows at depth d
+    int seq_rows;               // rows per sequence in this call (walk trigger)
+};
+
+}  // namespace psd

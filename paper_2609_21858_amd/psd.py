@@ -1,0 +1,211 @@
+"""Thin ctypes binding of libpsd (the C ABI in include/psd.h).
+
+Argument marshalling only: every step of the sampler runs in the HIP kernels of
+libpsd.  PyTorch provides device memory and the current stream.  If the built
+library is missing, importing this module raises -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libpsd.so")
+
+PSD_OK, PSD_E_ARG, PSD_E_UNSUPPORTED, PSD_E_HIP, PSD_E_WORKSPACE = 0, -1, -2, -3, -4
+PSD_F32, PSD_BF16 = 0, 1
+PSD_MODE_HET, PSD_MODE_MPFR = 0, 1
+PSD_CLOCKS_TREE, PSD_CLOCKS_FLAT = 0, 1
+ERR_SPIN, ERR_CAND = 1, 2
+
+
+class PsdError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"psd status {status}: {msg}")
+        self.status = status
+
+
+class Params(ctypes.Structure):
+    _fields_ = [
+        ("key", ctypes.c_uint64),
+        ("vocab", ctypes.c_int32),
+        ("num_drafts", ctypes.c_int32),
+        ("ctx_window", ctypes.c_int32),
+        ("temp_target", ctypes.c_float),
+        ("temp_draft", ctypes.c_float),
+        ("dtype", ctypes.c_int32),
+        ("mode", ctypes.c_int32),
+        ("clocks", ctypes.c_int32),
+    ]
+
+
+class Block(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("gamma", ctypes.c_int32),
+        ("prefix_tokens", ctypes.c_void_p),
+        ("start_pos", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run __graft_entry__.build() (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER(Params)
+    Bp = ctypes.POINTER(Block)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    sigs = {
+        "psd_abi_version": ([], i32),
+        "psd_last_error": ([], ctypes.c_char_p),
+        "psd_workspace_bytes": ([P, i32, i32], sz),
+        "psd_workspace_clear": ([vp, sz, vp], i32),
+        "psd_workspace_errors": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], i32),
+        "psd_draft": ([P, Bp, i32, i32, vp, vp, vp, vp], i32),
+        "psd_verify": ([P, Bp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
+        "psd_detect": ([P, i32, i32, vp, vp, vp, vp, vp, vp], i32),
+        "psd_philox": ([i32, vp, vp, vp, vp], i32),
+        "psd_context_keys": ([P, i32, vp, vp, vp, vp], i32),
+        "psd_clock_values": ([P, i32, vp, vp, vp, vp, vp], i32),
+    }
+    for name, (args, res) in sigs.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    return lib
+
+
+_lib = _load()
+EXPORTS = ("psd_abi_version", "psd_last_error", "psd_workspace_bytes", "psd_workspace_clear",
+           "psd_workspace_errors", "psd_draft", "psd_verify", "psd_detect", "psd_philox", "psd_context_keys",
+           "psd_clock_values")
+
+
+def lib():
+    return _lib
+
+
+def _check(status: int):
+    if status != PSD_OK:
+        raise PsdError(status, (_lib.psd_last_error() or b"").decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def make_params(key: int, vocab: int, num_drafts: int, ctx_window: int, temp_target: float = 1.0,
+                temp_draft: float = 1.0, dtype=torch.bfloat16, mode: int = PSD_MODE_HET,
+                clocks: int = PSD_CLOCKS_TREE) -> Params:
+    dt = dtype if isinstance(dtype, int) else (PSD_BF16 if dtype == torch.bfloat16 else PSD_F32)
+    return Params(key & 0xFFFFFFFFFFFFFFFF, vocab, num_drafts, ctx_window, temp_target, temp_draft, dt, mode,
+                  clocks)
+
+
+def workspace_bytes(params: Params, batch: int, gamma: int) -> int:
+    return int(_lib.psd_workspace_bytes(ctypes.byref(params), batch, gamma))
+
+
+def new_workspace(params: Params, batch: int, gamma: int, device="cuda") -> torch.Tensor:
+    """Zero-filled device workspace (torch allocation, 256-byte aligned)."""
+    n = workspace_bytes(params, batch, gamma)
+    if n == 0:
+        raise PsdError(PSD_E_ARG, "invalid parameters for workspace sizing")
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def workspace_clear(ws: torch.Tensor, stream=None):
+    _check(_lib.psd_workspace_clear(_ptr(ws), ws.numel(), _stream(stream)))
+
+
+def workspace_errors(ws: torch.Tensor, stream=None) -> int:
+    out = ctypes.c_uint32(0)
+    _check(_lib.psd_workspace_errors(_ptr(ws), _stream(stream), ctypes.byref(out)))
+    return int(out.value)
+
+
+def _block(batch, gamma, prefix, start_pos, ws):
+    return Block(batch, gamma, prefix.data_ptr() if prefix is not None and prefix.numel() else None,
+                 start_pos.data_ptr(), ws.data_ptr(), ws.numel())
+
+
+def draft(params: Params, ws, prefix_tokens, start_pos, gamma: int, s_begin: int, draft_logits, draft_tokens,
+          draft_lse=None, stream=None):
+    """psd_draft: draft depths [s_begin, s_begin + draft_logits.shape[2])."""
+    B = int(start_pos.shape[0])
+    blk = _block(B, gamma, prefix_tokens, start_pos, ws)
+    _check(_lib.psd_draft(ctypes.byref(params), ctypes.byref(blk), s_begin, int(draft_logits.shape[2]),
+                          _ptr(draft_logits), _ptr(draft_tokens), _ptr(draft_lse), _stream(stream)))
+
+
+def verify(params: Params, ws, prefix_tokens, start_pos, target_logits, draft_logits=None, draft_tokens=None,
+           target_rows: int = 1, want_lse: bool = False, want_targets: bool = False, out=None, stream=None):
+    """psd_verify; allocates the outputs it is not given.  Returns a dict of tensors."""
+    B = int(start_pos.shape[0])
+    K = params.num_drafts
+    gamma = int(target_logits.shape[-2]) - 1
+    dev = target_logits.device
+    o = {} if out is None else dict(out)
+    if draft_tokens is None:
+        draft_tokens = torch.empty((B, K, gamma), dtype=torch.int32, device=dev)
+    o["draft_tokens"] = draft_tokens
+    o.setdefault("out_tokens", torch.empty((B, gamma + 1), dtype=torch.int32, device=dev))
+    o.setdefault("out_len", torch.empty((B,), dtype=torch.int32, device=dev))
+    tshape = (B, gamma + 1) if target_rows == 1 else (B, K, gamma + 1)
+    if want_lse:
+        o.setdefault("target_lse", torch.empty(tshape, dtype=torch.float32, device=dev))
+        if draft_logits is not None:
+            o.setdefault("draft_lse", torch.empty((B, K, gamma), dtype=torch.float32, device=dev))
+    if want_targets:
+        o.setdefault("target_tokens", torch.empty(tshape, dtype=torch.int32, device=dev))
+    blk = _block(B, gamma, prefix_tokens, start_pos, ws)
+    _check(_lib.psd_verify(ctypes.byref(params), ctypes.byref(blk), target_rows, _ptr(target_logits),
+                           _ptr(draft_logits), _ptr(draft_tokens), _ptr(o["out_tokens"]), _ptr(o["out_len"]),
+                           _ptr(o.get("target_lse")), _ptr(o.get("draft_lse")), _ptr(o.get("target_tokens")),
+                           _stream(stream)))
+    return o
+
+
+def detect(params: Params, tokens, n0, per_token: bool = False, stream=None):
+    """psd_detect -> (score f64 [n_seq], count i32 [n_seq], per-token f32 or None)."""
+    n_seq, seq_len = int(tokens.shape[0]), int(tokens.shape[1])
+    dev = tokens.device
+    score = torch.empty((n_seq,), dtype=torch.float64, device=dev)
+    count = torch.empty((n_seq,), dtype=torch.int32, device=dev)
+    per = torch.empty((n_seq, seq_len), dtype=torch.float32, device=dev) if per_token else None
+    _check(_lib.psd_detect(ctypes.byref(params), n_seq, seq_len, _ptr(tokens), _ptr(n0), _ptr(score), _ptr(count),
+                           _ptr(per), _stream(stream)))
+    return score, count, per
+
+
+def philox(ctr, key, stream=None):
+    n = int(ctr.shape[0])
+    out = torch.empty((n, 4), dtype=torch.int32, device=ctr.device)
+    _check(_lib.psd_philox(n, _ptr(ctr), _ptr(key), _ptr(out), _stream(stream)))
+    return out
+
+
+def context_keys(params: Params, t, windows, stream=None):
+    n = int(t.shape[0])
+    out = torch.empty((n, 2), dtype=torch.int32, device=t.device)
+    _check(_lib.psd_context_keys(ctypes.byref(params), n, _ptr(t), _ptr(windows) if windows is not None and
+                                 windows.numel() else None, _ptr(out), _stream(stream)))
+    return out
+
+
+def clock_values(params: Params, kappa, slot, token, stream=None):
+    n = int(slot.shape[0])
+    out = torch.empty((n,), dtype=torch.float64, device=slot.device)
+    _check(_lib.psd_clock_values(ctypes.byref(params), n, _ptr(kappa), _ptr(slot), _ptr(token), _ptr(out),
+                                 _stream(stream)))
+    return out

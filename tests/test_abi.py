@@ -1,0 +1,103 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function include/psd.h declares, and rejects invalid arguments before launching."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def psd():
+    from paper_2609_21858_amd import psd as m
+    return m
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "psd.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(psd_[a-z_]+)\s*\(", txt, re.M)))
+
+
+def test_library_exports_every_declared_symbol(psd):
+    names = _declared()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(psd.lib(), n), n
+        assert n in psd.EXPORTS
+    assert psd.lib().psd_abi_version() == 1
+
+
+def test_workspace_bytes(psd):
+    p = psd.make_params(1, 128256, 4, 4, 0.7, 0.7)
+    n = psd.workspace_bytes(p, 64, 4)
+    assert n > 0 and n % 256 == 0
+    assert psd.workspace_bytes(p, 128, 4) > n
+    bad = psd.make_params(1, 0, 4, 4)
+    assert psd.workspace_bytes(bad, 64, 4) == 0
+    assert psd.workspace_bytes(psd.make_params(1, 1 << 20, 4, 4), 1, 1) == 0
+    assert psd.workspace_bytes(p, 0, 4) == 0 and psd.workspace_bytes(p, 1, 33) == 0
+
+
+FAKE = 4096  # a non-NULL, 256-aligned dummy address: never dereferenced by rejected calls
+
+
+def _verify(psd, params, B=2, gamma=3, target_rows=1, ws_bytes=None, tl=FAKE, dt=FAKE, ot=FAKE, ol=FAKE,
+            sp=FAKE, pre=FAKE, ws=FAKE):
+    if ws_bytes is None:
+        ws_bytes = max(psd.workspace_bytes(params, B, gamma), 1)
+    blk = psd.Block(B, gamma, pre, sp, ws, ws_bytes)
+    return psd.lib().psd_verify(ctypes.byref(params), ctypes.byref(blk), target_rows, tl, None, dt, ot, ol, None,
+                                None, None, None)
+
+
+@pytest.mark.parametrize("field,value", [("vocab", 0), ("vocab", (1 << 19) + 1), ("num_drafts", 0),
+                                         ("num_drafts", 33), ("ctx_window", -1), ("ctx_window", 17),
+                                         ("temp_target", 0.0), ("temp_target", float("inf")),
+                                         ("temp_draft", -1.0), ("temp_draft", float("nan")), ("dtype", 2),
+                                         ("clocks", 5), ("mode", 7)])
+def test_verify_rejects_bad_params(psd, field, value):
+    p = psd.make_params(1, 1000, 2, 4)
+    setattr(p, field, value)
+    assert _verify(psd, p) == psd.PSD_E_ARG
+    assert psd.lib().psd_last_error()
+
+
+def test_verify_rejects_bad_block(psd):
+    p = psd.make_params(1, 1000, 2, 4)
+    assert _verify(psd, p, B=0) == psd.PSD_E_ARG
+    assert _verify(psd, p, gamma=0) == psd.PSD_E_ARG
+    assert _verify(psd, p, gamma=33) == psd.PSD_E_ARG
+    assert _verify(psd, p, sp=None) == psd.PSD_E_ARG
+    assert _verify(psd, p, pre=None) == psd.PSD_E_ARG
+    assert _verify(psd, p, tl=None) == psd.PSD_E_ARG
+    assert _verify(psd, p, dt=None) == psd.PSD_E_ARG
+    assert _verify(psd, p, ot=None) == psd.PSD_E_ARG
+    assert _verify(psd, p, target_rows=3) == psd.PSD_E_ARG
+    assert _verify(psd, p, ws=None) == psd.PSD_E_WORKSPACE
+    assert _verify(psd, p, ws_bytes=100) == psd.PSD_E_WORKSPACE
+    assert _verify(psd, p, ws=FAKE + 16) == psd.PSD_E_WORKSPACE
+    assert "workspace" in psd.lib().psd_last_error().decode()
+
+
+def test_mode_mpfr_unsupported(psd):
+    p = psd.make_params(1, 1000, 2, 4, mode=psd.PSD_MODE_MPFR)
+    assert _verify(psd, p) == psd.PSD_E_UNSUPPORTED
+
+
+def test_draft_and_detect_reject_bad_args(psd):
+    p = psd.make_params(1, 1000, 2, 4)
+    blk = psd.Block(2, 3, FAKE, FAKE, FAKE, psd.workspace_bytes(p, 2, 3))
+    L = psd.lib()
+    assert L.psd_draft(ctypes.byref(p), ctypes.byref(blk), -1, 1, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_draft(ctypes.byref(p), ctypes.byref(blk), 2, 2, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_draft(ctypes.byref(p), ctypes.byref(blk), 0, 0, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_draft(ctypes.byref(p), ctypes.byref(blk), 0, 1, None, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_detect(ctypes.byref(p), -1, 4, FAKE, FAKE, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_detect(ctypes.byref(p), 2, 4, None, FAKE, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_philox(-1, None, None, None, None) == psd.PSD_E_ARG
+    assert L.psd_philox(3, None, FAKE, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_context_keys(None, 1, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_clock_values(ctypes.byref(p), 2, None, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_workspace_clear(None, 16, None) == psd.PSD_E_ARG

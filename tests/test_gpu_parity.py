@@ -1,0 +1,294 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Token indices, accepted lengths and Philox words must match exactly, except
+near-ties (oracle score gap below 1e-6 in natural-log units, i.e. a relative gap
+of E/p below 1e-6), where either token is accepted and the comparison continues
+in the GPU's context.  Log-sum-exp and detection scores must agree within
+1e-5 * max(1, |value|).
+"""
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import oracle  # noqa: E402
+import workloads  # noqa: E402
+
+DEV = "cuda"
+LSE_TOL = 1e-5
+LAYOUTS = [0, 1]  # tree, flat
+
+
+@pytest.fixture(scope="module")
+def psd():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_21858_amd import psd as m
+    return m
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _sync():
+    torch.cuda.synchronize()
+
+
+def run_block(psd, w, seed, layout, target_rows=1, mode="fused", gen_device="cpu", seqs=None, blk=None):
+    """Run one verify call on the GPU and check it against the oracle on `seqs`."""
+    print(f"[parity] {w.name} V={w.V} K={w.K} g={w.gamma} B={w.B} {w.dtype} layout={layout} rows={target_rows} "
+          f"mode={mode} seed={seed}", flush=True)
+    if blk is None:
+        blk = workloads.make_block(w, seed, device=gen_device, target_rows=target_rows)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in blk.items()}
+    params = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype, clocks=layout)
+    ws = psd.new_workspace(params, w.B, w.gamma, DEV)
+    if mode == "fused":
+        out = psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], g["draft_logits"],
+                         target_rows=target_rows, want_lse=True, want_targets=True)
+    else:  # psd_draft per depth, then verify with the drafts given
+        dt = torch.full((w.B, w.K, w.gamma), -7, dtype=torch.int32, device=DEV)
+        dl = torch.empty((w.B, w.K, w.gamma), dtype=torch.float32, device=DEV)
+        for s in range(w.gamma):
+            psd.draft(params, ws, g["prefix_tokens"], g["start_pos"], w.gamma, s,
+                      g["draft_logits"][:, :, s:s + 1].contiguous(), dt, dl)
+        out = psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], None, dt,
+                         target_rows=target_rows, want_lse=True, want_targets=True)
+        out["draft_lse"] = dl
+    _sync()
+    assert psd.workspace_errors(ws) == 0
+    seqs = list(range(w.B)) if seqs is None else list(seqs)
+    gpu = {k: _np(v)[seqs] for k, v in out.items()}
+    tl = workloads.as_f32_numpy(blk["target_logits"][seqs])
+    dl = workloads.as_f32_numpy(blk["draft_logits"][seqs])
+    ref = oracle.verify_block(key=w.key, K=w.K, gamma=w.gamma, m=w.m, T_target=w.T_target, T_draft=w.T_draft,
+                              prefix=_np(blk["prefix_tokens"])[seqs], start_pos=_np(blk["start_pos"])[seqs],
+                              target_logits=tl, draft_logits=dl, target_rows=target_rows, layout=layout, gpu=gpu)
+    st = ref["stats"]
+    assert st["mismatch"] == 0, st["mismatches"][:5]
+    for i in range(len(seqs)):
+        n = int(gpu["out_len"][i])
+        assert n == ref["out_len"][i], (i, n, ref["out_len"][i])
+        assert list(gpu["out_tokens"][i][:n]) == ref["out_tokens"][i]
+        assert all(x == -1 for x in gpu["out_tokens"][i][n:])
+    for key, v in ref["target_lse"].items():
+        got = gpu["target_lse"][key] if target_rows == 1 else gpu["target_lse"][key[0]][key[1]][key[2]]
+        assert abs(got - v) <= LSE_TOL * max(1.0, abs(v)), (key, got, v)
+    for (b, k, s), v in ref["draft_lse"].items():
+        got = gpu["draft_lse"][b][k][s]
+        assert abs(got - v) <= LSE_TOL * max(1.0, abs(v)), ((b, k, s), got, v)
+    print(f"[parity]   exact={st['exact']} near_tie={st['near_tie']} mean_tau="
+          f"{np.mean([ref['out_len'][i] for i in range(len(seqs))]):.3f}", flush=True)
+    return out, ref
+
+
+# ---------------------------------------------------------------- keyed randomness
+
+def test_philox_words_bit_exact(psd):
+    rng = np.random.default_rng(1)
+    n = 4096
+    ctr = rng.integers(0, 2**32, (n, 4), dtype=np.uint64).astype(np.uint32)
+    key = rng.integers(0, 2**32, (n, 2), dtype=np.uint64).astype(np.uint32)
+    ctr[0] = 0
+    key[0] = 0
+    ctr[1] = 0xFFFFFFFF
+    key[1] = 0xFFFFFFFF
+    out = _np(psd.philox(torch.from_numpy(ctr.view(np.int32)).to(DEV), torch.from_numpy(key.view(np.int32)).to(DEV)))
+    out = out.view(np.uint32)
+    for i in range(0, n, 7):
+        assert list(out[i]) == oracle.philox(ctr[i], key[i]), i
+
+
+def test_context_keys_bit_exact(psd):
+    rng = np.random.default_rng(2)
+    for m in (0, 1, 4, 16):
+        n = 300
+        t = rng.integers(0, 2**40, n).astype(np.int64)
+        win = rng.integers(-1, 300000, (n, m)).astype(np.int32)
+        p = psd.make_params(0x0123456789ABCDEF, 1000, 2, m)
+        got = _np(psd.context_keys(p, torch.from_numpy(t).to(DEV), torch.from_numpy(win).to(DEV))).view(np.uint32)
+        for i in range(n):
+            assert tuple(int(x) for x in got[i]) == oracle.context_key(0x0123456789ABCDEF, int(t[i]), list(win[i]))
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("V", [1, 9, 1000, 128256, 1 << 19])
+def test_clock_values(psd, layout, V):
+    rng = np.random.default_rng(V + layout)
+    n = 2000
+    kappa = rng.integers(0, 2**32, (n, 2), dtype=np.uint64).astype(np.uint32)
+    slot = rng.integers(0, 32, n).astype(np.int32)
+    tok = rng.integers(0, V, n).astype(np.int32)
+    p = psd.make_params(1, V, 32, 0, clocks=layout)
+    got = _np(psd.clock_values(p, torch.from_numpy(kappa.view(np.int32)).to(DEV), torch.from_numpy(slot).to(DEV),
+                               torch.from_numpy(tok).to(DEV)))
+    for i in range(0, n, 3):
+        want = oracle.clock(kappa[i], int(slot[i]), V, int(tok[i]), layout)
+        assert abs(got[i] - want) <= 1e-13 * want, (i, got[i], want)
+
+
+# ---------------------------------------------------------------- full path, small configs
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_config1_fused(psd, layout):
+    for seed in range(6):
+        run_block(psd, workloads.WORKLOADS[1], seed, layout)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("case", [
+    dict(V=1000, K=3, gamma=4, B=3, dtype="fp32", m=4),   # ragged V (not a multiple of 8)
+    dict(V=777, K=2, gamma=2, B=2, dtype="bf16", m=0),    # ragged, no context window
+    dict(V=3, K=2, gamma=3, B=4, dtype="fp32", m=2),      # tiny vocabulary
+    dict(V=1, K=1, gamma=1, B=1, dtype="fp32", m=1),      # degenerate: one token
+    dict(V=4100, K=5, gamma=6, B=2, dtype="bf16", m=7),   # several groups + ragged tail
+    dict(V=33000, K=1, gamma=3, B=2, dtype="fp32", m=3),  # single draft, two level-4 nodes
+    dict(V=20000, K=7, gamma=2, B=3, dtype="bf16", m=16), # long window
+])
+def test_ragged_and_edge_shapes(psd, layout, case):
+    w = workloads.custom(case["V"], case["K"], case["gamma"], case["B"], dtype=case["dtype"], m=case["m"],
+                         tau=0.7, sigma=2.0, alpha=1.0)
+    run_block(psd, w, 11, layout)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_per_path_target_rows(psd, layout):
+    w = workloads.custom(3000, 3, 3, 4, dtype="bf16", m=3, tau=0.5, sigma=2.0, alpha=1.0)
+    run_block(psd, w, 5, layout, target_rows=3)
+    run_block(psd, w, 6, layout, target_rows=3, mode="two_call")
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_two_call_path_equals_fused(psd, layout):
+    w = workloads.custom(5000, 4, 4, 5, dtype="fp32", m=4, tau=0.6)
+    blk = workloads.make_block(w, 21)
+    a, _ = run_block(psd, w, 21, layout, blk=blk)
+    b, _ = run_block(psd, w, 21, layout, mode="two_call", blk=blk)
+    for k in ("draft_tokens", "out_tokens", "out_len", "target_tokens"):
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_temperatures_and_neg_inf(psd):
+    w = workloads.custom(2048, 3, 3, 3, dtype="fp32", m=2, T_target=0.3, T_draft=2.5)
+    blk = workloads.make_block(w, 4)
+    blk["target_logits"][0, 1, :2000] = -float("inf")   # a nearly empty row
+    blk["target_logits"][1, 2, :] = -float("inf")       # an empty target row -> -1, rejection
+    blk["draft_logits"][2, 0, 0, :] = -float("inf")     # an empty draft row -> -1
+    blk["draft_logits"][2, 1, 1, 100:] = -float("inf")
+    for layout in LAYOUTS:
+        out, ref = run_block(psd, w, 4, layout, blk=blk)
+        assert int(out["target_tokens"][1, 2]) == -1
+        assert int(out["draft_tokens"][2, 0, 0]) == -1
+        assert math.isinf(float(out["target_lse"][1, 2]))
+
+
+def test_determinism_and_workspace_reuse(psd):
+    w = workloads.custom(6000, 3, 3, 4, dtype="bf16", m=4)
+    blk = workloads.make_block(w, 8)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in blk.items()}
+    params = psd.make_params(w.key, w.V, w.K, w.m, dtype=torch.bfloat16)
+    ws = psd.new_workspace(params, 8, 5, DEV)  # larger than needed, reused
+    outs = []
+    for _ in range(3):
+        outs.append(psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], g["draft_logits"],
+                               want_lse=True, want_targets=True))
+    small = workloads.custom(6000, 3, 2, 2, dtype="bf16", m=4)
+    sb = workloads.make_block(small, 9)
+    sg = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in sb.items()}
+    psd.verify(params, ws, sg["prefix_tokens"], sg["start_pos"], sg["target_logits"], sg["draft_logits"])
+    outs.append(psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], g["draft_logits"],
+                           want_lse=True, want_targets=True))
+    _sync()
+    assert psd.workspace_errors(ws) == 0
+    for o in outs[1:]:
+        for k in o:
+            assert torch.equal(o[k], outs[0][k]), k
+
+
+# ---------------------------------------------------------------- full-size configs
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_config2_full(psd, layout):
+    run_block(psd, workloads.WORKLOADS[2], 2, layout)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_config3_full_sampled(psd, layout):
+    # both halves of the batch (draft noise 0.3 and 1.0), oracle on 4 sequences
+    run_block(psd, workloads.WORKLOADS[3], 3, layout, gen_device=DEV, seqs=[0, 17, 32, 63])
+
+
+def test_config4_full_sampled(psd):
+    run_block(psd, workloads.WORKLOADS[4], 4, 0, gen_device=DEV, seqs=[0, 127])
+
+
+def test_config5_full_sampled(psd):
+    run_block(psd, workloads.WORKLOADS[5], 5, 0, gen_device=DEV, seqs=[255])
+
+
+# ---------------------------------------------------------------- detection
+
+def _generate(psd, w, key, n_pos, seed, layout=0):
+    """Multi-block generation over a position-indexed toy LM with the GPU sampler."""
+    B, K, G, V = w.B, w.K, w.gamma, w.V
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(seed)
+    text = torch.randint(0, V, (B, w.m), generator=gen, device=DEV, dtype=torch.int64).to(torch.int32)
+    rows = workloads.target_rows_fp32(w, B * (n_pos + w.m + G + 2), gen, DEV)
+    rows = rows.view(B, n_pos + w.m + G + 2, V)
+    params = psd.make_params(key, V, K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype, clocks=layout)
+    ws = psd.new_workspace(params, B, G, DEV)
+    length = torch.full((B,), w.m, dtype=torch.int64, device=DEV)
+    buf = torch.full((B, w.m + n_pos + G + 1), -1, dtype=torch.int32, device=DEV)
+    buf[:, :w.m] = text
+    while int(length.min()) < w.m + n_pos:
+        idx = length.view(B, 1) + torch.arange(G + 1, device=DEV).view(1, G + 1)
+        tl = torch.gather(rows, 1, idx.view(B, G + 1, 1).expand(B, G + 1, V)).to(w.torch_dtype).contiguous()
+        dl = (tl[:, None, :G].float() + 0.8 * torch.randn((B, K, G, V), generator=gen, device=DEV)).to(w.torch_dtype)
+        prefix = torch.gather(buf, 1, length.view(B, 1) - w.m + torch.arange(w.m, device=DEV).view(1, w.m))
+        out = psd.verify(params, ws, prefix.contiguous(), length, tl, dl)
+        for b in range(B):
+            n = int(out["out_len"][b])
+            L0 = int(length[b])
+            if L0 >= w.m + n_pos:
+                continue
+            buf[b, L0:L0 + n] = out["out_tokens"][b, :n]
+            length[b] = L0 + n
+    return buf[:, :w.m + n_pos].contiguous()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_detect_parity_and_power(psd, layout):
+    w = workloads.custom(5000, 4, 4, 6, dtype="bf16", m=3, sigma=3.0, alpha=1.2)
+    key, wrong = 0x1111222233334444, 0x5555666677778888
+    wm = _generate(psd, w, key, 60, 1, layout)
+    nw = _generate(psd, w, wrong, 60, 2, layout)
+    toks = torch.cat([wm, nw], 0)
+    toks[0, 10] = 99999   # out of range: not scored
+    n0 = torch.full((toks.shape[0],), w.m, dtype=torch.int32, device=DEV)
+    n0[1] = 200           # nothing scored
+    p = psd.make_params(key, w.V, w.K, w.m, dtype=torch.bfloat16, clocks=layout)
+    score, count, per = psd.detect(p, toks, n0, per_token=True)
+    _sync()
+    score, count, per, tk = _np(score), _np(count), _np(per), _np(toks)
+    for i in range(tk.shape[0]):
+        S, M, ref_per = oracle.detect_sequence(key, w.m, w.K, w.V, tk[i], int(_np(n0)[i]), layout)
+        assert count[i] == M
+        assert abs(score[i] - S) <= LSE_TOL * max(1.0, abs(S)), (i, score[i], S)
+        ok = ~np.isnan(ref_per)
+        assert np.array_equal(np.isnan(per[i]), ~ok)
+        assert np.allclose(per[i][ok], ref_per[ok], rtol=1e-5, atol=1e-6)
+    # watermarked text scores far above its null mean M; the wrong key's does not
+    z = (score - count) / np.sqrt(np.maximum(count, 1))
+    assert np.all(z[[0, 2, 3, 4, 5]] > 3.0), z
+    assert np.all(np.abs(z[6:]) < 4.5), z
