@@ -193,6 +193,18 @@ __device__ __forceinline__ float row16_max(float x) {
     return x;
 }
 
+__device__ __forceinline__ float row16_min(float x) {
+    int v = __float_as_int(x);
+    x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false)));
+    v = __float_as_int(x);
+    x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false)));
+    v = __float_as_int(x);
+    x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false)));
+    v = __float_as_int(x);
+    x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false)));
+    return x;
+}
+
 // Order-preserving map float -> int (for integer atomic min on scores).
 __device__ __forceinline__ int ordered_key(float f) {
     const int i = __float_as_int(f);

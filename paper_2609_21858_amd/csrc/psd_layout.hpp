@@ -19,11 +19,11 @@ inline int seg_tokens(int dtype_bf16) { return dtype_bf16 ? kSegTokensBf16 : kSe
 //   target shared (b, s)       : D + b*(gamma+1) + s                 D = B*K*gamma
 //   target per path (b, k, s)  : D + (b*K + k)*(gamma+1) + s
 struct WsLayout {
-    size_t ctrl;     // uint32[16]: [0] ticket, [1] finished workgroups, [2] error bits
+    size_t ctrl;     // uint32[16]: [0] ticket, [1] finished workgroups, [2] error bits, [4] cleared flag
     size_t row_cnt;  // uint32[n_rows]: finished segments per row
     size_t flag;     // uint32[n_rows]: row token published
     size_t seq_cnt;  // uint32[B]: finished rows per sequence
-    size_t ctrl_end; // [0, ctrl_end) is cleared after every call
+    size_t ctrl_end; // [row_cnt, ctrl_end) is cleared at the start of every call
     size_t tok;      // int32[n_rows]: race winner per row
     size_t part;     // float2[n_rows][nseg]: per-segment (max, sum) in log2 units
     size_t gmax;     // float[n_rows][ng]: max logit of every 128-token group

@@ -94,6 +94,25 @@ __device__ __forceinline__ uint32_t* ctrl_of(const RaceArgs& a) { return (uint32
 
 __device__ __forceinline__ void set_error(const RaceArgs& a, uint32_t bit) { atomicOr(ctrl_of(a) + 2, bit); }
 
+// Cross-workgroup words (group maxima, LSE partials, tokens, flags, counters) are
+// only touched with relaxed device-scope atomics, which are coherent across the
+// XCDs without L2-wide write-back / invalidate.  Ordering between a producer's
+// data and its flag comes from waiting for its stores to complete (s_waitcnt)
+// before the flag is written; compiler fences keep the accesses in program order.
+template <typename T>
+__device__ __forceinline__ void st_dev(T* p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T ld_dev(const T* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void drain_memory() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ __forceinline__ int target_row_id(const RaceArgs& a, int b, int k, int s) {
     const int D = a.B * a.K * a.gamma;
     return a.target_rows == 1 ? D + b * (a.gamma + 1) + s : D + (b * a.K + k) * (a.gamma + 1) + s;
@@ -103,19 +122,24 @@ __device__ __forceinline__ int draft_row_id(const RaceArgs& a, int b, int k, int
     return (b * a.K + k) * a.gamma + s;
 }
 
-// Wait until row `rid` has published its token; returns it.
-__device__ int wait_token(const RaceArgs& a, int rid) {
-    const uint32_t* flag = (const uint32_t*)(a.ws + a.L.flag) + rid;
+// Bounded wait until *flag != 0 (acquire).  On timeout an error bit is recorded
+// and the caller proceeds, so every wave always terminates.
+__device__ void wait_nonzero(const RaceArgs& a, const uint32_t* flag) {
     for (uint32_t i = 0;; ++i) {
-        if (__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != 0u) break;
+        if (ld_dev(flag) != 0u) break;
         if (i >= kSpinLimit) {
             set_error(a, kErrSpin);
             break;
         }
         __builtin_amdgcn_s_sleep(4);
     }
-    const int32_t* tok = (const int32_t*)(a.ws + a.L.tok) + rid;
-    return __hip_atomic_load(tok, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    drain_memory();
+}
+
+// Wait until row `rid` has published its token; returns it.
+__device__ int wait_token(const RaceArgs& a, int rid) {
+    wait_nonzero(a, (const uint32_t*)(a.ws + a.L.flag) + rid);
+    return ld_dev((const int32_t*)(a.ws + a.L.tok) + rid);
 }
 
 // ---------------------------------------------------------------- logits access
@@ -179,7 +203,7 @@ __device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared&
         float um = fmaxf(fmaxf(fmaxf(x[q][0], x[q][1]), fmaxf(x[q][2], x[q][3])),
                          fmaxf(fmaxf(x[q][4], x[q][5]), fmaxf(x[q][6], x[q][7])));
         const float g = row16_max(um);
-        if ((tid & 15) == 0 && base < V) gmax_row[base >> 7] = g;
+        if ((tid & 15) == 0 && base < V) st_dev(gmax_row + (base >> 7), g);
         const float mn = fmaxf(mrun, um * c2);
         if (mn != -INFINITY) {
             float acc = (mrun == -INFINITY) ? 0.f : srun * __builtin_amdgcn_exp2f(mrun - mn);
@@ -204,8 +228,8 @@ __device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared&
     if (tid == 0) {
         float m = sm.red_a[0], s = sm.red_b[0];
         for (int w = 1; w < kBlock / 64; ++w) lse_combine(m, s, sm.red_a[w], sm.red_b[w]);
-        float2* part = (float2*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
-        part[seg] = make_float2(m, s);
+        unsigned long long* part = (unsigned long long*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
+        st_dev(part + seg, ((unsigned long long)__float_as_uint(s) << 32) | __float_as_uint(m));
     }
 }
 
@@ -223,7 +247,6 @@ __device__ __forceinline__ void push_node(Node* list, int* count, int cap, uint3
 }
 
 __device__ __forceinline__ void push_candidate(Shared& sm, const RaceArgs& a, int v, int j, float s) {
-    atomicMin(&sm.best_key, ordered_key(s));
     const int i = atomicAdd(&sm.n_cand, 1);
     if (i < kCandCap) {
         sm.cand_v[i] = v;
@@ -234,89 +257,120 @@ __device__ __forceinline__ void push_candidate(Shared& sm, const RaceArgs& a, in
     }
 }
 
-// Evaluate chunk c (8 tokens) of a listed group for one slot.
-template <bool BF16, int LAYOUT>
+// Evaluate chunk c (8 tokens) of a listed group for one slot.  The 16 lanes of a
+// DPP row hold the 16 chunks of one group entry; the entry-level test is uniform
+// over the row, and every lane of the row reaches the row minimum below, so only
+// tokens within the margin of the group's best score become candidates (any
+// token within the margin of the final best is within the margin of its group's).
+template <bool BF16, bool VEC, int LAYOUT>
 __device__ void eval_chunk(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, const Node nd, int c,
                            uint32_t k0, uint32_t k1) {
     const uint32_t slot = nd.id >> 20;
     const uint32_t g = nd.id & 0xFFFFFu;
     const uint32_t V = (uint32_t)a.V;
-    float thr = current_threshold(sm);
+    const float thr = current_threshold(sm);
     if (LAYOUT == 0 && ln_f32(nd.m) - gm[g] * r.invT > thr) return;
     if (LAYOUT == 1 && kLnClockFloor - gm[g] * r.invT > thr) return;
     const uint32_t base = g * kGroupTokens + (uint32_t)c * 8u;
-    if (base >= V) return;
-    float x[8];
-    load8<BF16, false>(r.ptr, (int)V, (int)base, x);
-    if constexpr (LAYOUT == 0) {
-        const uint32_t chunk = g * 16u + (uint32_t)c;
-        float mc;
-        uint32_t pc;
-        child_min_f32(nd.m, nd.p, 1, chunk, base, node_end(kShift1, chunk, V), slot, k0, k1, mc, pc);
-        const float cmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-        if (ln_f32(mc) - cmax * r.invT > thr) return;
-        const Words w0 = philox(chunk, slot, 8u, kDomainTree, k0, k1);
-        const Words w1 = philox(chunk, slot, 9u, kDomainTree, k0, k1);
-        const uint32_t ws[8] = {w0.w0, w0.w1, w0.w2, w0.w3, w1.w0, w1.w1, w1.w2, w1.w3};
+    float sc[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const uint32_t v = base + (uint32_t)i;
-            if (v >= V || x[i] == -INFINITY) continue;
-            const float E = (v == pc) ? mc : mc + exp1_f32(ws[i]);
-            const float s = ln_f32(E) - x[i] * r.invT;
-            if (s <= thr) {
-                push_candidate(sm, a, (int)v, (int)slot, s);
-                thr = fminf(thr, s + kMargin);
+    for (int i = 0; i < 8; ++i) sc[i] = INFINITY;
+    if (base < V) {
+        float x[8];
+        load8<BF16, VEC>(r.ptr, (int)V, (int)base, x);
+        if constexpr (LAYOUT == 0) {
+            const uint32_t chunk = g * 16u + (uint32_t)c;
+            float mc;
+            uint32_t pc;
+            child_min_f32(nd.m, nd.p, 1, chunk, base, node_end(kShift1, chunk, V), slot, k0, k1, mc, pc);
+            const float cmax =
+                fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+            if (ln_f32(mc) - cmax * r.invT <= thr) {
+                const Words w0 = philox(chunk, slot, 8u, kDomainTree, k0, k1);
+                const Words w1 = philox(chunk, slot, 9u, kDomainTree, k0, k1);
+                const uint32_t ws[8] = {w0.w0, w0.w1, w0.w2, w0.w3, w1.w0, w1.w1, w1.w2, w1.w3};
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const uint32_t v = base + (uint32_t)i;
+                    if (v < V && x[i] != -INFINITY) {
+                        const float E = (v == pc) ? mc : mc + exp1_f32(ws[i]);
+                        sc[i] = ln_f32(E) - x[i] * r.invT;
+                    }
+                }
             }
-        }
-    } else {
+        } else {
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            bool any = false;
+            for (int h = 0; h < 2; ++h) {
+                bool any = false;
 #pragma unroll
-            for (int i = 4 * h; i < 4 * h + 4; ++i)
-                any |= (base + (uint32_t)i < V) && (kLnClockFloor - x[i] * r.invT <= thr);
-            if (!any) continue;
-            const Words w = philox((base >> 2) + (uint32_t)h, slot, 0u, kDomainFlat, k0, k1);
-            const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
+                for (int i = 4 * h; i < 4 * h + 4; ++i)
+                    any |= (base + (uint32_t)i < V) && (kLnClockFloor - x[i] * r.invT <= thr);
+                if (!any) continue;
+                const Words w = philox((base >> 2) + (uint32_t)h, slot, 0u, kDomainFlat, k0, k1);
+                const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint32_t v = base + (uint32_t)(4 * h + i);
-                const float xv = x[4 * h + i];
-                if (v >= V || xv == -INFINITY) continue;
-                const float s = ln_f32(exp1_f32(ws[i])) - xv * r.invT;
-                if (s <= thr) {
-                    push_candidate(sm, a, (int)v, (int)slot, s);
-                    thr = fminf(thr, s + kMargin);
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t v = base + (uint32_t)(4 * h + i);
+                    const float xv = x[4 * h + i];
+                    if (v < V && xv != -INFINITY) sc[4 * h + i] = ln_f32(exp1_f32(ws[i])) - xv * r.invT;
                 }
             }
         }
     }
+    float lm = sc[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) lm = fminf(lm, sc[i]);
+    const float rm = row16_min(lm);
+    if (!(rm <= thr) || rm == INFINITY) return;
+    if (lm == rm) atomicMin(&sm.best_key, ordered_key(rm));
+    const float lim = fminf(thr, rm + kMargin);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        if (sc[i] <= lim && sc[i] < INFINITY) push_candidate(sm, a, (int)(base + (uint32_t)i), (int)slot, sc[i]);
 }
 
 // Evaluate every listed group (16 lanes per group, 16 groups per pass), then empty the list.
-template <bool BF16, int LAYOUT>
+template <bool BF16, bool VEC, int LAYOUT>
 __device__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0,
                              uint32_t k1) {
     const int tid = threadIdx.x;
     const int n = min(sm.n_l2, kL2Cap);
     for (int base = 0; base < n; base += kBlock / 16) {
         const int e = base + (tid >> 4);
-        if (e < n) eval_chunk<BF16, LAYOUT>(a, r, sm, gm, sm.l2[e], tid & 15, k0, k1);
+        if (e < n) eval_chunk<BF16, VEC, LAYOUT>(a, r, sm, gm, sm.l2[e], tid & 15, k0, k1);
+        __syncthreads();
+        if (tid == 0 && sm.n_cand > kCandCap / 2) {
+            // keep only candidates still within the margin of the best score
+            const float lim = ordered_value(sm.best_key) + kMargin;
+            const int nc = min(sm.n_cand, kCandCap);
+            int o = 0;
+            for (int i = 0; i < nc; ++i)
+                if (sm.cand_s[i] <= lim) {
+                    sm.cand_v[o] = sm.cand_v[i];
+                    sm.cand_j[o] = sm.cand_j[i];
+                    sm.cand_s[o] = sm.cand_s[i];
+                    ++o;
+                }
+            sm.n_cand = o;
+        }
+        __syncthreads();
     }
-    __syncthreads();
     if (tid == 0) sm.n_l2 = 0;
     __syncthreads();
 }
 
 // Expand listed level-3 nodes into level-2 groups (tree layout), evaluating groups as the list fills.
-template <bool BF16>
+template <bool BF16, bool VEC>
 __device__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
     const int tid = threadIdx.x;
     const int n = min(sm.n_l3, kL3Cap) * 16;
     const uint32_t V = (uint32_t)a.V;
     for (int base = 0; base < n; base += kBlock) {
-        if (sm.n_l2 > 0) flush_groups<BF16, 0>(a, r, sm, gm, k0, k1);
+        // Every thread reads the list count before any thread of this pass can push
+        // (otherwise waves could disagree on calling the barrier-bearing flush).
+        const bool flush = sm.n_l2 > 0;
+        __syncthreads();
+        if (flush) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
         const int e = base + tid;
         if (e < n) {
             const Node pa = sm.l3[e >> 4];
@@ -333,7 +387,8 @@ __device__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const floa
         }
         __syncthreads();
     }
-    if (sm.n_l2 > 0) flush_groups<BF16, 0>(a, r, sm, gm, k0, k1);
+    if (sm.n_l2 > 0) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
+    __syncthreads();
     if (tid == 0) sm.n_l3 = 0;
     __syncthreads();
 }
@@ -343,7 +398,7 @@ __device__ __forceinline__ bool lex_less(double s, int v, int j, double s2, int 
     return s < s2 || (s == s2 && (v < v2 || (v == v2 && j < j2)));
 }
 
-template <bool BF16, int LAYOUT>
+template <bool BF16, bool VEC, int LAYOUT>
 __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
     const int tid = threadIdx.x;
     const uint32_t V = (uint32_t)a.V;
@@ -356,7 +411,7 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
     __syncthreads();
 
     // (A) threshold from the group holding the row maximum, for every slot.
-    if (tid < ns) {
+    if (tid < ns && sm.gstar >= 0 && sm.gstar < ng) {
         const uint32_t slot = (uint32_t)(r.slot0 + tid);
         const uint32_t g = (uint32_t)sm.gstar;
         float m = 0.f;
@@ -372,9 +427,9 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
         }
         sm.l2[tid] = Node{(slot << 20) | g, m, p};
     }
-    if (tid == 0) sm.n_l2 = ns;
+    if (tid == 0) sm.n_l2 = (sm.gstar >= 0 && sm.gstar < ng) ? ns : 0;
     __syncthreads();
-    flush_groups<BF16, LAYOUT>(a, r, sm, gm, k0, k1);
+    flush_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, k0, k1);
 
     if constexpr (LAYOUT == 0) {
         // (B) tree descent: roots -> level 4 -> level 3 -> level 2 groups.
@@ -398,7 +453,9 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
         __syncthreads();
         const int n3tot = min(sm.n_l4, kL4Cap) * 16;
         for (int base = 0; base < n3tot; base += kBlock) {
-            if (sm.n_l3 + kBlock > kL3Cap) flush_l3<BF16>(a, r, sm, gm, k0, k1);
+            const bool flush = sm.n_l3 + kBlock > kL3Cap;
+            __syncthreads();
+            if (flush) flush_l3<BF16, VEC>(a, r, sm, gm, k0, k1);
             const int e = base + tid;
             if (e < n3tot) {
                 const Node pa = sm.l4[e >> 4];
@@ -415,12 +472,14 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
             }
             __syncthreads();
         }
-        flush_l3<BF16>(a, r, sm, gm, k0, k1);
+        flush_l3<BF16, VEC>(a, r, sm, gm, k0, k1);
     } else {
         // (B) flat clocks: every (group, slot) whose floor bound can win.
         const int tot = ng * ns;
         for (int base = 0; base < tot; base += kBlock) {
-            if (sm.n_l2 > 0) flush_groups<BF16, 1>(a, r, sm, gm, k0, k1);
+            const bool flush = sm.n_l2 > 0;
+            __syncthreads();
+            if (flush) flush_groups<BF16, VEC, 1>(a, r, sm, gm, k0, k1);
             const int e = base + tid;
             if (e < tot) {
                 const int g = e / ns;
@@ -430,7 +489,7 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
             }
             __syncthreads();
         }
-        flush_groups<BF16, 1>(a, r, sm, gm, k0, k1);
+        flush_groups<BF16, VEC, 1>(a, r, sm, gm, k0, k1);
     }
 
     // (C) exact decision among the candidates within the margin of the best.
@@ -489,7 +548,7 @@ __device__ void walk(const RaceArgs& a, int b) {
     bool done = false;
     for (int s = 0; s < G && !done; ++s) {
         const int kk = __ffs((int)act) - 1;
-        const int y = __hip_atomic_load(tok + target_row_id(a, b, kk, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int y = ld_dev(tok + target_row_id(a, b, kk, s));
         a.out_tokens[(size_t)b * (G + 1) + s] = y;
         tau = s + 1;
         if (y < 0) {
@@ -498,7 +557,7 @@ __device__ void walk(const RaceArgs& a, int b) {
         }
         uint32_t na = 0u;
         for (int k = 0; k < K; ++k)
-            if (((act >> k) & 1u) && a.draft_tokens[((size_t)b * K + k) * G + s] == y) na |= 1u << k;
+            if (((act >> k) & 1u) && ld_dev(a.draft_tokens + ((size_t)b * K + k) * G + s) == y) na |= 1u << k;
         if (!na) {
             done = true;
             break;
@@ -507,8 +566,7 @@ __device__ void walk(const RaceArgs& a, int b) {
     }
     if (!done) {
         const int kk = __ffs((int)act) - 1;
-        a.out_tokens[(size_t)b * (G + 1) + G] =
-            __hip_atomic_load(tok + target_row_id(a, b, kk, G), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        a.out_tokens[(size_t)b * (G + 1) + G] = ld_dev(tok + target_row_id(a, b, kk, G));
         tau = G + 1;
     }
     for (int s = tau; s <= G; ++s) a.out_tokens[(size_t)b * (G + 1) + s] = -1;
@@ -517,22 +575,28 @@ __device__ void walk(const RaceArgs& a, int b) {
 
 // ---------------------------------------------------------------- row finisher
 
-template <bool BF16, int LAYOUT>
+template <bool BF16, bool VEC, int LAYOUT>
 __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* gm) {
     const int tid = threadIdx.x;
     const int ng = a.L.ng;
     const int n3 = (ng + 15) / 16, n4 = (n3 + 15) / 16;
     const float* gsrc = (const float*)(a.ws + a.L.gmax) + (size_t)r.row_id * ng;
-    for (int g = tid; g < ng; g += kBlock) gm[g] = gsrc[g];
+    for (int g = tid; g < ng; g += kBlock) gm[g] = ld_dev(gsrc + g);
     if (tid == 0) {
         // LSE from the segment partials (log2 units), merged in double.
-        const float2* part = (const float2*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
-        double M = -INFINITY;
-        for (int i = 0; i < a.L.nseg; ++i) M = fmax(M, (double)part[i].x);
-        double S = 0.0;
-        if (M != -INFINITY)
-            for (int i = 0; i < a.L.nseg; ++i)
-                if (part[i].x != -INFINITY) S += (double)part[i].y * exp2((double)part[i].x - M);
+        const unsigned long long* part = (const unsigned long long*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
+        double M = -INFINITY, S = 0.0;
+        for (int i = 0; i < a.L.nseg; ++i) {
+            const unsigned long long bits = ld_dev(part + i);
+            const double pm = (double)__uint_as_float((uint32_t)bits), ps = (double)__uint_as_float((uint32_t)(bits >> 32));
+            if (pm == -INFINITY) continue;
+            if (pm > M) {
+                S = (M == -INFINITY ? 0.0 : S * exp2(M - pm)) + ps;
+                M = pm;
+            } else {
+                S += ps * exp2(pm - M);
+            }
+        }
         const double lse = M == -INFINITY ? -INFINITY : (M + log2(S)) * 0.69314718055994530942;
         if (r.kind == 0) {
             if (a.draft_lse) a.draft_lse[((size_t)r.b * a.K + r.k) * a.gamma + r.s] = (float)lse;
@@ -615,25 +679,27 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         }
         __syncthreads();
     } else {
-        race<BF16, LAYOUT>(a, r, sm, gm, k0, k1);
+        race<BF16, VEC, LAYOUT>(a, r, sm, gm, k0, k1);
     }
     if (tid == 0) {
         const int y = sm.win_token;
         if (r.kind == 0) {
-            a.draft_tokens[((size_t)r.b * a.K + r.k) * a.gamma + r.s] = y;
+            st_dev(a.draft_tokens + ((size_t)r.b * a.K + r.k) * a.gamma + r.s, y);
         } else if (a.target_tokens) {
             const size_t o = a.target_rows == 1 ? (size_t)r.b * (a.gamma + 1) + r.s
                                                 : ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + r.s;
             a.target_tokens[o] = y;
         }
-        int32_t* tok = (int32_t*)(a.ws + a.L.tok) + r.row_id;
-        __hip_atomic_store(tok, y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        uint32_t* flag = (uint32_t*)(a.ws + a.L.flag) + r.row_id;
-        __hip_atomic_store(flag, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        st_dev((int32_t*)(a.ws + a.L.tok) + r.row_id, y);
+        drain_memory();
+        st_dev((uint32_t*)(a.ws + a.L.flag) + r.row_id, 1u);
         if (a.target_rows > 0) {
             uint32_t* sc = (uint32_t*)(a.ws + a.L.seq_cnt) + r.b;
-            const uint32_t old = __hip_atomic_fetch_add(sc, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-            if ((int)old + 1 == a.seq_rows) walk(a, r.b);
+            const uint32_t old = __hip_atomic_fetch_add(sc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if ((int)old + 1 == a.seq_rows) {
+                drain_memory();
+                walk(a, r.b);
+            }
         }
     }
 }
@@ -649,11 +715,26 @@ __global__ __launch_bounds__(kBlock) void race_kernel(RaceArgs a) {
     uint32_t* ctrl = ctrl_of(a);
     const size_t esize = BF16 ? 2 : 4;
     const int D = a.B * a.K * a.gamma;
+    // Ticket 0 clears this call's row counters, flags and sequence counters (their
+    // placement depends on the call's shape, so a previous call with another shape
+    // may have left data there); every workgroup waits for that clear before its
+    // first counter update.  Tickets 1.. are the work items.
+    bool cleared = false;
     for (;;) {
-        if (tid == 0) sm.item = (int)atomicAdd(ctrl, 1u);
+        if (tid == 0) sm.item = (int)atomicAdd(ctrl, 1u) - 1;
         __syncthreads();
         const int item = sm.item;
         if (item >= a.n_items) break;
+        if (item < 0) {
+            uint32_t* base = (uint32_t*)(a.ws + a.L.row_cnt);
+            const size_t n = (a.L.ctrl_end - a.L.row_cnt) / 4;
+            for (size_t i = tid; i < n; i += kBlock) st_dev(base + i, 0u);
+            drain_memory();
+            __syncthreads();
+            if (tid == 0) st_dev(ctrl + 4, 1u);
+            cleared = true;
+            continue;
+        }
         int d = 0;
         while (d + 1 < a.n_depth && item >= a.depth_first[d + 1]) ++d;
         const int local = item - a.depth_first[d];
@@ -693,38 +774,28 @@ __global__ __launch_bounds__(kBlock) void race_kernel(RaceArgs a) {
             r.T = a.T_target;
         }
         stream_segment<BF16, VEC>(a, r, seg, sm);
-        __threadfence();
+        drain_memory();
         __syncthreads();
         if (tid == 0) {
+            if (!cleared) wait_nonzero(a, ctrl + 4);
             uint32_t* rc = (uint32_t*)(a.ws + a.L.row_cnt) + r.row_id;
-            const uint32_t old = __hip_atomic_fetch_add(rc, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+            const uint32_t old = __hip_atomic_fetch_add(rc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            drain_memory();
             sm.fin = ((int)old == a.L.nseg - 1);
         }
+        cleared = true;
         __syncthreads();
-        if (sm.fin) {
-            __threadfence();
-            finish_row<BF16, LAYOUT>(a, r, sm, gm);
-        }
+        if (sm.fin) finish_row<BF16, VEC, LAYOUT>(a, r, sm, gm);
         __syncthreads();
     }
-    // The last workgroup to leave clears the control words for the next call.
+    // The last workgroup to leave resets the fixed header words for the next call.
     if (tid == 0) {
-        __threadfence();
-        const uint32_t old = __hip_atomic_fetch_add(ctrl + 1, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        sm.last = (old == gridDim.x - 1);
-    }
-    __syncthreads();
-    if (sm.last) {
-        __threadfence();
-        uint32_t* base = (uint32_t*)(a.ws + a.L.row_cnt);
-        const size_t n = (a.L.ctrl_end - a.L.row_cnt) / 4;
-        for (size_t i = tid; i < n; i += kBlock) base[i] = 0u;
-        __threadfence();
-        __syncthreads();
-        if (tid == 0) {
-            ctrl[0] = 0u;
-            ctrl[1] = 0u;
-            __threadfence();
+        drain_memory();
+        const uint32_t old = __hip_atomic_fetch_add(ctrl + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == gridDim.x - 1) {
+            st_dev(ctrl + 0, 0u);
+            st_dev(ctrl + 1, 0u);
+            st_dev(ctrl + 4, 0u);
         }
     }
 }
