@@ -48,6 +48,42 @@ def measured_traffic(clocks: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def write_traffic(fetch_csv: str, write_csv: str, out: str = TRAFFIC_FILE) -> dict:
+    """HBM bytes per launch of the race kernel from two rocprofv3 --pmc runs of
+    `bench.py --pmc-copy-calibration` (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch).
+
+    Each counter is scaled by what it reads for the plain 1 GiB device copy that the
+    calibration run issues after the timed steps (1 GiB read, 1 GiB written)."""
+    import csv
+
+    def per_dispatch(path):
+        rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+        race = [r for r in rows if "race_kernel<" in r["Kernel_Name"]]
+        last = int(race[-1]["Dispatch_Id"])
+        copy = [r for r in rows if int(r["Dispatch_Id"]) > last and int(r["Grid_Size"]) >= 65536]
+        if not race or not copy:
+            raise SystemExit(f"{path}: no race_kernel or calibration copy dispatches")
+        kib = sum(float(r["Counter_Value"]) for r in race) / len(race)
+        cal = sum(float(r["Counter_Value"]) for r in copy) / len(copy)
+        clocks = "flat" if race[0]["Kernel_Name"].split("race_kernel<")[1].split(">")[0].endswith("1") else "tree"
+        return kib, cal, len(race), len(copy), clocks
+
+    fk, fc, fn, fcn, clocks = per_dispatch(fetch_csv)
+    wk, wc, wn, wcn, _ = per_dispatch(write_csv)
+    copy_kib = float(1 << 20)  # 1 GiB each way
+    f_scale, w_scale = copy_kib / fc, copy_kib / wc
+    rec = {"kernel": "race_kernel", "workload": "V=128256 K=4 gamma=4 B=64 bf16", "clocks": clocks,
+           "kernel_digest": kernel_digest(),
+           "fetch_kib_per_dispatch": fk, "write_kib_per_dispatch": wk,
+           "copy_fetch_kib": fc, "copy_write_kib": wc, "fetch_scale": f_scale, "write_scale": w_scale,
+           "race_dispatches": [fn, wn], "copy_dispatches": [fcn, wcn],
+           "hbm_bytes_per_launch": int(round((fk * f_scale + wk * w_scale) * 1024))}
+    with open(out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    return rec
+
+
 def cpu_baseline(blk, w, clocks_id, n_seq):
     import oracle
     import workloads
@@ -78,7 +114,12 @@ def main():
     ap.add_argument("--cpu-seqs", type=int, default=40)
     ap.add_argument("--pmc-copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for FETCH/WRITE_SIZE scaling)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the HBM traffic record from two rocprofv3 --pmc counter files and exit")
     args = ap.parse_args()
+    if args.traffic_from:
+        print(json.dumps(write_traffic(*args.traffic_from)))
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path has no "
               f"inter-GPU collectives.  Run with --gpus 1.", file=sys.stderr)

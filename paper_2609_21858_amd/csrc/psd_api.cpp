@@ -161,7 +161,6 @@ psd_status psd_draft(const psd_params* params, const psd_block* block, int32_t s
     a.s_count = s_count;
     a.target_rows = 0;
     build_depths(a, s_begin + s_count);
-    a.seq_rows = 0;
     return run_race(params, a, stream);
 }
 
@@ -191,7 +190,6 @@ psd_status psd_verify(const psd_params* params, const psd_block* block, int32_t 
     a.s_count = draft_logits ? block->gamma : 0;
     a.target_rows = target_rows;
     build_depths(a, block->gamma + 1);
-    a.seq_rows = a.K * a.s_count + target_rows * (block->gamma + 1);
     return run_race(params, a, stream);
 }
 

@@ -14,19 +14,27 @@ constexpr int kMaxDepth = 33;           // gamma + 1 <= 33
 
 inline int seg_tokens(int dtype_bf16) { return dtype_bf16 ? kSegTokensBf16 : kSegTokensF32; }
 
+// Control words at the start of every workspace (fixed positions for every call shape).
+constexpr int kCtrlTicket = 0;   // next work ticket
+constexpr int kCtrlExited = 1;   // workgroups that left the kernel
+constexpr int kCtrlErrors = 2;   // sticky error bits
+constexpr int kCtrlEpoch = 5;    // epoch of the last completed call (24 bits)
+
+// Every slot a call publishes carries that call's epoch (1 .. 2^24-1), so readers
+// detect fresh data by its tag and nothing needs clearing between calls:
+//   tok  : (epoch << 32) | uint32 token
+//   part : (epoch << 32) | float bits of the segment's sum of exp2 (relative to its max)
+//   gmax : (epoch << 40) | (argmax offset within the group << 32) | float bits of the max
+//
 // Row identifiers (independent of the call):
 //   draft (b, k, s)            : (b*K + k)*gamma + s
 //   target shared (b, s)       : D + b*(gamma+1) + s                 D = B*K*gamma
 //   target per path (b, k, s)  : D + (b*K + k)*(gamma+1) + s
 struct WsLayout {
-    size_t ctrl;     // uint32[16]: [0] ticket, [1] finished workgroups, [2] error bits, [4] cleared flag
-    size_t row_cnt;  // uint32[n_rows]: finished segments per row
-    size_t flag;     // uint32[n_rows]: row token published
-    size_t seq_cnt;  // uint32[B]: finished rows per sequence
-    size_t ctrl_end; // [row_cnt, ctrl_end) is cleared at the start of every call
-    size_t tok;      // int32[n_rows]: race winner per row
-    size_t part;     // float2[n_rows][nseg]: per-segment (max, sum) in log2 units
-    size_t gmax;     // float[n_rows][ng]: max logit of every 128-token group
+    size_t ctrl;  // uint32[64]
+    size_t tok;   // uint64[n_rows]
+    size_t part;  // uint64[n_rows][nseg]
+    size_t gmax;  // uint64[n_rows][ng]
     size_t total;
     int n_rows, nseg, ng;
 };
@@ -41,20 +49,13 @@ inline WsLayout ws_layout(int B, int K, int gamma, int V, int dtype_bf16) {
     L.ng = (V + 127) / 128;
     size_t o = 0;
     L.ctrl = o;
-    o = align256(o + 16 * 4);
-    L.row_cnt = o;
-    o = align256(o + (size_t)L.n_rows * 4);
-    L.flag = o;
-    o = align256(o + (size_t)L.n_rows * 4);
-    L.seq_cnt = o;
-    o = align256(o + (size_t)B * 4);
-    L.ctrl_end = o;
+    o = align256(o + 64 * 4);
     L.tok = o;
-    o = align256(o + (size_t)L.n_rows * 4);
+    o = align256(o + (size_t)L.n_rows * 8);
     L.part = o;
     o = align256(o + (size_t)L.n_rows * L.nseg * 8);
     L.gmax = o;
-    o = align256(o + (size_t)L.n_rows * L.ng * 4);
+    o = align256(o + (size_t)L.n_rows * L.ng * 8);
     L.total = o;
     return L;
 }
@@ -83,7 +84,6 @@ struct RaceArgs {
     int depth_first[kMaxDepth]; // first item of depth d
     int depth_nd[kMaxDepth];    // draft rows at depth d
     int depth_nt[kMaxDepth];    // target rows at depth d
-    int seq_rows;               // rows per sequence in this call (walk trigger)
 };
 
 }  // namespace psd

@@ -6,18 +6,22 @@
 // of a row are consecutive, so every row a race depends on holds lower tickets.
 //
 // Per segment (key-independent, HBM-streaming): coalesced 16-byte loads, the
-// online log-sum-exp partial (max, sum of exp2) and the maximum logit of every
-// 128-token group.  The workgroup that completes a row's last segment becomes the
-// row's finisher: it merges the LSE partials, waits for the token its context
-// needs (the previous depth of the same path or chain), folds the context key and
-// runs the keyed race over the row's group maxima:
+// online log-sum-exp partial (sum of exp2 relative to the segment maximum) and the
+// maximum logit of every 128-token group together with its position.  Each value
+// is published as one 64-bit slot tagged with the call's epoch, so nothing waits
+// for stores to drain and nothing is cleared between calls.  The workgroup that
+// holds a row's last segment becomes the row's finisher: it gathers the row's
+// slots, folds the context key (waiting only for the newest context token), runs
+// the keyed race, publishes the winner and -- for the last row of a sequence --
+// walks the block.
 //
-//  * TREE clocks: best-first by level.  A node's lower bound is
-//    ln(min clock of the node) - max logit / T; only nodes whose bound can still
-//    beat the best score found so far are expanded, and only the 128-token groups
-//    that survive are re-read from memory (a few per row).
-//  * FLAT clocks: every group whose bound ln(clock floor) - max logit / T can win
-//    is re-read and its surviving tokens draw their Philox word.
+// The race (TREE clocks): the argmax tokens of four top groups give achievable
+// scores; a level-by-level descent then expands only nodes whose lower bound
+// ln(min clock of the node) - max logit / T can still beat the best score; a
+// child's minimum is never below its parent's, so the parent's minimum bounds a
+// child before its own draw.  Only the 128-token groups that survive are re-read.
+// FLAT clocks: every group whose floor bound ln(clock floor) - max logit / T can
+// win is re-read and its surviving tokens draw their Philox word.
 //
 // Pruning and candidate scores run in float32 with a safety margin; every
 // candidate within the margin of the best is re-scored in float64 (clock rebuilt
@@ -40,12 +44,14 @@ namespace psd {
 
 namespace {
 
-constexpr int kL4Cap = 512;   // <= 32 slots x 16 level-4 nodes
+constexpr int kTopG = kBlock / 64;         // top groups seeding the threshold (one per wave)
+constexpr int kL4Cap = 512;                // <= 32 slots x 16 level-4 nodes
 constexpr int kL3Cap = 512;
-constexpr int kL2Cap = 256;
+constexpr int kL2Cap = 512;
 constexpr int kCandCap = 256;
+constexpr int kRowEntries = 1;             // group entries per 16-lane row per evaluation pass
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
-constexpr uint32_t kSpinLimit = 1u << 22;  // bounded dependency wait
+constexpr uint32_t kSpinLimit = 1u << 22;  // bounded waits for other workgroups' slots
 constexpr uint32_t kErrSpin = 1u, kErrCand = 2u;
 
 struct Node {
@@ -57,15 +63,17 @@ struct Node {
 struct Shared {
     float m3[256];
     float m4[16];
+    int topg[kTopG];
+    int topa[kTopG];
     Node l4[kL4Cap];
     Node l3[kL3Cap];
     Node l2[kL2Cap];
     int cand_v[kCandCap];
     int cand_j[kCandCap];
     float cand_s[kCandCap];
+    float cand_x[kCandCap];
     float root_m[32];
     uint32_t root_p[32];
-    int32_t window[16];
     double red_s[kBlock / 64];
     int red_v[kBlock / 64];
     int red_j[kBlock / 64];
@@ -73,9 +81,9 @@ struct Shared {
     float red_b[kBlock / 64];
     int n_l4, n_l3, n_l2, n_cand;
     int best_key;
-    int item, fin, last;
+    int tick[2];
+    uint32_t epoch;
     int win_token, win_slot;
-    int gstar;
     float rowmax;
     uint32_t kappa0, kappa1;
 };
@@ -92,13 +100,11 @@ struct Row {
 
 __device__ __forceinline__ uint32_t* ctrl_of(const RaceArgs& a) { return (uint32_t*)(a.ws + a.L.ctrl); }
 
-__device__ __forceinline__ void set_error(const RaceArgs& a, uint32_t bit) { atomicOr(ctrl_of(a) + 2, bit); }
+__device__ __forceinline__ void set_error(const RaceArgs& a, uint32_t bit) { atomicOr(ctrl_of(a) + kCtrlErrors, bit); }
 
-// Cross-workgroup words (group maxima, LSE partials, tokens, flags, counters) are
-// only touched with relaxed device-scope atomics, which are coherent across the
-// XCDs without L2-wide write-back / invalidate.  Ordering between a producer's
-// data and its flag comes from waiting for its stores to complete (s_waitcnt)
-// before the flag is written; compiler fences keep the accesses in program order.
+// Cross-workgroup slots are touched only with relaxed device-scope atomics, which
+// are coherent across the XCDs without L2-wide write-back / invalidate; each slot
+// carries its epoch, so a reader knows when the producer's value has landed.
 template <typename T>
 __device__ __forceinline__ void st_dev(T* p, T v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -107,10 +113,20 @@ template <typename T>
 __device__ __forceinline__ T ld_dev(const T* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void drain_memory() {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0);
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+
+// Bounded wait for a slot whose tag (bits >= shift) equals the epoch.  On timeout an
+// error bit is recorded and the stale value is returned, so every wave terminates.
+__device__ uint64_t wait_slot(const RaceArgs& a, const uint64_t* p, uint32_t epoch, int shift) {
+    uint64_t v = ld_dev(p);
+    for (uint32_t i = 0; (uint32_t)(v >> shift) != epoch; ++i) {
+        if (i >= kSpinLimit) {
+            set_error(a, kErrSpin);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        v = ld_dev(p);
+    }
+    return v;
 }
 
 __device__ __forceinline__ int target_row_id(const RaceArgs& a, int b, int k, int s) {
@@ -122,24 +138,8 @@ __device__ __forceinline__ int draft_row_id(const RaceArgs& a, int b, int k, int
     return (b * a.K + k) * a.gamma + s;
 }
 
-// Bounded wait until *flag != 0 (acquire).  On timeout an error bit is recorded
-// and the caller proceeds, so every wave always terminates.
-__device__ void wait_nonzero(const RaceArgs& a, const uint32_t* flag) {
-    for (uint32_t i = 0;; ++i) {
-        if (ld_dev(flag) != 0u) break;
-        if (i >= kSpinLimit) {
-            set_error(a, kErrSpin);
-            break;
-        }
-        __builtin_amdgcn_s_sleep(4);
-    }
-    drain_memory();
-}
-
-// Wait until row `rid` has published its token; returns it.
-__device__ int wait_token(const RaceArgs& a, int rid) {
-    wait_nonzero(a, (const uint32_t*)(a.ws + a.L.flag) + rid);
-    return ld_dev((const int32_t*)(a.ws + a.L.tok) + rid);
+__device__ __forceinline__ int wait_token(const RaceArgs& a, int rid, uint32_t epoch) {
+    return (int)(uint32_t)wait_slot(a, (const uint64_t*)(a.ws + a.L.tok) + rid, epoch, 32);
 }
 
 // ---------------------------------------------------------------- logits access
@@ -174,6 +174,52 @@ __device__ __forceinline__ void load8(const unsigned char* row, int V, int base,
     }
 }
 
+// Raw 16-byte words of one 8-token unit (bf16: one word, float32: two); -inf past V.
+template <bool BF16, bool VEC>
+struct Unit {
+    uint4 w[BF16 ? 1 : 2];
+};
+
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void load_unit(const unsigned char* row, int V, int base, Unit<BF16, VEC>& u) {
+    if constexpr (VEC) {
+        if constexpr (BF16) {
+            u.w[0] = make_uint4(0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u);
+            if (base < V) u.w[0] = *(const uint4*)((const uint16_t*)row + base);
+        } else {
+            u.w[0] = u.w[1] = make_uint4(0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u);
+            if (base < V) u.w[0] = *(const uint4*)((const float*)row + base);
+            if (base + 4 < V) u.w[1] = *(const uint4*)((const float*)row + base + 4);
+        }
+    } else {
+        float x[8];
+        load8<BF16, false>(row, V, base, x);
+        if constexpr (BF16) {
+            uint32_t p[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                p[i] = (__float_as_uint(x[2 * i]) >> 16) | (__float_as_uint(x[2 * i + 1]) & 0xFFFF0000u);
+            u.w[0] = make_uint4(p[0], p[1], p[2], p[3]);
+        } else {
+            u.w[0] = make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3]));
+            u.w[1] = make_uint4(__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]), __float_as_uint(x[7]));
+        }
+    }
+}
+
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void unpack_unit(const Unit<BF16, VEC>& u, float (&x)[8]) {
+    if constexpr (BF16) {
+        x[0] = bf16_lo(u.w[0].x); x[1] = bf16_hi(u.w[0].x); x[2] = bf16_lo(u.w[0].y); x[3] = bf16_hi(u.w[0].y);
+        x[4] = bf16_lo(u.w[0].z); x[5] = bf16_hi(u.w[0].z); x[6] = bf16_lo(u.w[0].w); x[7] = bf16_hi(u.w[0].w);
+    } else {
+        x[0] = __uint_as_float(u.w[0].x); x[1] = __uint_as_float(u.w[0].y);
+        x[2] = __uint_as_float(u.w[0].z); x[3] = __uint_as_float(u.w[0].w);
+        x[4] = __uint_as_float(u.w[1].x); x[5] = __uint_as_float(u.w[1].y);
+        x[6] = __uint_as_float(u.w[1].z); x[7] = __uint_as_float(u.w[1].w);
+    }
+}
+
 // ---------------------------------------------------------------- streaming pass
 
 __device__ __forceinline__ void lse_combine(float& m, float& s, float om, float os) {
@@ -184,31 +230,48 @@ __device__ __forceinline__ void lse_combine(float& m, float& s, float om, float 
     m = mn;
 }
 
-// One 32 KiB segment: group maxima -> gmax_row, (max, sum) of exp2(l * log2e / T) -> part_row[seg].
+// One 32 KiB segment: (max, argmax) of every 128-token group and the segment's sum
+// of exp2(l * log2e / T - M), M = log2e / T * (segment max).  Unless the
+// workgroup is about to finish a row (which can wait on other workgroups), thread 0
+// fetches its next ticket while the loads are in flight: a ticket held through such
+// a wait would stall the rows that need that segment.
 template <bool BF16, bool VEC>
-__device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared& sm) {
+__device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared& sm, int parity, bool prefetch) {
     constexpr int NU = BF16 ? 8 : 4;  // 8-token units per lane
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
     const int V = a.V;
     const int seg0 = seg * (BF16 ? kSegTokensBf16 : kSegTokensF32);
-    float* gmax_row = (float*)(a.ws + a.L.gmax) + (size_t)r.row_id * a.L.ng;
+    const uint64_t ep = sm.epoch;
+    uint64_t* gslot = (uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * a.L.ng;
     const float c2 = r.invT * 1.4426950408889634f;
-    float x[NU][8];
+    Unit<BF16, VEC> u[NU];
 #pragma unroll
-    for (int q = 0; q < NU; ++q) load8<BF16, VEC>(r.ptr, V, seg0 + 8 * (q * kBlock + tid), x[q]);
+    for (int q = 0; q < NU; ++q) load_unit<BF16, VEC>(r.ptr, V, seg0 + 8 * (q * kBlock + tid), u[q]);
+    if (tid == 0 && prefetch) sm.tick[parity ^ 1] = (int)atomicAdd(ctrl_of(a) + kCtrlTicket, 1u);
     float mrun = -INFINITY, srun = 0.f;
 #pragma unroll
     for (int q = 0; q < NU; ++q) {
         const int base = seg0 + 8 * (q * kBlock + tid);
-        float um = fmaxf(fmaxf(fmaxf(x[q][0], x[q][1]), fmaxf(x[q][2], x[q][3])),
-                         fmaxf(fmaxf(x[q][4], x[q][5]), fmaxf(x[q][6], x[q][7])));
+        float x[8];
+        unpack_unit<BF16, VEC>(u[q], x);
+        const float um = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
         const float g = row16_max(um);
-        if ((tid & 15) == 0 && base < V) st_dev(gmax_row + (base >> 7), g);
+        // the lowest lane of the 16-lane row holding the maximum publishes (max, position)
+        const uint64_t holders = __ballot(um == g);
+        const uint32_t rowbits = (uint32_t)(holders >> (lane & 48)) & 0xFFFFu;
+        if ((uint32_t)(lane & 15) == (uint32_t)(__ffs(rowbits) - 1) && base < V) {
+            int i = 0;
+#pragma unroll
+            for (int t = 7; t >= 0; --t)
+                if (x[t] == g) i = t;
+            const uint64_t off = (uint64_t)((lane & 15) * 8 + i);
+            st_dev(gslot + (base >> 7), (ep << 40) | (off << 32) | __float_as_uint(g));
+        }
         const float mn = fmaxf(mrun, um * c2);
         if (mn != -INFINITY) {
             float acc = (mrun == -INFINITY) ? 0.f : srun * __builtin_amdgcn_exp2f(mrun - mn);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc += __builtin_amdgcn_exp2f(fmaf(x[q][i], c2, -mn));
+            for (int i = 0; i < 8; ++i) acc += __builtin_amdgcn_exp2f(fmaf(x[i], c2, -mn));
             srun = acc;
             mrun = mn;
         }
@@ -220,7 +283,7 @@ __device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared&
         lse_combine(mrun, srun, om, os);
     }
     const int wave = tid >> 6;
-    if ((tid & 63) == 0) {
+    if (lane == 0) {
         sm.red_a[wave] = mrun;
         sm.red_b[wave] = srun;
     }
@@ -228,8 +291,8 @@ __device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared&
     if (tid == 0) {
         float m = sm.red_a[0], s = sm.red_b[0];
         for (int w = 1; w < kBlock / 64; ++w) lse_combine(m, s, sm.red_a[w], sm.red_b[w]);
-        unsigned long long* part = (unsigned long long*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
-        st_dev(part + seg, ((unsigned long long)__float_as_uint(s) << 32) | __float_as_uint(m));
+        uint64_t* part = (uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
+        st_dev(part + seg, (ep << 32) | __float_as_uint(s));
     }
 }
 
@@ -240,149 +303,175 @@ __device__ __forceinline__ float current_threshold(Shared& sm) {
            kMargin;
 }
 
-__device__ __forceinline__ void push_node(Node* list, int* count, int cap, uint32_t id, float m, uint32_t p,
-                                          const RaceArgs& a) {
+__device__ __forceinline__ void push_node(Node* list, int* count, int cap, uint32_t id, float m, uint32_t p) {
     const int i = atomicAdd(count, 1);
     if (i < cap) list[i] = Node{id, m, p};
 }
 
-__device__ __forceinline__ void push_candidate(Shared& sm, const RaceArgs& a, int v, int j, float s) {
+__device__ __forceinline__ void push_candidate(Shared& sm, const RaceArgs& a, int v, int j, float s, float x) {
     const int i = atomicAdd(&sm.n_cand, 1);
     if (i < kCandCap) {
         sm.cand_v[i] = v;
         sm.cand_j[i] = j;
         sm.cand_s[i] = s;
+        sm.cand_x[i] = x;
     } else {
         set_error(a, kErrCand);
     }
 }
 
-// Evaluate chunk c (8 tokens) of a listed group for one slot.  The 16 lanes of a
-// DPP row hold the 16 chunks of one group entry; the entry-level test is uniform
-// over the row, and every lane of the row reaches the row minimum below, so only
-// tokens within the margin of the group's best score become candidates (any
-// token within the margin of the final best is within the margin of its group's).
+// Keep only candidates within the margin of the current best (thread 0, between barriers).
+__device__ __forceinline__ void compact_candidates(Shared& sm) {
+    if (sm.n_cand <= kCandCap / 2) return;
+    const float lim = ordered_value(sm.best_key) + kMargin;
+    const int nc = min(sm.n_cand, kCandCap);
+    int o = 0;
+    for (int i = 0; i < nc; ++i)
+        if (sm.cand_s[i] <= lim) {
+            sm.cand_v[o] = sm.cand_v[i];
+            sm.cand_j[o] = sm.cand_j[i];
+            sm.cand_s[o] = sm.cand_s[i];
+            sm.cand_x[o] = sm.cand_x[i];
+            ++o;
+        }
+    sm.n_cand = o;
+}
+
+// Evaluate listed group entries [first, first + n): 16 lanes hold the 16 chunks of
+// one entry; each row takes kRowEntries entries, whose loads are issued together.
+// A chunk and its token words are drawn together when any of its tokens can still
+// win against the group minimum (chunk and token minima are never below it).
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ void eval_chunk(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, const Node nd, int c,
-                           uint32_t k0, uint32_t k1) {
-    const uint32_t slot = nd.id >> 20;
-    const uint32_t g = nd.id & 0xFFFFFu;
+__device__ void eval_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, int first, int n,
+                            uint32_t k0, uint32_t k1) {
+    const int tid = threadIdx.x;
+    const int c = tid & 15;
+    const int row = tid >> 4;  // 16 rows of 16 lanes
     const uint32_t V = (uint32_t)a.V;
-    const float thr = current_threshold(sm);
-    if (LAYOUT == 0 && ln_f32(nd.m) - gm[g] * r.invT > thr) return;
-    if (LAYOUT == 1 && kLnClockFloor - gm[g] * r.invT > thr) return;
-    const uint32_t base = g * kGroupTokens + (uint32_t)c * 8u;
-    float sc[8];
+    float x[kRowEntries][8];
+    Node nd[kRowEntries];
+    bool act[kRowEntries];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) sc[i] = INFINITY;
-    if (base < V) {
-        float x[8];
-        load8<BF16, VEC>(r.ptr, (int)V, (int)base, x);
-        if constexpr (LAYOUT == 0) {
-            const uint32_t chunk = g * 16u + (uint32_t)c;
-            float mc;
-            uint32_t pc;
-            child_min_f32(nd.m, nd.p, 1, chunk, base, node_end(kShift1, chunk, V), slot, k0, k1, mc, pc);
-            const float cmax =
-                fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-            if (ln_f32(mc) - cmax * r.invT <= thr) {
-                const Words w0 = philox(chunk, slot, 8u, kDomainTree, k0, k1);
-                const Words w1 = philox(chunk, slot, 9u, kDomainTree, k0, k1);
+    for (int q = 0; q < kRowEntries; ++q) {
+        const int e = first + row * kRowEntries + q;
+        act[q] = e < first + n;
+        nd[q] = act[q] ? sm.l2[e] : Node{0u, 0.f, 0u};
+        const uint32_t g = nd[q].id & 0xFFFFFu;
+        load8<BF16, VEC>(r.ptr, act[q] ? (int)V : 0, (int)(g * kGroupTokens + (uint32_t)c * 8u), x[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < kRowEntries; ++q) {
+        if (!act[q]) continue;  // uniform over the 16-lane row
+        const uint32_t slot = nd[q].id >> 20;
+        const uint32_t g = nd[q].id & 0xFFFFFu;
+        const float thr = current_threshold(sm);
+        const float lnm = LAYOUT == 0 ? ln_f32(nd[q].m) : kLnClockFloor;
+        if (lnm - gm[g] * r.invT > thr) continue;  // uniform over the row
+        const uint32_t base = g * kGroupTokens + (uint32_t)c * 8u;
+        float sc[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sc[i] = INFINITY;
+        bool need[2] = {false, false};
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (base + (uint32_t)i < V && lnm - x[q][i] * r.invT <= thr) need[i >> 2] = true;
+        if (need[0] || need[1]) {
+            if constexpr (LAYOUT == 0) {
+                const uint32_t chunk = g * 16u + (uint32_t)c;
+                const uint32_t ce = node_end(kShift1, chunk, V);
+                // chunk draw and token words are independent Philox calls: issue together
+                const bool inherit = nd[q].p >= base && nd[q].p < ce;
+                Words wc = Words{0u, 0u, 0u, 0u}, w0 = wc, w1 = wc;
+                if (!inherit) wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
+                if (need[0]) w0 = philox(chunk, slot, 8u, kDomainTree, k0, k1);
+                if (need[1]) w1 = philox(chunk, slot, 9u, kDomainTree, k0, k1);
+                float mc = nd[q].m;
+                uint32_t pc = nd[q].p;
+                if (!inherit) {
+                    mc = nd[q].m + exp1_f32(wc.w0) / (float)(ce - base);
+                    pc = base + uniform_position(wc.w1, wc.w2, ce - base);
+                }
+                const float lnmc = ln_f32(mc);
                 const uint32_t ws[8] = {w0.w0, w0.w1, w0.w2, w0.w3, w1.w0, w1.w1, w1.w2, w1.w3};
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
                     const uint32_t v = base + (uint32_t)i;
-                    if (v < V && x[i] != -INFINITY) {
-                        const float E = (v == pc) ? mc : mc + exp1_f32(ws[i]);
-                        sc[i] = ln_f32(E) - x[i] * r.invT;
+                    if (v >= V || x[q][i] == -INFINITY || !need[i >> 2]) continue;
+                    if (v == pc)
+                        sc[i] = lnmc - x[q][i] * r.invT;
+                    else if (lnmc - x[q][i] * r.invT <= thr)
+                        sc[i] = ln_f32(mc + exp1_f32(ws[i])) - x[q][i] * r.invT;
+                }
+            } else {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    if (!need[h]) continue;
+                    const Words w = philox((base >> 2) + (uint32_t)h, slot, 0u, kDomainFlat, k0, k1);
+                    const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int t = 4 * h + i;
+                        if (base + (uint32_t)t < V && x[q][t] != -INFINITY)
+                            sc[t] = ln_f32(exp1_f32(ws[i])) - x[q][t] * r.invT;
                     }
                 }
             }
-        } else {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                bool any = false;
-#pragma unroll
-                for (int i = 4 * h; i < 4 * h + 4; ++i)
-                    any |= (base + (uint32_t)i < V) && (kLnClockFloor - x[i] * r.invT <= thr);
-                if (!any) continue;
-                const Words w = philox((base >> 2) + (uint32_t)h, slot, 0u, kDomainFlat, k0, k1);
-                const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const uint32_t v = base + (uint32_t)(4 * h + i);
-                    const float xv = x[4 * h + i];
-                    if (v < V && xv != -INFINITY) sc[4 * h + i] = ln_f32(exp1_f32(ws[i])) - xv * r.invT;
-                }
-            }
         }
+        float lm = sc[0];
+#pragma unroll
+        for (int i = 1; i < 8; ++i) lm = fminf(lm, sc[i]);
+        const float rm = row16_min(lm);  // every lane of the row reaches this point
+        if (!(rm <= thr) || rm == INFINITY) continue;
+        if (lm == rm) atomicMin(&sm.best_key, ordered_key(rm));
+        const float lim = fminf(thr, rm + kMargin);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (sc[i] <= lim && sc[i] < INFINITY)
+                push_candidate(sm, a, (int)(base + (uint32_t)i), (int)slot, sc[i], x[q][i]);
     }
-    float lm = sc[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) lm = fminf(lm, sc[i]);
-    const float rm = row16_min(lm);
-    if (!(rm <= thr) || rm == INFINITY) return;
-    if (lm == rm) atomicMin(&sm.best_key, ordered_key(rm));
-    const float lim = fminf(thr, rm + kMargin);
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        if (sc[i] <= lim && sc[i] < INFINITY) push_candidate(sm, a, (int)(base + (uint32_t)i), (int)slot, sc[i]);
 }
 
-// Evaluate every listed group (16 lanes per group, 16 groups per pass), then empty the list.
+// Evaluate and empty the group list.  Callers read the list count after a barrier
+// and before any push of the current pass.
 template <bool BF16, bool VEC, int LAYOUT>
 __device__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0,
                              uint32_t k1) {
-    const int tid = threadIdx.x;
     const int n = min(sm.n_l2, kL2Cap);
-    for (int base = 0; base < n; base += kBlock / 16) {
-        const int e = base + (tid >> 4);
-        if (e < n) eval_chunk<BF16, VEC, LAYOUT>(a, r, sm, gm, sm.l2[e], tid & 15, k0, k1);
+    for (int first = 0; first < n; first += 16 * kRowEntries) {
+        eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, 16 * kRowEntries), k0, k1);
         __syncthreads();
-        if (tid == 0 && sm.n_cand > kCandCap / 2) {
-            // keep only candidates still within the margin of the best score
-            const float lim = ordered_value(sm.best_key) + kMargin;
-            const int nc = min(sm.n_cand, kCandCap);
-            int o = 0;
-            for (int i = 0; i < nc; ++i)
-                if (sm.cand_s[i] <= lim) {
-                    sm.cand_v[o] = sm.cand_v[i];
-                    sm.cand_j[o] = sm.cand_j[i];
-                    sm.cand_s[o] = sm.cand_s[i];
-                    ++o;
-                }
-            sm.n_cand = o;
-        }
+        if (threadIdx.x == 0) compact_candidates(sm);
         __syncthreads();
     }
-    if (tid == 0) sm.n_l2 = 0;
+    if (threadIdx.x == 0) sm.n_l2 = 0;
     __syncthreads();
 }
 
-// Expand listed level-3 nodes into level-2 groups (tree layout), evaluating groups as the list fills.
+// Expand listed level-3 nodes into groups (tree clocks), evaluating the groups as the list fills.
 template <bool BF16, bool VEC>
 __device__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
     const int tid = threadIdx.x;
     const int n = min(sm.n_l3, kL3Cap) * 16;
     const uint32_t V = (uint32_t)a.V;
+    const int ng = a.L.ng;
     for (int base = 0; base < n; base += kBlock) {
-        // Every thread reads the list count before any thread of this pass can push
-        // (otherwise waves could disagree on calling the barrier-bearing flush).
-        const bool flush = sm.n_l2 > 0;
+        // The count is read by every thread before any thread of this pass pushes.
+        const bool flush = sm.n_l2 > kL2Cap - kBlock;
         __syncthreads();
         if (flush) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
         const int e = base + tid;
         if (e < n) {
             const Node pa = sm.l3[e >> 4];
             const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
-            const uint32_t cs = g << kShift2;
-            if (cs < V) {
-                const uint32_t slot = pa.id >> 20;
-                float m;
-                uint32_t p;
-                child_min_f32(pa.m, pa.p, 2, g, cs, node_end(kShift2, g, V), slot, k0, k1, m, p);
-                if (ln_f32(m) - gm[g] * r.invT <= current_threshold(sm))
-                    push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | g, m, p, a);
+            if ((int)g < ng) {
+                const float thr = current_threshold(sm);
+                if (ln_f32(pa.m) - gm[g] * r.invT <= thr) {
+                    const uint32_t slot = pa.id >> 20;
+                    float m;
+                    uint32_t p;
+                    child_min_f32(pa.m, pa.p, 2, g, g << kShift2, node_end(kShift2, g, V), slot, k0, k1, m, p);
+                    if (ln_f32(m) - gm[g] * r.invT <= thr) push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | g, m, p);
+                }
             }
         }
         __syncthreads();
@@ -393,9 +482,27 @@ __device__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const floa
     __syncthreads();
 }
 
-// Lexicographic minimum of (score, token, slot) over the workgroup.
+// Lexicographic minimum of (score, token, slot).
 __device__ __forceinline__ bool lex_less(double s, int v, int j, double s2, int v2, int j2) {
     return s < s2 || (s == s2 && (v < v2 || (v == v2 && j < j2)));
+}
+
+// Philox words of path node l of token v (tree clocks): 0 = root, 1..4 = the
+// token's level-4..1 ancestors, 5 = the token's own word block.
+__device__ __forceinline__ Words path_draw(int l, uint32_t v, uint32_t slot, uint32_t k0, uint32_t k1) {
+    if (l == 0) return philox(0u, slot, 5u, kDomainTree, k0, k1);
+    if (l == 5) return philox(v >> 3, slot, 8u + ((v >> 2) & 1u), kDomainTree, k0, k1);
+    const int level = 5 - l;  // 4, 3, 2, 1
+    const int sh = level == 4 ? kShift4 : level == 3 ? kShift3 : level == 2 ? kShift2 : kShift1;
+    return philox(v >> sh, slot, (uint32_t)level, kDomainTree, k0, k1);
+}
+
+__device__ __forceinline__ int path_shift(int l) {
+    return l == 1 ? kShift4 : l == 2 ? kShift3 : l == 3 ? kShift2 : kShift1;
+}
+
+__device__ __forceinline__ uint32_t pick_word(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3, uint32_t i) {
+    return i == 0 ? a0 : i == 1 ? a1 : i == 2 ? a2 : a3;
 }
 
 template <bool BF16, bool VEC, int LAYOUT>
@@ -410,74 +517,121 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
     }
     __syncthreads();
 
-    // (A) threshold from the group holding the row maximum, for every slot.
-    if (tid < ns && sm.gstar >= 0 && sm.gstar < ng) {
-        const uint32_t slot = (uint32_t)(r.slot0 + tid);
-        const uint32_t g = (uint32_t)sm.gstar;
-        float m = 0.f;
-        uint32_t p = 0u;
-        if (LAYOUT == 0) {
-            root_min_f32(V, slot, k0, k1, m, p);
-            const int sh[3] = {kShift4, kShift3, kShift2};
+    // init: the argmax token of each top group (its logit is the group maximum) for
+    // every slot.  Tree clocks: 8 lanes per (group, slot) draw the token's path
+    // nodes in parallel and the first lane chains them into the token's clock.
+    for (int e0 = 0; e0 < kTopG * ns * 8; e0 += kBlock) {
+        const int e = e0 + tid;
+        const int pair = e >> 3, l = e & 7;
+        const bool valid = pair < kTopG * ns;
+        const int w = valid ? pair / ns : 0, j = valid ? pair % ns : 0;
+        const int g = valid ? sm.topg[w] : -1;
+        const uint32_t slot = (uint32_t)(r.slot0 + j);
+        const uint32_t av = (uint32_t)max(g, 0) * kGroupTokens + (uint32_t)(valid ? sm.topa[w] : 0);
+        const float xa = g >= 0 ? gm[g] : -INFINITY;
+        if constexpr (LAYOUT == 0) {
+            Words wd = Words{0u, 0u, 0u, 0u};
+            if (valid && l < 6) wd = path_draw(l, av, slot, k0, k1);
+            // chain the pair's draws in every lane (shuffles are wave-wide); lane 0 of
+            // the pair holds the token's clock at the end
+            float m = 0.f, rm = 0.f, E = 0.f;
+            uint32_t p = 0u, rp = 0u;
 #pragma unroll
-            for (int l = 0; l < 3; ++l) {
-                const uint32_t i = (g << kShift2) >> sh[l];
-                child_min_f32(m, p, 4 - l, i, node_start(sh[l], i), node_end(sh[l], i, V), slot, k0, k1, m, p);
+            for (int q = 0; q < 6; ++q) {
+                const int src = (tid & ~7) + q;
+                const uint32_t a0 = (uint32_t)__shfl((int)wd.w0, src);
+                const uint32_t a1 = (uint32_t)__shfl((int)wd.w1, src);
+                const uint32_t a2 = (uint32_t)__shfl((int)wd.w2, src);
+                const uint32_t a3 = (uint32_t)__shfl((int)wd.w3, src);
+                if (q == 0) {
+                    m = rm = exp1_f32(a0) / (float)V;
+                    p = rp = uniform_position(a1, a2, V);
+                } else if (q <= 4) {
+                    const int sh = path_shift(q);
+                    const uint32_t i = av >> sh, cs = i << sh, ce = node_end(sh, i, V);
+                    if (!(p >= cs && p < ce)) {
+                        m = m + exp1_f32(a0) / (float)(ce - cs);
+                        p = cs + uniform_position(a1, a2, ce - cs);
+                    }
+                } else {
+                    E = (av == p) ? m : m + exp1_f32(pick_word(a0, a1, a2, a3, av & 3u));
+                }
+            }
+            if (l == 0 && valid) {
+                if (w == 0) {
+                    sm.root_m[j] = rm;
+                    sm.root_p[j] = rp;
+                }
+                if (g >= 0) {
+                    const float sc = ln_f32(E) - xa * r.invT;
+                    if (sc < INFINITY) {
+                        atomicMin(&sm.best_key, ordered_key(sc));
+                        push_candidate(sm, a, (int)av, (int)slot, sc, xa);
+                    }
+                }
+            }
+        } else {
+            if (l == 0 && g >= 0) {
+                const Words wd = philox(av >> 2, slot, 0u, kDomainFlat, k0, k1);
+                const float s = ln_f32(exp1_f32(word_at(wd, av & 3u))) - xa * r.invT;
+                if (s < INFINITY) {
+                    atomicMin(&sm.best_key, ordered_key(s));
+                    push_candidate(sm, a, (int)av, (int)slot, s, xa);
+                }
             }
         }
-        sm.l2[tid] = Node{(slot << 20) | g, m, p};
     }
-    if (tid == 0) sm.n_l2 = (sm.gstar >= 0 && sm.gstar < ng) ? ns : 0;
     __syncthreads();
-    flush_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, k0, k1);
+    if (tid == 0) compact_candidates(sm);
+    __syncthreads();
 
     if constexpr (LAYOUT == 0) {
-        // (B) tree descent: roots -> level 4 -> level 3 -> level 2 groups.
-        if (tid < ns) root_min_f32(V, (uint32_t)(r.slot0 + tid), k0, k1, sm.root_m[tid], sm.root_p[tid]);
-        __syncthreads();
+        // descent: level-4 children of the roots.
         const int n4 = (int)((V + (1u << kShift4) - 1) >> kShift4);
-        for (int base = 0; base < ns * n4; base += kBlock) {
-            const int e = base + tid;
-            if (e < ns * n4) {
-                const int j = e / n4;
-                const uint32_t i4 = (uint32_t)(e % n4);
-                const uint32_t slot = (uint32_t)(r.slot0 + j);
-                float m;
-                uint32_t p;
-                child_min_f32(sm.root_m[j], sm.root_p[j], 4, i4, node_start(kShift4, i4), node_end(kShift4, i4, V),
-                              slot, k0, k1, m, p);
-                if (ln_f32(m) - sm.m4[i4] * r.invT <= current_threshold(sm))
-                    push_node(sm.l4, &sm.n_l4, kL4Cap, (slot << 20) | i4, m, p, a);
-            }
+        for (int e = tid; e < ns * n4; e += kBlock) {
+            const int j = e / n4;
+            const uint32_t i4 = (uint32_t)(e % n4);
+            const float thr = current_threshold(sm);
+            if (ln_f32(sm.root_m[j]) - sm.m4[i4] * r.invT > thr) continue;
+            const uint32_t slot = (uint32_t)(r.slot0 + j);
+            float m;
+            uint32_t p;
+            child_min_f32(sm.root_m[j], sm.root_p[j], 4, i4, node_start(kShift4, i4), node_end(kShift4, i4, V), slot,
+                          k0, k1, m, p);
+            if (ln_f32(m) - sm.m4[i4] * r.invT <= thr) push_node(sm.l4, &sm.n_l4, kL4Cap, (slot << 20) | i4, m, p);
         }
         __syncthreads();
+        // level-3 children of the surviving level-4 nodes.
         const int n3tot = min(sm.n_l4, kL4Cap) * 16;
+        const int n3 = (ng + 15) / 16;
         for (int base = 0; base < n3tot; base += kBlock) {
-            const bool flush = sm.n_l3 + kBlock > kL3Cap;
+            const bool flush = sm.n_l3 > kL3Cap - kBlock;
             __syncthreads();
             if (flush) flush_l3<BF16, VEC>(a, r, sm, gm, k0, k1);
             const int e = base + tid;
             if (e < n3tot) {
                 const Node pa = sm.l4[e >> 4];
                 const uint32_t i3 = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
-                const uint32_t cs = i3 << kShift3;
-                if (cs < V) {
-                    const uint32_t slot = pa.id >> 20;
-                    float m;
-                    uint32_t p;
-                    child_min_f32(pa.m, pa.p, 3, i3, cs, node_end(kShift3, i3, V), slot, k0, k1, m, p);
-                    if (ln_f32(m) - sm.m3[i3] * r.invT <= current_threshold(sm))
-                        push_node(sm.l3, &sm.n_l3, kL3Cap, (slot << 20) | i3, m, p, a);
+                if ((int)i3 < n3) {
+                    const float thr = current_threshold(sm);
+                    if (ln_f32(pa.m) - sm.m3[i3] * r.invT <= thr) {
+                        const uint32_t slot = pa.id >> 20;
+                        float m;
+                        uint32_t p;
+                        child_min_f32(pa.m, pa.p, 3, i3, i3 << kShift3, node_end(kShift3, i3, V), slot, k0, k1, m, p);
+                        if (ln_f32(m) - sm.m3[i3] * r.invT <= thr)
+                            push_node(sm.l3, &sm.n_l3, kL3Cap, (slot << 20) | i3, m, p);
+                    }
                 }
             }
             __syncthreads();
         }
         flush_l3<BF16, VEC>(a, r, sm, gm, k0, k1);
     } else {
-        // (B) flat clocks: every (group, slot) whose floor bound can win.
+        // flat clocks: every (group, slot) whose floor bound can win.
         const int tot = ng * ns;
         for (int base = 0; base < tot; base += kBlock) {
-            const bool flush = sm.n_l2 > 0;
+            const bool flush = sm.n_l2 > kL2Cap - kBlock;
             __syncthreads();
             if (flush) flush_groups<BF16, VEC, 1>(a, r, sm, gm, k0, k1);
             const int e = base + tid;
@@ -485,28 +639,62 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
                 const int g = e / ns;
                 const uint32_t slot = (uint32_t)(r.slot0 + e % ns);
                 if (kLnClockFloor - gm[g] * r.invT <= current_threshold(sm))
-                    push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | (uint32_t)g, 0.f, 0u, a);
+                    push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | (uint32_t)g, 0.f, 0u);
             }
             __syncthreads();
         }
         flush_groups<BF16, VEC, 1>(a, r, sm, gm, k0, k1);
     }
 
-    // (C) exact decision among the candidates within the margin of the best.
+    // decide: float64 scores of the candidates within the margin of the best; for
+    // tree clocks 8 lanes per candidate draw its path nodes in parallel.
     const float best = ordered_value(sm.best_key);
     const int nc = min(sm.n_cand, kCandCap);
     double bs = INFINITY;
     int bv = 0x7FFFFFFF, bj = 0x7FFFFFFF;
-    for (int i = tid; i < nc; i += kBlock) {
-        if (sm.cand_s[i] > best + kMargin) continue;
-        const int v = sm.cand_v[i], j = sm.cand_j[i];
-        const double E = LAYOUT == 0 ? tree_clock_f64(V, (uint32_t)j, (uint32_t)v, k0, k1)
-                                     : flat_clock_f64((uint32_t)j, (uint32_t)v, k0, k1);
-        const double s = log(E) - (double)load_logit<BF16>(r.ptr, v) / (double)r.T;
-        if (lex_less(s, v, j, bs, bv, bj)) {
-            bs = s;
-            bv = v;
-            bj = j;
+    for (int e0 = 0; e0 < nc * 8; e0 += kBlock) {
+        const int e = e0 + tid;
+        const int ci = e >> 3, l = e & 7;
+        const bool valid = ci < nc && sm.cand_s[ci] <= best + kMargin;
+        const int v = valid ? sm.cand_v[ci] : 0, j = valid ? sm.cand_j[ci] : 0;
+        double E = 0.0;
+        if constexpr (LAYOUT == 0) {
+            Words wd = Words{0u, 0u, 0u, 0u};
+            if (valid && l < 6) wd = path_draw(l, (uint32_t)v, (uint32_t)j, k0, k1);
+            double m = 0.0;
+            uint32_t p = 0u;
+#pragma unroll
+            for (int q = 0; q < 6; ++q) {
+                const int src = (tid & ~7) + q;
+                const uint32_t a0 = (uint32_t)__shfl((int)wd.w0, src);
+                const uint32_t a1 = (uint32_t)__shfl((int)wd.w1, src);
+                const uint32_t a2 = (uint32_t)__shfl((int)wd.w2, src);
+                const uint32_t a3 = (uint32_t)__shfl((int)wd.w3, src);
+                if (l != 0 || !valid) continue;
+                if (q == 0) {
+                    m = exp1_f64(a0) / (double)V;
+                    p = uniform_position(a1, a2, V);
+                } else if (q <= 4) {
+                    const int sh = path_shift(q);
+                    const uint32_t i = (uint32_t)v >> sh, cs = i << sh, ce = node_end(sh, i, V);
+                    if (!(p >= cs && p < ce)) {
+                        m = m + exp1_f64(a0) / (double)(ce - cs);
+                        p = cs + uniform_position(a1, a2, ce - cs);
+                    }
+                } else {
+                    E = ((uint32_t)v == p) ? m : m + exp1_f64(pick_word(a0, a1, a2, a3, (uint32_t)v & 3u));
+                }
+            }
+        } else {
+            if (l == 0 && valid) E = flat_clock_f64((uint32_t)j, (uint32_t)v, k0, k1);
+        }
+        if (l == 0 && valid) {
+            const double s = log(E) - (double)sm.cand_x[ci] / (double)r.T;
+            if (lex_less(s, v, j, bs, bv, bj)) {
+                bs = s;
+                bv = v;
+                bj = j;
+            }
         }
     }
 #pragma unroll
@@ -540,15 +728,20 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
 
 // ---------------------------------------------------------------- walk
 
-__device__ void walk(const RaceArgs& a, int b) {
+__device__ int walk_draft(const RaceArgs& a, int b, int k, int s, uint32_t ep) {
+    if (a.s_count > 0 && s >= a.s_begin) return wait_token(a, draft_row_id(a, b, k, s), ep);
+    return a.draft_tokens[((size_t)b * a.K + k) * a.gamma + s];
+}
+
+// Realised-path walk of sequence b; every token it reads carries this call's epoch.
+__device__ void walk(const RaceArgs& a, int b, uint32_t ep) {
     const int K = a.K, G = a.gamma;
-    const int32_t* tok = (const int32_t*)(a.ws + a.L.tok);
     uint32_t act = K >= 32 ? 0xFFFFFFFFu : ((1u << K) - 1u);
     int tau = 0;
     bool done = false;
     for (int s = 0; s < G && !done; ++s) {
         const int kk = __ffs((int)act) - 1;
-        const int y = ld_dev(tok + target_row_id(a, b, kk, s));
+        const int y = wait_token(a, target_row_id(a, b, kk, s), ep);
         a.out_tokens[(size_t)b * (G + 1) + s] = y;
         tau = s + 1;
         if (y < 0) {
@@ -557,7 +750,7 @@ __device__ void walk(const RaceArgs& a, int b) {
         }
         uint32_t na = 0u;
         for (int k = 0; k < K; ++k)
-            if (((act >> k) & 1u) && ld_dev(a.draft_tokens + ((size_t)b * K + k) * G + s) == y) na |= 1u << k;
+            if (((act >> k) & 1u) && walk_draft(a, b, k, s, ep) == y) na |= 1u << k;
         if (!na) {
             done = true;
             break;
@@ -566,7 +759,7 @@ __device__ void walk(const RaceArgs& a, int b) {
     }
     if (!done) {
         const int kk = __ffs((int)act) - 1;
-        a.out_tokens[(size_t)b * (G + 1) + G] = ld_dev(tok + target_row_id(a, b, kk, G));
+        a.out_tokens[(size_t)b * (G + 1) + G] = wait_token(a, target_row_id(a, b, kk, G), ep);
         tau = G + 1;
     }
     for (int s = tau; s <= G; ++s) a.out_tokens[(size_t)b * (G + 1) + s] = -1;
@@ -575,56 +768,42 @@ __device__ void walk(const RaceArgs& a, int b) {
 
 // ---------------------------------------------------------------- row finisher
 
+// Token at path depth d of this row's context (prefix excluded).
+__device__ __forceinline__ int path_token(const RaceArgs& a, const Row& r, int d, uint32_t ep) {
+    if (r.kind == 1 && a.target_rows == 1) return wait_token(a, target_row_id(a, r.b, 0, d), ep);
+    if (a.s_count > 0 && d >= a.s_begin) return wait_token(a, draft_row_id(a, r.b, r.k, d), ep);
+    return a.draft_tokens[((size_t)r.b * a.K + r.k) * a.gamma + d];
+}
+
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* gm) {
-    const int tid = threadIdx.x;
+__device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* gm, uint8_t* ga) {
+    // The race is a latency chain (the next depth of this path waits for it) while
+    // the other waves on the same SIMDs stream: raise this wave's issue priority.
+    __builtin_amdgcn_s_setprio(3);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int ng = a.L.ng;
     const int n3 = (ng + 15) / 16, n4 = (n3 + 15) / 16;
-    const float* gsrc = (const float*)(a.ws + a.L.gmax) + (size_t)r.row_id * ng;
-    for (int g = tid; g < ng; g += kBlock) gm[g] = ld_dev(gsrc + g);
-    if (tid == 0) {
-        // LSE from the segment partials (log2 units), merged in double.
-        const unsigned long long* part = (const unsigned long long*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
-        double M = -INFINITY, S = 0.0;
-        for (int i = 0; i < a.L.nseg; ++i) {
-            const unsigned long long bits = ld_dev(part + i);
-            const double pm = (double)__uint_as_float((uint32_t)bits), ps = (double)__uint_as_float((uint32_t)(bits >> 32));
-            if (pm == -INFINITY) continue;
-            if (pm > M) {
-                S = (M == -INFINITY ? 0.0 : S * exp2(M - pm)) + ps;
-                M = pm;
-            } else {
-                S += ps * exp2(pm - M);
-            }
+    const uint32_t ep = sm.epoch;
+    const float c2 = r.invT * 1.4426950408889634f;
+
+    // ---- gather the row's slots (waves 0-2) while wave 3 folds the context key,
+    // waiting for path tokens as they are published (normally only the newest).
+    if (wave < 3) {
+        const uint64_t* gslot = (const uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * ng;
+        for (int g = tid; g < ng; g += 192) {
+            const uint64_t v = wait_slot(a, gslot + g, ep, 40);
+            gm[g] = __uint_as_float((uint32_t)v);
+            ga[g] = (uint8_t)(v >> 32);
         }
-        const double lse = M == -INFINITY ? -INFINITY : (M + log2(S)) * 0.69314718055994530942;
-        if (r.kind == 0) {
-            if (a.draft_lse) a.draft_lse[((size_t)r.b * a.K + r.k) * a.gamma + r.s] = (float)lse;
-        } else if (a.target_lse) {
-            const size_t o = a.target_rows == 1 ? (size_t)r.b * (a.gamma + 1) + r.s
-                                                : ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + r.s;
-            a.target_lse[o] = (float)lse;
-        }
-        // Context window: last m tokens of prefix || path tokens before depth s.
+    } else if (lane == 0) {
+        uint32_t k0 = (uint32_t)a.key, k1 = (uint32_t)(a.key >> 32);
+        const uint64_t t = (uint64_t)(a.start_pos[r.b] + r.s);
+        fold(k0, k1, (uint32_t)t, (uint32_t)(t >> 32), 0u);
         for (int i = 0; i < a.m; ++i) {
-            const int idx = r.s + i;  // index into prefix (m tokens) || path (s tokens)
-            int tk;
-            if (idx < a.m) {
-                tk = a.prefix[(size_t)r.b * a.m + idx];
-            } else {
-                const int d = idx - a.m;  // path depth
-                if (r.kind == 1 && a.target_rows == 1) {
-                    tk = wait_token(a, target_row_id(a, r.b, 0, d));
-                } else if (a.s_count > 0 && d >= a.s_begin) {
-                    tk = wait_token(a, draft_row_id(a, r.b, r.k, d));
-                } else {
-                    tk = a.draft_tokens[((size_t)r.b * a.K + r.k) * a.gamma + d];
-                }
-            }
-            sm.window[i] = tk;
+            const int idx = r.s + i;  // position in prefix (m tokens) || path (s tokens)
+            const int tk = idx < a.m ? a.prefix[(size_t)r.b * a.m + idx] : path_token(a, r, idx - a.m, ep);
+            fold(k0, k1, (uint32_t)tk, (uint32_t)i, 1u);
         }
-        uint32_t k0, k1;
-        context_key(a.key, a.start_pos[r.b] + r.s, sm.window, a.m, k0, k1);
         sm.kappa0 = k0;
         sm.kappa1 = k1;
     }
@@ -634,26 +813,30 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         for (int g = 16 * t; g < min(ng, 16 * t + 16); ++g) mx = fmaxf(mx, gm[g]);
         sm.m3[t] = mx;
     }
-    // argmax group (lowest index among equal maxima)
-    float bvv = -INFINITY;
-    int bi = 0x7FFFFFFF;
-    for (int g = tid; g < ng; g += kBlock)
-        if (gm[g] > bvv) {
-            bvv = gm[g];
-            bi = g;
-        }
+    {
+        // wave w keeps the largest group among g = w (mod 4) (lowest index on ties);
+        // together the four hold the row maximum.
+        float bv = -INFINITY;
+        int bi = -1;
+        for (int g = wave + 4 * lane; g < ng; g += 256)
+            if (gm[g] > bv) {
+                bv = gm[g];
+                bi = g;
+            }
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const float ov = __shfl_xor(bvv, off);
-        const int oi = __shfl_xor(bi, off);
-        if (ov > bvv || (ov == bvv && oi < bi)) {
-            bvv = ov;
-            bi = oi;
+        for (int off = 32; off > 0; off >>= 1) {
+            const float ov = __shfl_xor(bv, off);
+            const int oi = __shfl_xor(bi, off);
+            if (ov > bv || (ov == bv && oi >= 0 && (bi < 0 || oi < bi))) {
+                bv = ov;
+                bi = oi;
+            }
         }
-    }
-    if ((tid & 63) == 0) {
-        sm.red_a[tid >> 6] = bvv;
-        sm.red_v[tid >> 6] = bi;
+        if (lane == 0) {
+            sm.topg[wave] = (bv == -INFINITY) ? -1 : bi;
+            sm.topa[wave] = bi >= 0 ? ga[bi] : 0;
+            sm.red_a[wave] = bv;
+        }
     }
     __syncthreads();
     if (tid < n4) {
@@ -661,14 +844,40 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         for (int t = 16 * tid; t < min(n3, 16 * tid + 16); ++t) mx = fmaxf(mx, sm.m3[t]);
         sm.m4[tid] = mx;
     }
-    if (tid == 0) {
-        for (int w = 1; w < kBlock / 64; ++w)
-            if (sm.red_a[w] > bvv || (sm.red_a[w] == bvv && sm.red_v[w] < bi)) {
-                bvv = sm.red_a[w];
-                bi = sm.red_v[w];
+    if (wave == 1) {
+        // LSE: segment i's maximum is the maximum of its groups (the same float product
+        // the segment used), merged with the segments' sums in float32.
+        constexpr int per = (BF16 ? kSegTokensBf16 : kSegTokensF32) / 2048;  // level-3 blocks per segment
+        float mi = -INFINITY, si = 0.f;
+        if (lane < a.L.nseg) {
+            const uint64_t v =
+                wait_slot(a, (const uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg + lane, ep, 32);
+            float gmx = -INFINITY;
+            for (int t = lane * per; t < min(n3, lane * per + per); ++t) gmx = fmaxf(gmx, sm.m3[t]);
+            mi = gmx * c2;
+            si = __uint_as_float((uint32_t)v);
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const float om = __shfl_xor(mi, off);
+            const float os = __shfl_xor(si, off);
+            lse_combine(mi, si, om, os);
+        }
+        if (lane == 0) {
+            const float lse = mi == -INFINITY ? -INFINITY : (mi + __builtin_amdgcn_logf(si)) * 0.69314718055994531f;
+            if (r.kind == 0) {
+                if (a.draft_lse) a.draft_lse[((size_t)r.b * a.K + r.k) * a.gamma + r.s] = lse;
+            } else if (a.target_lse) {
+                const size_t o = a.target_rows == 1 ? (size_t)r.b * (a.gamma + 1) + r.s
+                                                    : ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + r.s;
+                a.target_lse[o] = lse;
             }
-        sm.rowmax = bvv;
-        sm.gstar = bi;
+        }
+    }
+    if (tid == 0) {
+        float mx = -INFINITY;
+        for (int w = 0; w < kBlock / 64; ++w) mx = fmaxf(mx, sm.red_a[w]);
+        sm.rowmax = mx;
     }
     __syncthreads();
     const uint32_t k0 = sm.kappa0, k1 = sm.kappa1;
@@ -683,58 +892,40 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
     }
     if (tid == 0) {
         const int y = sm.win_token;
+        st_dev((uint64_t*)(a.ws + a.L.tok) + r.row_id, ((uint64_t)ep << 32) | (uint32_t)y);
         if (r.kind == 0) {
-            st_dev(a.draft_tokens + ((size_t)r.b * a.K + r.k) * a.gamma + r.s, y);
+            a.draft_tokens[((size_t)r.b * a.K + r.k) * a.gamma + r.s] = y;
         } else if (a.target_tokens) {
             const size_t o = a.target_rows == 1 ? (size_t)r.b * (a.gamma + 1) + r.s
                                                 : ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + r.s;
             a.target_tokens[o] = y;
         }
-        st_dev((int32_t*)(a.ws + a.L.tok) + r.row_id, y);
-        drain_memory();
-        st_dev((uint32_t*)(a.ws + a.L.flag) + r.row_id, 1u);
-        if (a.target_rows > 0) {
-            uint32_t* sc = (uint32_t*)(a.ws + a.L.seq_cnt) + r.b;
-            const uint32_t old = __hip_atomic_fetch_add(sc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if ((int)old + 1 == a.seq_rows) {
-                drain_memory();
-                walk(a, r.b);
-            }
-        }
+        // The last row of a sequence in ticket order walks its block.
+        if (r.kind == 1 && r.s == a.gamma && (a.target_rows == 1 || r.k == a.K - 1)) walk(a, r.b, ep);
     }
+    __builtin_amdgcn_s_setprio(0);
 }
 
 // ---------------------------------------------------------------- kernel
 
 template <bool BF16, bool VEC, int LAYOUT>
-__global__ __launch_bounds__(kBlock) void race_kernel(RaceArgs a) {
+__global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Shared& sm = *reinterpret_cast<Shared*>(smem_raw);
     float* gm = reinterpret_cast<float*>(smem_raw + ((sizeof(Shared) + 15) & ~(size_t)15));
+    uint8_t* ga = reinterpret_cast<uint8_t*>(gm + a.L.ng);
     const int tid = threadIdx.x;
     uint32_t* ctrl = ctrl_of(a);
     const size_t esize = BF16 ? 2 : 4;
     const int D = a.B * a.K * a.gamma;
-    // Ticket 0 clears this call's row counters, flags and sequence counters (their
-    // placement depends on the call's shape, so a previous call with another shape
-    // may have left data there); every workgroup waits for that clear before its
-    // first counter update.  Tickets 1.. are the work items.
-    bool cleared = false;
-    for (;;) {
-        if (tid == 0) sm.item = (int)atomicAdd(ctrl, 1u) - 1;
-        __syncthreads();
-        const int item = sm.item;
+    if (tid == 0) {
+        sm.epoch = ld_dev(ctrl + kCtrlEpoch) % 0xFFFFFFu + 1u;  // 1 .. 2^24-1
+        sm.tick[0] = (int)atomicAdd(ctrl + kCtrlTicket, 1u);
+    }
+    __syncthreads();
+    for (int parity = 0;; parity ^= 1) {
+        const int item = sm.tick[parity];
         if (item >= a.n_items) break;
-        if (item < 0) {
-            uint32_t* base = (uint32_t*)(a.ws + a.L.row_cnt);
-            const size_t n = (a.L.ctrl_end - a.L.row_cnt) / 4;
-            for (size_t i = tid; i < n; i += kBlock) st_dev(base + i, 0u);
-            drain_memory();
-            __syncthreads();
-            if (tid == 0) st_dev(ctrl + 4, 1u);
-            cleared = true;
-            continue;
-        }
         int d = 0;
         while (d + 1 < a.n_depth && item >= a.depth_first[d + 1]) ++d;
         const int local = item - a.depth_first[d];
@@ -773,36 +964,31 @@ __global__ __launch_bounds__(kBlock) void race_kernel(RaceArgs a) {
             r.invT = a.inv_T_target;
             r.T = a.T_target;
         }
-        stream_segment<BF16, VEC>(a, r, seg, sm);
-        drain_memory();
-        __syncthreads();
-        if (tid == 0) {
-            if (!cleared) wait_nonzero(a, ctrl + 4);
-            uint32_t* rc = (uint32_t*)(a.ws + a.L.row_cnt) + r.row_id;
-            const uint32_t old = __hip_atomic_fetch_add(rc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            drain_memory();
-            sm.fin = ((int)old == a.L.nseg - 1);
+        const bool last = seg == a.L.nseg - 1;
+        stream_segment<BF16, VEC>(a, r, seg, sm, parity, !last);
+        // the workgroup holding the row's last segment (highest ticket) finishes it
+        if (last) {
+            finish_row<BF16, VEC, LAYOUT>(a, r, sm, gm, ga);
+            if (tid == 0) sm.tick[parity ^ 1] = (int)atomicAdd(ctrl + kCtrlTicket, 1u);
         }
-        cleared = true;
-        __syncthreads();
-        if (sm.fin) finish_row<BF16, VEC, LAYOUT>(a, r, sm, gm);
         __syncthreads();
     }
-    // The last workgroup to leave resets the fixed header words for the next call.
+    // The last workgroup to leave resets the ticket and advances the epoch.
     if (tid == 0) {
-        drain_memory();
-        const uint32_t old = __hip_atomic_fetch_add(ctrl + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t old = __hip_atomic_fetch_add(ctrl + kCtrlExited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (old == gridDim.x - 1) {
-            st_dev(ctrl + 0, 0u);
-            st_dev(ctrl + 1, 0u);
-            st_dev(ctrl + 4, 0u);
+            st_dev(ctrl + kCtrlTicket, 0u);
+            st_dev(ctrl + kCtrlExited, 0u);
+            st_dev(ctrl + kCtrlEpoch, sm.epoch);
         }
     }
 }
 
+size_t shared_bytes(int ng) { return ((sizeof(Shared) + 15) & ~(size_t)15) + (size_t)ng * (sizeof(float) + 1); }
+
 template <bool BF16, bool VEC, int LAYOUT>
 hipError_t launch_one(const RaceArgs& a, hipStream_t stream) {
-    const size_t smem = ((sizeof(Shared) + 15) & ~(size_t)15) + (size_t)a.L.ng * sizeof(float);
+    const size_t smem = shared_bytes(a.L.ng);
     auto fn = race_kernel<BF16, VEC, LAYOUT>;
     int per_cu = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, smem);
@@ -829,6 +1015,6 @@ hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipSt
     return layout == 0 ? launch_one<false, false, 0>(a, stream) : launch_one<false, false, 1>(a, stream);
 }
 
-size_t race_shared_bytes(int ng) { return ((sizeof(Shared) + 15) & ~(size_t)15) + (size_t)ng * sizeof(float); }
+size_t race_shared_bytes(int ng) { return shared_bytes(ng); }
 
 }  // namespace psd
