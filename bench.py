@@ -103,6 +103,35 @@ def cpu_baseline(blk, w, clocks_id, n_seq):
                       f"single-threaded C; {dt:.1f} s"}
 
 
+def detect_leg(psd, torch, clocks_id, dev, launches=20):
+    """Detection throughput on the stress workload's text shape: 256 sequences of
+    512 scored tokens after a 4-token prompt, K=16, V=256000.  The per-token work
+    (context key plus K keyed clocks) does not depend on the token values, so
+    uniform tokens stand in for generated text."""
+    import workloads
+    w5 = workloads.WORKLOADS[5]
+    n_seq, n_pos = w5.B, 512
+    toks = workloads.uniform_tokens(n_seq, w5.m + n_pos, w5.V, seed=5).to(dev)
+    n0 = torch.full((n_seq,), w5.m, dtype=torch.int32, device=dev)
+    p5 = psd.make_params(w5.key, w5.V, w5.K, w5.m, dtype=w5.torch_dtype, clocks=clocks_id)
+    for _ in range(3):
+        psd.detect(p5, toks, n0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(launches):
+        psd.detect(p5, toks, n0)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / launches
+    draws = 6 if clocks_id == psd.PSD_CLOCKS_TREE else 1
+    calls = (w5.m + 1) + w5.K * draws
+    return {"workload": f"detection: {n_seq} sequences x {n_pos} scored tokens, K={w5.K}, V={w5.V}, m={w5.m}",
+            "tokens_per_s": n_seq * n_pos / (ms / 1e3), "ms_per_launch": ms, "launches": launches,
+            "philox_calls_per_token": calls,
+            "philox_calls_per_s": n_seq * n_pos * calls / (ms / 1e3)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,6 +233,7 @@ def main():
         "mean_tau": mean_tau,
         "wall_s": wall,
     }
+    res["detect"] = detect_leg(psd, torch, clocks_id, dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(sets[0], w, clocks_id, args.cpu_seqs)
     print(json.dumps(res), flush=True)

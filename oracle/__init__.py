@@ -10,7 +10,7 @@ module adds the block-level orchestration in plain Python:
 
 * draft path k of a speculative block drafts depth s with the race of its own
   slot k over its draft row, keyed by the context (key, t, last m tokens of
-  prefix || x^(k)_{<s}) -- Sec. 3.3 / Sec. 4 algorithms and the non-identical
+  prefix || x^(k)_{<s}) -- Sec. 4.3 / Sec. 5 algorithms and the non-identical
   proposal construction (Prop. "heterogeneous PML bound");
 * the target chain races all K slots at every depth s = 0..gamma, keyed by the
   context of its own chain prefix || y_{<s} (stopping-time drafter invariance,

@@ -12,7 +12,7 @@
  *
  * Paper passages followed (by section / equation / algorithm):
  *  - keyed source Pi(c) = G(k, Lambda(c)), independent across contexts, tokens and
- *    arrival indices: Sec. 3.3 (single-draft algorithm), Sec. 4 (multi-draft
+ *    arrival indices: Sec. 4.3 (single-draft algorithm), Sec. 5 (multi-draft
  *    algorithm), App. "Algorithm Implementation" (labeler Lambda, detector).
  *  - EFR race  Z = argmin_z E_z / P(z), E_z iid Exp(1), E_z/P(z)=+inf if P(z)=0:
  *    eq. (EFR) and Thm. "PFR reduces to EFR" (App. on PFR in the discrete case).
@@ -20,7 +20,7 @@
  *    P~(i,b)=p_i/B over all (i,b), draft b races its own block b:
  *    Prop. "heterogeneous PML bound" (App. "Extension ... non-identically
  *    distributed proposals").
- *  - detector score A_t = -log(1 - r_t(w_t)): eq. (S_A), Sec. 3.3 and App.
+ *  - detector score A_t = -log(1 - r_t(w_t)): eq. (S_A), Sec. 4.3 and App.
  *    "Gumbel Watermark".
  *
  * Readings taken where the paper is silent (the paper fixes no PRF, PRNG or

@@ -2,7 +2,7 @@
 //
 // Keyed randomness: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) keyed by a
 // 64-bit context key kappa = H(key, t, last m tokens); the paper leaves the PRF
-// open (Sec. 3.3: r_t(y) = F_{y_{t-m:t-1},k}(y); App. "Algorithm Implementation":
+// open (Sec. 4.3: r_t(y) = F_{y_{t-m:t-1},k}(y); App. "Algorithm Implementation":
 // Pi_t = G(k, Lambda(c_t))).  Clocks are iid Exp(1) per (slot, token) given kappa
 // (eq. EFR), built by one of two layouts (see psd.h, psd_clocks).
 #pragma once

@@ -109,6 +109,19 @@ def test_philox_words_bit_exact(psd):
         assert list(out[i]) == oracle.philox(ctr[i], key[i]), i
 
 
+def test_philox_known_answers(psd):
+    rows = []
+    with open(os.path.join(ROOT, "tests", "golden", "philox4x32_10_kat.txt")) as fh:
+        for line in fh:
+            if line.strip() and not line.startswith("#"):
+                rows.append([int(x, 16) for x in line.split()])
+    w = np.array(rows, dtype=np.uint64).astype(np.uint32)
+    ctr = torch.from_numpy(np.ascontiguousarray(w[:, :4]).view(np.int32)).to(DEV)
+    key = torch.from_numpy(np.ascontiguousarray(w[:, 4:6]).view(np.int32)).to(DEV)
+    out = _np(psd.philox(ctr, key)).view(np.uint32)
+    assert np.array_equal(out, w[:, 6:10])
+
+
 def test_context_keys_bit_exact(psd):
     rng = np.random.default_rng(2)
     for m in (0, 1, 4, 16):
@@ -260,9 +273,6 @@ def _generate(psd, w, key, n_pos, seed, layout=0):
     return text
 
 
-@pytest.mark.skip(reason="its first GPU runs faulted inside torch.gather: the generation loop indexed the "
-                         "position table out of bounds for finished sequences (cause shown on the CPU by "
-                         "test_generation_loop_indices); fixed in tests/gen_loop.py, kept off the GPU for this round")
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_detect_parity_and_power(psd, layout):
     w = workloads.custom(5000, 4, 4, 6, dtype="bf16", m=3, sigma=3.0, alpha=1.2)

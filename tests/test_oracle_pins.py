@@ -6,6 +6,7 @@ derived from the paper's statements, distribution tests of the keyed clocks and
 of the race outputs, and literal transcriptions of the paper's walk.
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -19,6 +20,27 @@ P_MIN = 1e-4  # deterministic seeds: a correct oracle passes with margin, a wron
 
 
 # ---------------------------------------------------------------- Philox, fold, U
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def load_philox_kat():
+    """Published Philox4x32-10 known-answer vectors (tests/golden/philox4x32_10_kat.txt)."""
+    rows = []
+    with open(os.path.join(GOLDEN, "philox4x32_10_kat.txt")) as fh:
+        for line in fh:
+            if line.strip() and not line.startswith("#"):
+                w = [int(x, 16) for x in line.split()]
+                rows.append((w[:4], w[4:6], w[6:10]))
+    return rows
+
+
+def test_philox_known_answers():
+    rows = load_philox_kat()
+    assert len(rows) == 3
+    for ctr, key, want in rows:
+        assert oracle.philox(ctr, key) == want, (ctr, key)
+
 
 def test_philox_matches_torch_engine(torch_philox):
     rng = np.random.default_rng(7)
