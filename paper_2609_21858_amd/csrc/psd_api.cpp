@@ -96,6 +96,7 @@ void build_depths(psd::RaceArgs& a, int n_depth) {
         first += (nd + nt) * a.L.nseg;
     }
     a.n_items = first;
+    a.n_rows = first / a.L.nseg;
 }
 
 psd_status run_race(const psd_params* p, psd::RaceArgs& a, hipStream_t stream) {

@@ -15,28 +15,39 @@ constexpr int kMaxDepth = 33;           // gamma + 1 <= 33
 inline int seg_tokens(int dtype_bf16) { return dtype_bf16 ? kSegTokensBf16 : kSegTokensF32; }
 
 // Control words at the start of every workspace (fixed positions for every call shape).
-constexpr int kCtrlTicket = 0;   // next work ticket
-constexpr int kCtrlExited = 1;   // workgroups that left the kernel
-constexpr int kCtrlErrors = 2;   // sticky error bits
-constexpr int kCtrlEpoch = 5;    // epoch of the last completed call (24 bits)
+constexpr int kCtrlWords = 1024;   // 4 KiB
+constexpr int kCtrlExited = 1;     // workgroups that left the kernel
+constexpr int kCtrlErrors = 2;     // sticky error bits
+constexpr int kCtrlEpoch = 5;      // epoch of the last completed call
+constexpr int kMaxQueues = 8;      // work queues (one per XCD), counters 256 B apart
+inline constexpr int ctrl_queue(int q) { return 64 * (q + 1); }
 
-// Every slot a call publishes carries that call's epoch (1 .. 2^24-1), so readers
-// detect fresh data by its tag and nothing needs clearing between calls:
-//   tok  : (epoch << 32) | uint32 token
-//   part : (epoch << 32) | float bits of the segment's sum of exp2 (relative to its max)
-//   gmax : (epoch << 40) | (argmax offset within the group << 32) | float bits of the max
+// Every slot a call publishes is (epoch << 32) | 32-bit payload, with the call's
+// epoch (1 .. 2^32-1) in the same bits for every slot kind, so readers detect fresh
+// data by its tag, stale data of another call shape never matches, and nothing is
+// cleared between calls:
+//   tok  : payload = int32 token
+//   part : payload = float bits of the segment's sum of exp2 (relative to its max)
+//   gmax : payload = float bits of the group's maximum logit
+//   m3   : payload = float bits of a 2048-token block's maximum logit
+//   stop : payload = int32 index of the segment's largest group (lowest index; -1: none)
+//   keys : two slots per row, payload = the two words of the context key of the
+//          next depth of the row's path (published by the row's race)
 //
 // Row identifiers (independent of the call):
 //   draft (b, k, s)            : (b*K + k)*gamma + s
 //   target shared (b, s)       : D + b*(gamma+1) + s                 D = B*K*gamma
 //   target per path (b, k, s)  : D + (b*K + k)*(gamma+1) + s
 struct WsLayout {
-    size_t ctrl;  // uint32[64]
+    size_t ctrl;  // uint32[kCtrlWords]
     size_t tok;   // uint64[n_rows]
     size_t part;  // uint64[n_rows][nseg]
     size_t gmax;  // uint64[n_rows][ng]
+    size_t m3;    // uint64[n_rows][n3]
+    size_t stop;  // uint64[n_rows][nseg]
+    size_t keys;  // uint64[n_rows][2]
     size_t total;
-    int n_rows, nseg, ng;
+    int n_rows, nseg, ng, n3;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -47,15 +58,22 @@ inline WsLayout ws_layout(int B, int K, int gamma, int V, int dtype_bf16) {
     L.n_rows = (int)(D + (long)B * K * (gamma + 1));
     L.nseg = (V + seg_tokens(dtype_bf16) - 1) / seg_tokens(dtype_bf16);
     L.ng = (V + 127) / 128;
+    L.n3 = (V + 2047) / 2048;
     size_t o = 0;
     L.ctrl = o;
-    o = align256(o + 64 * 4);
+    o = align256(o + kCtrlWords * 4);
     L.tok = o;
     o = align256(o + (size_t)L.n_rows * 8);
     L.part = o;
     o = align256(o + (size_t)L.n_rows * L.nseg * 8);
     L.gmax = o;
     o = align256(o + (size_t)L.n_rows * L.ng * 8);
+    L.m3 = o;
+    o = align256(o + (size_t)L.n_rows * L.n3 * 8);
+    L.stop = o;
+    o = align256(o + (size_t)L.n_rows * L.nseg * 8);
+    L.keys = o;
+    o = align256(o + (size_t)L.n_rows * 16);
     L.total = o;
     return L;
 }
@@ -80,6 +98,7 @@ struct RaceArgs {
     int s_begin, s_count;       // draft depths computed in this call (s_count = 0: none)
     int target_rows;            // 0: no target rows, 1: shared, K: per path
     int n_items;                // rows * nseg
+    int n_rows;                 // rows of this call (depth-major)
     int n_depth;
     int depth_first[kMaxDepth]; // first item of depth d
     int depth_nd[kMaxDepth];    // draft rows at depth d

@@ -1,19 +1,20 @@
 // psd_race.hip -- fused draft + verify kernel of the keyed Poisson race (gfx950).
 //
-// One persistent kernel per call.  Workgroups pull work items from a global
-// ticket counter; an item is one 32 KiB segment of one logits row.  Items are
-// ordered depth-major (all rows of depth 0, then depth 1, ...), and the segments
-// of a row are consecutive, so every row a race depends on holds lower tickets.
+// One persistent kernel per call.  Rows are numbered depth-major (all rows of
+// depth 0, then depth 1, ...) and dealt round-robin to up to eight work queues,
+// one per XCD (workgroup w serves queue w mod 8), so the ticket counters are not
+// one contended atomic; a queue hands out its rows' 32 KiB segments in order, so
+// every row a race depends on is handed out before the rows that depend on it.
 //
-// Per segment (key-independent, HBM-streaming): coalesced 16-byte loads, the
-// online log-sum-exp partial (sum of exp2 relative to the segment maximum) and the
-// maximum logit of every 128-token group together with its position.  Each value
-// is published as one 64-bit slot tagged with the call's epoch, so nothing waits
-// for stores to drain and nothing is cleared between calls.  The workgroup that
-// holds a row's last segment becomes the row's finisher: it gathers the row's
-// slots, folds the context key (waiting only for the newest context token), runs
-// the keyed race, publishes the winner and -- for the last row of a sequence --
-// walks the block.
+// Per segment (key-independent, HBM-streaming): coalesced 16-byte non-temporal
+// loads, the online log-sum-exp partial (sum of exp2 relative to the segment
+// maximum) and the maximum logit of every 128-token group.  Each value is published
+// as one 64-bit slot tagged with the call's epoch, so nothing waits for stores to
+// drain and nothing is cleared between calls.  The workgroup that holds a row's
+// last segment becomes the row's finisher: it gathers the row's slots and does all
+// key-independent work (block maxima, top groups, LSE), then folds the context key
+// (waiting only for the newest context token), runs the keyed race, publishes the
+// winner and -- for the last row of a sequence -- walks the block.
 //
 // The race (TREE clocks): the argmax tokens of four top groups give achievable
 // scores; a level-by-level descent then expands only nodes whose lower bound
@@ -44,7 +45,7 @@ namespace psd {
 
 namespace {
 
-constexpr int kTopG = kBlock / 64;         // top groups seeding the threshold (one per wave)
+constexpr int kInit = 8;                   // seed tokens of a race (segment top tokens)
 constexpr int kL4Cap = 512;                // <= 32 slots x 16 level-4 nodes
 constexpr int kL3Cap = 512;
 constexpr int kL2Cap = 512;
@@ -63,8 +64,8 @@ struct Node {
 struct Shared {
     float m3[256];
     float m4[16];
-    int topg[kTopG];
-    int topa[kTopG];
+    int init_v[kInit];     // seed tokens of the race (-1: none)
+    int stop[64];          // top token of every segment (-1: none)
     Node l4[kL4Cap];
     Node l3[kL3Cap];
     Node l2[kL2Cap];
@@ -83,9 +84,14 @@ struct Shared {
     int best_key;
     int tick[2];
     uint32_t epoch;
+    int queue, n_queues;
+    float gst[128];   // group maxima of the segment being streamed
     int win_token, win_slot;
     float rowmax;
     uint32_t kappa0, kappa1;
+    uint32_t next0, next1;  // partial context key of the path's next depth
+    int win[32];            // context tokens (own window, next depth's window)
+    int key_min, key_max;   // (token, slot) range of the candidates near the best
 };
 
 struct Row {
@@ -114,11 +120,11 @@ __device__ __forceinline__ T ld_dev(const T* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Bounded wait for a slot whose tag (bits >= shift) equals the epoch.  On timeout an
+// Bounded wait for a slot whose tag (high 32 bits) equals the epoch.  On timeout an
 // error bit is recorded and the stale value is returned, so every wave terminates.
-__device__ uint64_t wait_slot(const RaceArgs& a, const uint64_t* p, uint32_t epoch, int shift) {
+__device__ uint64_t wait_slot(const RaceArgs& a, const uint64_t* p, uint32_t epoch) {
     uint64_t v = ld_dev(p);
-    for (uint32_t i = 0; (uint32_t)(v >> shift) != epoch; ++i) {
+    for (uint32_t i = 0; (uint32_t)(v >> 32) != epoch; ++i) {
         if (i >= kSpinLimit) {
             set_error(a, kErrSpin);
             break;
@@ -139,7 +145,16 @@ __device__ __forceinline__ int draft_row_id(const RaceArgs& a, int b, int k, int
 }
 
 __device__ __forceinline__ int wait_token(const RaceArgs& a, int rid, uint32_t epoch) {
-    return (int)(uint32_t)wait_slot(a, (const uint64_t*)(a.ws + a.L.tok) + rid, epoch, 32);
+    return (int)(uint32_t)wait_slot(a, (const uint64_t*)(a.ws + a.L.tok) + rid, epoch);
+}
+
+// Next work item of queue q (of nq): the queue's rows are R = q, q + nq, ... in
+// depth-major order, each handed out segment by segment.  Returns n_items when the
+// queue is exhausted.
+__device__ __forceinline__ int take_item(const RaceArgs& a, int q, int nq) {
+    const uint32_t t = atomicAdd(ctrl_of(a) + ctrl_queue(q), 1u);
+    const uint32_t R = (uint32_t)q + (uint32_t)nq * (t / (uint32_t)a.L.nseg);
+    return R >= (uint32_t)a.n_rows ? a.n_items : (int)(R * (uint32_t)a.L.nseg + t % (uint32_t)a.L.nseg);
 }
 
 // ---------------------------------------------------------------- logits access
@@ -180,16 +195,24 @@ struct Unit {
     uint4 w[BF16 ? 1 : 2];
 };
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+    const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Vector path: the address is clamped into the row (V * element size is a multiple
+// of 16 bytes there), so every load is unconditional and the compiler can wait for
+// them one by one; words past V are masked by the caller (mask_tail).
 template <bool BF16, bool VEC>
 __device__ __forceinline__ void load_unit(const unsigned char* row, int V, int base, Unit<BF16, VEC>& u) {
     if constexpr (VEC) {
         if constexpr (BF16) {
-            u.w[0] = make_uint4(0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u);
-            if (base < V) u.w[0] = *(const uint4*)((const uint16_t*)row + base);
+            u.w[0] = ld_stream((const uint16_t*)row + min(base, V - 8));
         } else {
-            u.w[0] = u.w[1] = make_uint4(0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u);
-            if (base < V) u.w[0] = *(const uint4*)((const float*)row + base);
-            if (base + 4 < V) u.w[1] = *(const uint4*)((const float*)row + base + 4);
+            u.w[0] = ld_stream((const float*)row + min(base, V - 4));
+            u.w[1] = ld_stream((const float*)row + min(base + 4, V - 4));
         }
     } else {
         float x[8];
@@ -230,69 +253,104 @@ __device__ __forceinline__ void lse_combine(float& m, float& s, float om, float 
     m = mn;
 }
 
-// One 32 KiB segment: (max, argmax) of every 128-token group and the segment's sum
-// of exp2(l * log2e / T - M), M = log2e / T * (segment max).  Unless the
-// workgroup is about to finish a row (which can wait on other workgroups), thread 0
-// fetches its next ticket while the loads are in flight: a ticket held through such
-// a wait would stall the rows that need that segment.
+// Running maxima start at a finite sentinel, so that rescaling never meets inf - inf.
+constexpr float kNegBig = -1e30f;
+
+__device__ __forceinline__ void lse_merge_finite(float& m, float& s, float om, float os) {
+    const float mn = fmaxf(m, om);
+    s = s * __builtin_amdgcn_exp2f(m - mn) + os * __builtin_amdgcn_exp2f(om - mn);
+    m = mn;
+}
+
+// One 32 KiB segment: the maximum logit of every 128-token group (16 lanes hold a
+// group) and the segment's sum of exp2(l * log2e / T - M), M = log2e / T * (segment
+// maximum).  Unless the workgroup is about to finish a row (which can wait on other
+// workgroups), thread 0 takes its next ticket while the loads are in flight: a
+// ticket held through such a wait would stall the rows that need that segment.
 template <bool BF16, bool VEC>
 __device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared& sm, int parity, bool prefetch) {
-    constexpr int NU = BF16 ? 8 : 4;  // 8-token units per lane
+    constexpr int NU = BF16 ? 8 : 4;        // 2048-token units per segment
+    constexpr int UT = kBlock * 8;
     const int tid = threadIdx.x, lane = tid & 63;
     const int V = a.V;
     const int seg0 = seg * (BF16 ? kSegTokensBf16 : kSegTokensF32);
-    const uint64_t ep = sm.epoch;
-    uint64_t* gslot = (uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * a.L.ng;
-    const float c2 = r.invT * 1.4426950408889634f;
+    const uint64_t ep = (uint64_t)sm.epoch << 32;
     Unit<BF16, VEC> u[NU];
 #pragma unroll
-    for (int q = 0; q < NU; ++q) load_unit<BF16, VEC>(r.ptr, V, seg0 + 8 * (q * kBlock + tid), u[q]);
-    if (tid == 0 && prefetch) sm.tick[parity ^ 1] = (int)atomicAdd(ctrl_of(a) + kCtrlTicket, 1u);
-    float mrun = -INFINITY, srun = 0.f;
+    for (int q = 0; q < NU; ++q) load_unit<BF16, VEC>(r.ptr, V, seg0 + q * UT + 8 * tid, u[q]);
+    if (tid == 0 && prefetch) sm.tick[parity ^ 1] = take_item(a, sm.queue, sm.n_queues);
+    const float c2 = r.invT * 1.4426950408889634f;
+    float mrun = kNegBig, srun = 0.f;
 #pragma unroll
     for (int q = 0; q < NU; ++q) {
-        const int base = seg0 + 8 * (q * kBlock + tid);
         float x[8];
         unpack_unit<BF16, VEC>(u[q], x);
+        const int ub = seg0 + q * UT;
+        if (ub + UT > V) {  // uniform: this unit reaches past the row
+            const int base = ub + 8 * tid;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (base + i >= V) x[i] = -INFINITY;
+        }
         const float um = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
         const float g = row16_max(um);
-        // the lowest lane of the 16-lane row holding the maximum publishes (max, position)
-        const uint64_t holders = __ballot(um == g);
-        const uint32_t rowbits = (uint32_t)(holders >> (lane & 48)) & 0xFFFFu;
-        if ((uint32_t)(lane & 15) == (uint32_t)(__ffs(rowbits) - 1) && base < V) {
-            int i = 0;
-#pragma unroll
-            for (int t = 7; t >= 0; --t)
-                if (x[t] == g) i = t;
-            const uint64_t off = (uint64_t)((lane & 15) * 8 + i);
-            st_dev(gslot + (base >> 7), (ep << 40) | (off << 32) | __float_as_uint(g));
-        }
+        if ((lane & 15) == 0) sm.gst[q * 16 + (tid >> 4)] = g;
         const float mn = fmaxf(mrun, um * c2);
-        if (mn != -INFINITY) {
-            float acc = (mrun == -INFINITY) ? 0.f : srun * __builtin_amdgcn_exp2f(mrun - mn);
+        float acc = srun * __builtin_amdgcn_exp2f(mrun - mn);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc += __builtin_amdgcn_exp2f(fmaf(x[i], c2, -mn));
-            srun = acc;
-            mrun = mn;
-        }
+        for (int i = 0; i < 8; ++i) acc += __builtin_amdgcn_exp2f(fmaf(x[i], c2, -mn));
+        srun = acc;
+        mrun = mn;
     }
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const float om = __shfl_xor(mrun, off);
-        const float os = __shfl_xor(srun, off);
-        lse_combine(mrun, srun, om, os);
-    }
+    for (int off = 32; off > 0; off >>= 1) lse_merge_finite(mrun, srun, __shfl_xor(mrun, off), __shfl_xor(srun, off));
     const int wave = tid >> 6;
     if (lane == 0) {
         sm.red_a[wave] = mrun;
         sm.red_b[wave] = srun;
     }
     __syncthreads();
+    // publish: one 64-bit slot per group and per 2048-token block (one unit each),
+    // written by consecutive lanes
+    const int g0 = seg0 >> 7;
+    if (tid < NU * 16 && g0 + tid < a.L.ng) {
+        uint64_t* gslot = (uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * a.L.ng;
+        st_dev(gslot + g0 + tid, ep | __float_as_uint(sm.gst[tid]));
+    } else if (tid >= 128 && tid < 128 + NU && (seg0 >> 11) + (tid - 128) < a.L.n3) {
+        const int q = tid - 128;
+        float mx = sm.gst[16 * q];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sm.gst[16 * q + i]);
+        uint64_t* m3slot = (uint64_t*)(a.ws + a.L.m3) + (size_t)r.row_id * a.L.n3;
+        st_dev(m3slot + (seg0 >> 11) + q, ep | __float_as_uint(mx));
+    }
+    if (tid < 64) {
+        // the segment's top group: its largest group, lowest index on ties
+        float bv = lane < NU * 16 ? sm.gst[lane] : -INFINITY;
+        int bi = lane;
+        if (lane + 64 < NU * 16 && sm.gst[lane + 64] > bv) {
+            bv = sm.gst[lane + 64];
+            bi = lane + 64;
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const float ov = __shfl_xor(bv, off);
+            const int oi = __shfl_xor(bi, off);
+            if (ov > bv || (ov == bv && oi < bi)) {
+                bv = ov;
+                bi = oi;
+            }
+        }
+        if (lane == 0) {
+            uint64_t* stop = (uint64_t*)(a.ws + a.L.stop) + (size_t)r.row_id * a.L.nseg;
+            st_dev(stop + seg, ep | (uint32_t)(bv == -INFINITY ? -1 : g0 + bi));
+        }
+    }
     if (tid == 0) {
         float m = sm.red_a[0], s = sm.red_b[0];
-        for (int w = 1; w < kBlock / 64; ++w) lse_combine(m, s, sm.red_a[w], sm.red_b[w]);
+        for (int w = 1; w < kBlock / 64; ++w) lse_merge_finite(m, s, sm.red_a[w], sm.red_b[w]);
         uint64_t* part = (uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
-        st_dev(part + seg, (ep << 32) | __float_as_uint(s));
+        st_dev(part + seg, ep | __float_as_uint(s));
     }
 }
 
@@ -514,49 +572,62 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
     if (tid == 0) {
         sm.n_l4 = sm.n_l3 = sm.n_l2 = sm.n_cand = 0;
         sm.best_key = ordered_key(INFINITY);
+        sm.key_min = 0x7FFFFFFF;
+        sm.key_max = -1;
     }
     __syncthreads();
 
-    // init: the argmax token of each top group (its logit is the group maximum) for
-    // every slot.  Tree clocks: 8 lanes per (group, slot) draw the token's path
-    // nodes in parallel and the first lane chains them into the token's clock.
-    for (int e0 = 0; e0 < kTopG * ns * 8; e0 += kBlock) {
+    // init: the seed tokens (each the largest logit of its segment, so its logit is
+    // its group's maximum) for every slot.  Tree clocks: 8 lanes per (token, slot)
+    // draw the token's path nodes in parallel and the first lane chains them into
+    // the token's clock.
+    for (int e0 = 0; e0 < kInit * ns * 8; e0 += kBlock) {
         const int e = e0 + tid;
         const int pair = e >> 3, l = e & 7;
-        const bool valid = pair < kTopG * ns;
+        const bool valid = pair < kInit * ns;
         const int w = valid ? pair / ns : 0, j = valid ? pair % ns : 0;
-        const int g = valid ? sm.topg[w] : -1;
+        const int tv = valid ? sm.init_v[w] : -1;
+        const int g = tv >= 0 ? tv >> 7 : -1;
         const uint32_t slot = (uint32_t)(r.slot0 + j);
-        const uint32_t av = (uint32_t)max(g, 0) * kGroupTokens + (uint32_t)(valid ? sm.topa[w] : 0);
+        const uint32_t av = (uint32_t)max(tv, 0);
         const float xa = g >= 0 ? gm[g] : -INFINITY;
         if constexpr (LAYOUT == 0) {
-            Words wd = Words{0u, 0u, 0u, 0u};
-            if (valid && l < 6) wd = path_draw(l, av, slot, k0, k1);
-            // chain the pair's draws in every lane (shuffles are wave-wide); lane 0 of
-            // the pair holds the token's clock at the end
-            float m = 0.f, rm = 0.f, E = 0.f;
-            uint32_t p = 0u, rp = 0u;
-#pragma unroll
-            for (int q = 0; q < 6; ++q) {
-                const int src = (tid & ~7) + q;
-                const uint32_t a0 = (uint32_t)__shfl((int)wd.w0, src);
-                const uint32_t a1 = (uint32_t)__shfl((int)wd.w1, src);
-                const uint32_t a2 = (uint32_t)__shfl((int)wd.w2, src);
-                const uint32_t a3 = (uint32_t)__shfl((int)wd.w3, src);
-                if (q == 0) {
-                    m = rm = exp1_f32(a0) / (float)V;
-                    p = rp = uniform_position(a1, a2, V);
-                } else if (q <= 4) {
-                    const int sh = path_shift(q);
-                    const uint32_t i = av >> sh, cs = i << sh, ce = node_end(sh, i, V);
-                    if (!(p >= cs && p < ce)) {
-                        m = m + exp1_f32(a0) / (float)(ce - cs);
-                        p = cs + uniform_position(a1, a2, ce - cs);
-                    }
+            // lane l of the pair turns path node l's draw into (minimum increment,
+            // position); the chain then needs two shuffles per level
+            float val = 0.f;
+            uint32_t pos = 0u;
+            if (valid && l < 6) {
+                const Words wd = path_draw(l, av, slot, k0, k1);
+                if (l == 0) {
+                    val = exp1_f32(wd.w0) / (float)V;
+                    pos = uniform_position(wd.w1, wd.w2, V);
+                } else if (l <= 4) {
+                    const int sh = path_shift(l);
+                    const uint32_t i = av >> sh, cs = i << sh, n = node_end(sh, i, V) - cs;
+                    val = exp1_f32(wd.w0) / (float)n;
+                    pos = cs + uniform_position(wd.w1, wd.w2, n);
                 } else {
-                    E = (av == p) ? m : m + exp1_f32(pick_word(a0, a1, a2, a3, av & 3u));
+                    val = exp1_f32(pick_word(wd.w0, wd.w1, wd.w2, wd.w3, av & 3u));
                 }
             }
+            const int base = tid & ~7;
+            float m = __shfl(val, base), E = 0.f;
+            uint32_t p = (uint32_t)__shfl((int)pos, base);
+            const float rm = m;
+            const uint32_t rp = p;
+#pragma unroll
+            for (int q = 1; q <= 4; ++q) {
+                const float vq = __shfl(val, base + q);
+                const uint32_t pq = (uint32_t)__shfl((int)pos, base + q);
+                const int sh = path_shift(q);
+                const uint32_t i = av >> sh, cs = i << sh, ce = node_end(sh, i, V);
+                if (!(p >= cs && p < ce)) {
+                    m = m + vq;
+                    p = pq;
+                }
+            }
+            const float v5 = __shfl(val, base + 5);
+            E = (av == p) ? m : m + v5;
             if (l == 0 && valid) {
                 if (w == 0) {
                     sm.root_m[j] = rm;
@@ -650,6 +721,23 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
     // tree clocks 8 lanes per candidate draw its path nodes in parallel.
     const float best = ordered_value(sm.best_key);
     const int nc = min(sm.n_cand, kCandCap);
+    {
+        // A single candidate within the margin of the best is the winner: float32
+        // scores err by far less than the margin, and every token that was not kept
+        // scored above it.
+        static_assert(kCandCap <= kBlock, "one candidate per thread");
+        const bool in = tid < nc && sm.cand_s[tid] <= best + kMargin;
+        if (in) {
+            const int key = sm.cand_v[tid] * 32 + sm.cand_j[tid];  // token < 2^19, slot < 32
+            atomicMin(&sm.key_min, key);
+            atomicMax(&sm.key_max, key);
+            sm.win_token = sm.cand_v[tid];
+            sm.win_slot = sm.cand_j[tid];
+        }
+        __syncthreads();
+        if (sm.key_min == sm.key_max) return;  // one (token, slot), possibly listed twice
+        __syncthreads();
+    }
     double bs = INFINITY;
     int bv = 0x7FFFFFFF, bj = 0x7FFFFFFF;
     for (int e0 = 0; e0 < nc * 8; e0 += kBlock) {
@@ -734,14 +822,29 @@ __device__ int walk_draft(const RaceArgs& a, int b, int k, int s, uint32_t ep) {
 }
 
 // Realised-path walk of sequence b; every token it reads carries this call's epoch.
-__device__ void walk(const RaceArgs& a, int b, uint32_t ep) {
-    const int K = a.K, G = a.gamma;
+// Called by every thread: the tokens the walk may read are fetched in parallel
+// first (into the candidate arrays, free once the race is decided); thread 0 walks.
+__device__ void walk(const RaceArgs& a, Shared& sm, int b, uint32_t ep) {
+    const int K = a.K, G = a.gamma, tid = threadIdx.x;
+    const int ntp = a.target_rows == 1 ? 1 : K;
+    const int nt = ntp * (G + 1), n = nt + K * G;
+    const bool staged = n <= kCandCap;
+    if (staged) {
+        for (int e = tid; e < n; e += kBlock)
+            sm.cand_v[e] = e < nt ? wait_token(a, target_row_id(a, b, e / (G + 1), e % (G + 1)), ep)
+                                  : walk_draft(a, b, (e - nt) / G, (e - nt) % G, ep);
+        __syncthreads();
+    }
+    if (tid != 0) return;
+    auto target = [&](int k, int s) {
+        return staged ? sm.cand_v[(ntp == 1 ? 0 : k) * (G + 1) + s] : wait_token(a, target_row_id(a, b, k, s), ep);
+    };
+    auto draft = [&](int k, int s) { return staged ? sm.cand_v[nt + k * G + s] : walk_draft(a, b, k, s, ep); };
     uint32_t act = K >= 32 ? 0xFFFFFFFFu : ((1u << K) - 1u);
     int tau = 0;
     bool done = false;
     for (int s = 0; s < G && !done; ++s) {
-        const int kk = __ffs((int)act) - 1;
-        const int y = wait_token(a, target_row_id(a, b, kk, s), ep);
+        const int y = target(__ffs((int)act) - 1, s);
         a.out_tokens[(size_t)b * (G + 1) + s] = y;
         tau = s + 1;
         if (y < 0) {
@@ -750,7 +853,7 @@ __device__ void walk(const RaceArgs& a, int b, uint32_t ep) {
         }
         uint32_t na = 0u;
         for (int k = 0; k < K; ++k)
-            if (((act >> k) & 1u) && walk_draft(a, b, k, s, ep) == y) na |= 1u << k;
+            if (((act >> k) & 1u) && draft(k, s) == y) na |= 1u << k;
         if (!na) {
             done = true;
             break;
@@ -758,8 +861,7 @@ __device__ void walk(const RaceArgs& a, int b, uint32_t ep) {
         act = na;
     }
     if (!done) {
-        const int kk = __ffs((int)act) - 1;
-        a.out_tokens[(size_t)b * (G + 1) + G] = wait_token(a, target_row_id(a, b, kk, G), ep);
+        a.out_tokens[(size_t)b * (G + 1) + G] = target(__ffs((int)act) - 1, G);
         tau = G + 1;
     }
     for (int s = tau; s <= G; ++s) a.out_tokens[(size_t)b * (G + 1) + s] = -1;
@@ -775,8 +877,26 @@ __device__ __forceinline__ int path_token(const RaceArgs& a, const Row& r, int d
     return a.draft_tokens[((size_t)r.b * a.K + r.k) * a.gamma + d];
 }
 
+// Row whose race publishes this row's context key (-1: the key is folded here, all
+// its tokens being known before the call).  The key of depth s of a path is
+// finished by the race at depth s - 1, which alone knows the newest token.
+__device__ __forceinline__ int key_producer(const RaceArgs& a, const Row& r) {
+    if (a.m == 0 || r.s == 0) return -1;
+    if (r.kind == 1 && a.target_rows == 1) return target_row_id(a, r.b, 0, r.s - 1);
+    if (a.s_count > 0 && r.s - 1 >= a.s_begin && r.s - 1 < a.s_begin + a.s_count)
+        return draft_row_id(a, r.b, r.k, r.s - 1);
+    return -1;
+}
+
+// Whether this row's race publishes the context key of the next depth of its path.
+__device__ __forceinline__ bool key_consumer(const RaceArgs& a, const Row& r) {
+    if (a.m == 0) return false;
+    if (r.kind == 1) return a.target_rows == 1 && r.s + 1 <= a.gamma;
+    return r.s + 1 < a.s_begin + a.s_count || (a.target_rows > 1 && r.s + 1 <= a.gamma);
+}
+
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* gm, uint8_t* ga) {
+__device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* gm) {
     // The race is a latency chain (the next depth of this path waits for it) while
     // the other waves on the same SIMDs stream: raise this wave's issue priority.
     __builtin_amdgcn_s_setprio(3);
@@ -786,59 +906,91 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
     const uint32_t ep = sm.epoch;
     const float c2 = r.invT * 1.4426950408889634f;
 
-    // ---- gather the row's slots (waves 0-2) while wave 3 folds the context key,
-    // waiting for path tokens as they are published (normally only the newest).
-    if (wave < 3) {
-        const uint64_t* gslot = (const uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * ng;
-        for (int g = tid; g < ng; g += 192) {
-            const uint64_t v = wait_slot(a, gslot + g, ep, 40);
-            gm[g] = __uint_as_float((uint32_t)v);
-            ga[g] = (uint8_t)(v >> 32);
-        }
-    } else if (lane == 0) {
-        uint32_t k0 = (uint32_t)a.key, k1 = (uint32_t)(a.key >> 32);
-        const uint64_t t = (uint64_t)(a.start_pos[r.b] + r.s);
-        fold(k0, k1, (uint32_t)t, (uint32_t)(t >> 32), 0u);
-        for (int i = 0; i < a.m; ++i) {
-            const int idx = r.s + i;  // position in prefix (m tokens) || path (s tokens)
-            const int tk = idx < a.m ? a.prefix[(size_t)r.b * a.m + idx] : path_token(a, r, idx - a.m, ep);
-            fold(k0, k1, (uint32_t)tk, (uint32_t)i, 1u);
-        }
-        sm.kappa0 = k0;
-        sm.kappa1 = k1;
-    }
-    __syncthreads();
-    for (int t = tid; t < n3; t += kBlock) {
-        float mx = -INFINITY;
-        for (int g = 16 * t; g < min(ng, 16 * t + 16); ++g) mx = fmaxf(mx, gm[g]);
-        sm.m3[t] = mx;
-    }
+    // ---- gather the row's slots (group maxima, block maxima, segment top tokens):
+    // a batch of loads in flight per thread, then a wait only for slots not yet
+    // published.
     {
-        // wave w keeps the largest group among g = w (mod 4) (lowest index on ties);
-        // together the four hold the row maximum.
-        float bv = -INFINITY;
-        int bi = -1;
-        for (int g = wave + 4 * lane; g < ng; g += 256)
-            if (gm[g] > bv) {
-                bv = gm[g];
-                bi = g;
+        const uint64_t* gslot = (const uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * ng;
+        const uint64_t* m3slot = (const uint64_t*)(a.ws + a.L.m3) + (size_t)r.row_id * n3;
+        const uint64_t* stop = (const uint64_t*)(a.ws + a.L.stop) + (size_t)r.row_id * a.L.nseg;
+        const int ne = ng + n3 + a.L.nseg;
+        for (int e0 = 0; e0 < ne; e0 += 4 * kBlock) {
+            const uint64_t* src[4];
+            uint64_t v[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int e = e0 + i * kBlock + tid;
+                src[i] = e < ng ? gslot + e : e < ng + n3 ? m3slot + (e - ng) : stop + min(e - ng - n3, a.L.nseg - 1);
+                v[i] = e < ne ? ld_dev(src[i]) : 0;
             }
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-            const float ov = __shfl_xor(bv, off);
-            const int oi = __shfl_xor(bi, off);
-            if (ov > bv || (ov == bv && oi >= 0 && (bi < 0 || oi < bi))) {
-                bv = ov;
-                bi = oi;
+            for (int i = 0; i < 4; ++i) {
+                const int e = e0 + i * kBlock + tid;
+                if (e < ne) {
+                    if ((uint32_t)(v[i] >> 32) != ep) v[i] = wait_slot(a, src[i], ep);
+                    const uint32_t w = (uint32_t)v[i];
+                    if (e < ng)
+                        gm[e] = __uint_as_float(w);
+                    else if (e < ng + n3)
+                        sm.m3[e - ng] = __uint_as_float(w);
+                    else
+                        sm.stop[e - ng - n3] = (int)w;
+                }
             }
-        }
-        if (lane == 0) {
-            sm.topg[wave] = (bv == -INFINITY) ? -1 : bi;
-            sm.topa[wave] = bi >= 0 ? ga[bi] : 0;
-            sm.red_a[wave] = bv;
         }
     }
     __syncthreads();
+
+    // ---- key-independent work: the race's seed tokens (the largest token of each
+    // segment's top group, at most kInit of the largest groups), level-4 maxima,
+    // LSE, row maximum.
+    if (wave == 0) {
+        float bv = -INFINITY;
+        int bt = 0x7FFFFFFF;
+        if (lane < a.L.nseg && sm.stop[lane] >= 0) {
+            bt = sm.stop[lane];
+            bv = gm[bt];
+        }
+        if (a.L.nseg <= kInit) {
+            if (lane < kInit) sm.init_v[lane] = bv == -INFINITY ? -1 : bt;
+        } else {
+            for (int i = 0; i < kInit; ++i) {
+                float mv = bv;
+                int mt = bt;
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    const float ov = __shfl_xor(mv, off);
+                    const int ot = __shfl_xor(mt, off);
+                    if (ov > mv || (ov == mv && ot < mt)) {
+                        mv = ov;
+                        mt = ot;
+                    }
+                }
+                if (lane == 0) sm.init_v[i] = mv == -INFINITY ? -1 : mt;
+                if (bt == mt) bv = -INFINITY;
+            }
+        }
+    }
+    __syncthreads();
+    {
+        // 32 lanes per seed group, 4 tokens each: the group's lowest token holding its maximum
+        static_assert(kInit * 32 == kBlock, "one pass over the seed groups");
+        const int i = tid >> 5, sub = tid & 31;
+        const int g = sm.init_v[i];
+        int tk = 0x7FFFFFFF;
+        if (g >= 0) {
+            const float gmax = gm[g];
+#pragma unroll
+            for (int t = 3; t >= 0; --t) {
+                const int v = g * kGroupTokens + 4 * sub + t;
+                if (v < a.V && load_logit<BF16>(r.ptr, v) == gmax) tk = v;
+            }
+        }
+#pragma unroll
+        for (int off = 16; off > 0; off >>= 1) tk = min(tk, __shfl_xor(tk, off));
+        __syncthreads();
+        if (sub == 0) sm.init_v[i] = g >= 0 && tk != 0x7FFFFFFF ? tk : -1;
+    }
     if (tid < n4) {
         float mx = -INFINITY;
         for (int t = 16 * tid; t < min(n3, 16 * tid + 16); ++t) mx = fmaxf(mx, sm.m3[t]);
@@ -850,8 +1002,7 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         constexpr int per = (BF16 ? kSegTokensBf16 : kSegTokensF32) / 2048;  // level-3 blocks per segment
         float mi = -INFINITY, si = 0.f;
         if (lane < a.L.nseg) {
-            const uint64_t v =
-                wait_slot(a, (const uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg + lane, ep, 32);
+            const uint64_t v = wait_slot(a, (const uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg + lane, ep);
             float gmx = -INFINITY;
             for (int t = lane * per; t < min(n3, lane * per + per); ++t) gmx = fmaxf(gmx, sm.m3[t]);
             mi = gmx * c2;
@@ -874,10 +1025,52 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
             }
         }
     }
+    // ---- context keys.  Wave 3 fetches window tokens in parallel -- lanes [0, m)
+    // this row's own window (when no race of this call publishes its key), lanes
+    // [m, 2m - 1) the next depth's window without its newest token (when this race
+    // publishes the next key); positions index prefix (m tokens) || path -- and
+    // folds both chains at once: lane 0 this row's key, lane 1 the next depth's key
+    // up to its newest token (the winner of this race).  Meanwhile thread 0 waits
+    // for the key published by the race one depth up this path, if any.
+    const int prod = key_producer(a, r);
+    const bool cons = key_consumer(a, r);
+    if (wave == 3) {
+        int idx = -1;
+        if (lane < a.m && prod < 0)
+            idx = r.s + lane;
+        else if (lane >= a.m && lane < 2 * a.m - 1 && cons)
+            idx = r.s + 1 + (lane - a.m);
+        int tk = 0;
+        if (idx >= 0) tk = idx < a.m ? a.prefix[(size_t)r.b * a.m + idx] : path_token(a, r, idx - a.m, ep);
+        const uint64_t t = (uint64_t)(a.start_pos[r.b] + r.s) + (uint64_t)(lane == 1);
+        uint32_t c0 = (uint32_t)a.key, c1 = (uint32_t)(a.key >> 32);
+        const bool chain = (lane == 0 && prod < 0) || (lane == 1 && cons);
+        if (chain) fold(c0, c1, (uint32_t)t, (uint32_t)(t >> 32), 0u);
+        for (int i = 0; i < a.m; ++i) {
+            const int w = __shfl(tk, lane == 0 ? i : a.m + i);
+            if (chain && (lane == 0 || i + 1 < a.m)) fold(c0, c1, (uint32_t)w, (uint32_t)i, 1u);
+        }
+        if (lane == 0 && prod < 0) {
+            sm.kappa0 = c0;
+            sm.kappa1 = c1;
+        }
+        if (lane == 1 && cons) {
+            sm.next0 = c0;
+            sm.next1 = c1;
+        }
+    }
     if (tid == 0) {
         float mx = -INFINITY;
-        for (int w = 0; w < kBlock / 64; ++w) mx = fmaxf(mx, sm.red_a[w]);
+        for (int t = 0; t < n3; ++t) mx = fmaxf(mx, sm.m3[t]);
         sm.rowmax = mx;
+        if (prod >= 0) {
+            const uint64_t* ks = (const uint64_t*)(a.ws + a.L.keys) + 2 * (size_t)prod;
+            uint64_t w0 = ld_dev(ks), w1 = ld_dev(ks + 1);
+            if ((uint32_t)(w0 >> 32) != ep) w0 = wait_slot(a, ks, ep);
+            if ((uint32_t)(w1 >> 32) != ep) w1 = wait_slot(a, ks + 1, ep);
+            sm.kappa0 = (uint32_t)w0;
+            sm.kappa1 = (uint32_t)w1;
+        }
     }
     __syncthreads();
     const uint32_t k0 = sm.kappa0, k1 = sm.kappa1;
@@ -892,6 +1085,13 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
     }
     if (tid == 0) {
         const int y = sm.win_token;
+        if (cons) {
+            uint32_t n0 = sm.next0, n1 = sm.next1;
+            fold(n0, n1, (uint32_t)y, (uint32_t)(a.m - 1), 1u);
+            uint64_t* ks = (uint64_t*)(a.ws + a.L.keys) + 2 * (size_t)r.row_id;
+            st_dev(ks, ((uint64_t)ep << 32) | n0);
+            st_dev(ks + 1, ((uint64_t)ep << 32) | n1);
+        }
         st_dev((uint64_t*)(a.ws + a.L.tok) + r.row_id, ((uint64_t)ep << 32) | (uint32_t)y);
         if (r.kind == 0) {
             a.draft_tokens[((size_t)r.b * a.K + r.k) * a.gamma + r.s] = y;
@@ -900,9 +1100,9 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
                                                 : ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + r.s;
             a.target_tokens[o] = y;
         }
-        // The last row of a sequence in ticket order walks its block.
-        if (r.kind == 1 && r.s == a.gamma && (a.target_rows == 1 || r.k == a.K - 1)) walk(a, r.b, ep);
     }
+    // The last row of a sequence in the work order walks its block.
+    if (r.kind == 1 && r.s == a.gamma && (a.target_rows == 1 || r.k == a.K - 1)) walk(a, sm, r.b, ep);
     __builtin_amdgcn_s_setprio(0);
 }
 
@@ -913,14 +1113,16 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Shared& sm = *reinterpret_cast<Shared*>(smem_raw);
     float* gm = reinterpret_cast<float*>(smem_raw + ((sizeof(Shared) + 15) & ~(size_t)15));
-    uint8_t* ga = reinterpret_cast<uint8_t*>(gm + a.L.ng);
     const int tid = threadIdx.x;
     uint32_t* ctrl = ctrl_of(a);
     const size_t esize = BF16 ? 2 : 4;
     const int D = a.B * a.K * a.gamma;
     if (tid == 0) {
-        sm.epoch = ld_dev(ctrl + kCtrlEpoch) % 0xFFFFFFu + 1u;  // 1 .. 2^24-1
-        sm.tick[0] = (int)atomicAdd(ctrl + kCtrlTicket, 1u);
+        const uint32_t last = ld_dev(ctrl + kCtrlEpoch);
+        sm.epoch = last == 0xFFFFFFFFu ? 1u : last + 1u;  // 1 .. 2^32-1
+        sm.n_queues = min((int)gridDim.x, kMaxQueues);
+        sm.queue = (int)(blockIdx.x % (unsigned)sm.n_queues);
+        sm.tick[0] = take_item(a, sm.queue, sm.n_queues);
     }
     __syncthreads();
     for (int parity = 0;; parity ^= 1) {
@@ -968,23 +1170,23 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
         stream_segment<BF16, VEC>(a, r, seg, sm, parity, !last);
         // the workgroup holding the row's last segment (highest ticket) finishes it
         if (last) {
-            finish_row<BF16, VEC, LAYOUT>(a, r, sm, gm, ga);
-            if (tid == 0) sm.tick[parity ^ 1] = (int)atomicAdd(ctrl + kCtrlTicket, 1u);
+            finish_row<BF16, VEC, LAYOUT>(a, r, sm, gm);
+            if (tid == 0) sm.tick[parity ^ 1] = take_item(a, sm.queue, sm.n_queues);
         }
         __syncthreads();
     }
-    // The last workgroup to leave resets the ticket and advances the epoch.
+    // The last workgroup to leave resets the queues and advances the epoch.
     if (tid == 0) {
         const uint32_t old = __hip_atomic_fetch_add(ctrl + kCtrlExited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (old == gridDim.x - 1) {
-            st_dev(ctrl + kCtrlTicket, 0u);
+            for (int q = 0; q < kMaxQueues; ++q) st_dev(ctrl + ctrl_queue(q), 0u);
             st_dev(ctrl + kCtrlExited, 0u);
             st_dev(ctrl + kCtrlEpoch, sm.epoch);
         }
     }
 }
 
-size_t shared_bytes(int ng) { return ((sizeof(Shared) + 15) & ~(size_t)15) + (size_t)ng * (sizeof(float) + 1); }
+size_t shared_bytes(int ng) { return ((sizeof(Shared) + 15) & ~(size_t)15) + (size_t)ng * sizeof(float); }
 
 template <bool BF16, bool VEC, int LAYOUT>
 hipError_t launch_one(const RaceArgs& a, hipStream_t stream) {
