@@ -83,18 +83,40 @@ psd::RaceArgs base_args(const psd_params* p, const psd_block* b) {
     return a;
 }
 
-// Depth-major item table: at depth d, draft rows (if d is drafted) then target rows.
+// Work order.  Every row comes after the rows whose races it waits for.  With a
+// shared target chain and drafts in the same call, the two chains are
+// independent: the target rows (depth by depth) go first, so the longer chain
+// starts early, then the drafts depth by depth, and each sequence's last draft
+// row walks its block.  Otherwise rows go depth by depth, drafts before targets.
 void build_depths(psd::RaceArgs& a, int n_depth) {
-    int first = 0;
-    a.n_depth = n_depth;
-    for (int d = 0; d < n_depth; ++d) {
-        const int nd = (a.s_count > 0 && d >= a.s_begin && d < a.s_begin + a.s_count) ? a.B * a.K : 0;
-        const int nt = (a.target_rows > 0 && d <= a.gamma) ? a.B * a.target_rows : 0;
-        a.depth_first[d] = first;
-        a.depth_nd[d] = nd;
-        a.depth_nt[d] = nt;
+    int first = 0, n = 0;
+    auto add = [&](int d, int nd, int nt) {
+        if (nd + nt == 0) return;
+        a.phase_first[n] = first;
+        a.phase_depth[n] = d;
+        a.phase_nd[n] = nd;
+        a.phase_nt[n] = nt;
         first += (nd + nt) * a.L.nseg;
+        ++n;
+    };
+    const bool targets_first = a.target_rows == 1 && a.s_count > 0;
+    if (targets_first) {
+        for (int d = 0; d <= a.gamma; ++d) add(d, 0, a.B);
+        for (int d = a.s_begin; d < a.s_begin + a.s_count; ++d) add(d, a.B * a.K, 0);
+        a.walk_kind = 0;
+        a.walk_s = a.s_begin + a.s_count - 1;
+        a.walk_k = a.K - 1;
+    } else {
+        for (int d = 0; d < n_depth; ++d) {
+            const int nd = (a.s_count > 0 && d >= a.s_begin && d < a.s_begin + a.s_count) ? a.B * a.K : 0;
+            const int nt = (a.target_rows > 0 && d <= a.gamma) ? a.B * a.target_rows : 0;
+            add(d, nd, nt);
+        }
+        a.walk_kind = a.target_rows > 0 ? 1 : -1;
+        a.walk_s = a.gamma;
+        a.walk_k = a.target_rows == 1 ? 0 : a.K - 1;
     }
+    a.n_phase = n;
     a.n_items = first;
     a.n_rows = first / a.L.nseg;
 }

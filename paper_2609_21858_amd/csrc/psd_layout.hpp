@@ -11,6 +11,7 @@ constexpr int kBlock = 256;             // threads per workgroup (4 wave64)
 constexpr int kSegTokensBf16 = 16384;   // tokens per work item: 32 KiB of bf16
 constexpr int kSegTokensF32 = 8192;     // 32 KiB of float32
 constexpr int kMaxDepth = 33;           // gamma + 1 <= 33
+constexpr int kMaxPhases = 2 * kMaxDepth;
 
 inline int seg_tokens(int dtype_bf16) { return dtype_bf16 ? kSegTokensBf16 : kSegTokensF32; }
 
@@ -98,11 +99,16 @@ struct RaceArgs {
     int s_begin, s_count;       // draft depths computed in this call (s_count = 0: none)
     int target_rows;            // 0: no target rows, 1: shared, K: per path
     int n_items;                // rows * nseg
-    int n_rows;                 // rows of this call (depth-major)
-    int n_depth;
-    int depth_first[kMaxDepth]; // first item of depth d
-    int depth_nd[kMaxDepth];    // draft rows at depth d
-    int depth_nt[kMaxDepth];    // target rows at depth d
+    int n_rows;                 // rows of this call
+    // Work order: phases of rows, each at one depth: phase_nd draft rows, then
+    // phase_nt target rows; a phase's items start at phase_first.
+    int n_phase;
+    int phase_first[kMaxPhases];
+    int phase_depth[kMaxPhases];
+    int phase_nd[kMaxPhases];
+    int phase_nt[kMaxPhases];
+    // the row of each sequence that walks its block: (kind, depth, path); kind -1: none
+    int walk_kind, walk_s, walk_k;
 };
 
 }  // namespace psd

@@ -49,8 +49,8 @@ constexpr int kInit = 8;                   // seed tokens of a race (segment top
 constexpr int kL4Cap = 512;                // <= 32 slots x 16 level-4 nodes
 constexpr int kL3Cap = 512;
 constexpr int kL2Cap = 512;
+constexpr int kRowEntries = 1;
 constexpr int kCandCap = 256;
-constexpr int kRowEntries = 1;             // group entries per 16-lane row per evaluation pass
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
 constexpr uint32_t kSpinLimit = 1u << 22;  // bounded waits for other workgroups' slots
 constexpr uint32_t kErrSpin = 1u, kErrCand = 2u;
@@ -73,8 +73,6 @@ struct Shared {
     int cand_j[kCandCap];
     float cand_s[kCandCap];
     float cand_x[kCandCap];
-    float root_m[32];
-    uint32_t root_p[32];
     double red_s[kBlock / 64];
     int red_v[kBlock / 64];
     int red_j[kBlock / 64];
@@ -197,22 +195,29 @@ struct Unit {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint4 ld_stream(const void* p) {
-    const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
-    return make_uint4(v.x, v.y, v.z, v.w);
+template <bool NT>
+__device__ __forceinline__ uint4 ld16(const void* p) {
+    if constexpr (NT) {
+        const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+        return make_uint4(v.x, v.y, v.z, v.w);
+    } else {
+        return *(const uint4*)p;
+    }
 }
 
 // Vector path: the address is clamped into the row (V * element size is a multiple
 // of 16 bytes there), so every load is unconditional and the compiler can wait for
-// them one by one; words past V are masked by the caller (mask_tail).
-template <bool BF16, bool VEC>
+// them one by one; words past V are left for the caller to mask.  NT: streaming
+// (non-temporal) loads for the single pass over the logits; re-reads of a few
+// groups use ordinary loads.
+template <bool BF16, bool VEC, bool NT = true>
 __device__ __forceinline__ void load_unit(const unsigned char* row, int V, int base, Unit<BF16, VEC>& u) {
     if constexpr (VEC) {
         if constexpr (BF16) {
-            u.w[0] = ld_stream((const uint16_t*)row + min(base, V - 8));
+            u.w[0] = ld16<NT>((const uint16_t*)row + min(base, V - 8));
         } else {
-            u.w[0] = ld_stream((const float*)row + min(base, V - 4));
-            u.w[1] = ld_stream((const float*)row + min(base + 4, V - 4));
+            u.w[0] = ld16<NT>((const float*)row + min(base, V - 4));
+            u.w[1] = ld16<NT>((const float*)row + min(base + 4, V - 4));
         }
     } else {
         float x[8];
@@ -545,18 +550,17 @@ __device__ __forceinline__ bool lex_less(double s, int v, int j, double s2, int 
     return s < s2 || (s == s2 && (v < v2 || (v == v2 && j < j2)));
 }
 
-// Philox words of path node l of token v (tree clocks): 0 = root, 1..4 = the
-// token's level-4..1 ancestors, 5 = the token's own word block.
-__device__ __forceinline__ Words path_draw(int l, uint32_t v, uint32_t slot, uint32_t k0, uint32_t k1) {
-    if (l == 0) return philox(0u, slot, 5u, kDomainTree, k0, k1);
-    if (l == 5) return philox(v >> 3, slot, 8u + ((v >> 2) & 1u), kDomainTree, k0, k1);
-    const int level = 5 - l;  // 4, 3, 2, 1
-    const int sh = level == 4 ? kShift4 : level == 3 ? kShift3 : level == 2 ? kShift2 : kShift1;
-    return philox(v >> sh, slot, (uint32_t)level, kDomainTree, k0, k1);
-}
-
 __device__ __forceinline__ int path_shift(int l) {
     return l == 1 ? kShift4 : l == 2 ? kShift3 : l == 3 ? kShift2 : kShift1;
+}
+
+// Philox words of path node l of token v (tree clocks): 0 = root, 1..4 = the
+// token's level-4..1 ancestors, 5 = the token's own word block.  The counter is
+// selected per lane, so lanes of one token draw their nodes in a single call.
+__device__ __forceinline__ Words path_draw(int l, uint32_t v, uint32_t slot, uint32_t k0, uint32_t k1) {
+    const uint32_t c0 = l == 0 ? 0u : l == 5 ? v >> 3 : v >> path_shift(l);
+    const uint32_t c2 = l == 0 ? 5u : l == 5 ? 8u + ((v >> 2) & 1u) : (uint32_t)(5 - l);
+    return philox(c0, slot, c2, kDomainTree, k0, k1);
 }
 
 __device__ __forceinline__ uint32_t pick_word(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3, uint32_t i) {
@@ -565,146 +569,127 @@ __device__ __forceinline__ uint32_t pick_word(uint32_t a0, uint32_t a1, uint32_t
 
 template <bool BF16, bool VEC, int LAYOUT>
 __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
+    // (lists, candidates and the best score were reset by the caller)
     const int tid = threadIdx.x;
     const uint32_t V = (uint32_t)a.V;
     const int ng = a.L.ng;
     const int ns = r.nslots;
-    if (tid == 0) {
-        sm.n_l4 = sm.n_l3 = sm.n_l2 = sm.n_cand = 0;
-        sm.best_key = ordered_key(INFINITY);
-        sm.key_min = 0x7FFFFFFF;
-        sm.key_max = -1;
-    }
-    __syncthreads();
-
-    // init: the seed tokens (each the largest logit of its segment, so its logit is
-    // its group's maximum) for every slot.  Tree clocks: 8 lanes per (token, slot)
-    // draw the token's path nodes in parallel and the first lane chains them into
-    // the token's clock.
-    for (int e0 = 0; e0 < kInit * ns * 8; e0 += kBlock) {
+    const int n4 = (int)((V + (1u << kShift4) - 1) >> kShift4);
+    // Pass A: the seed tokens (each the largest logit of its group) in every slot --
+    // tree clocks: 8 lanes per (token, slot), lane l drawing path node l -- and, for
+    // tree clocks, the minimum of every (slot, level-4 node), one item per lane.
+    const int nseed = kInit;
+    const int seed_lanes = nseed * ns * 8;
+    const int nA = seed_lanes + (LAYOUT == 0 ? ns * n4 : 0);
+    for (int e0 = 0; e0 < nA; e0 += kBlock) {
         const int e = e0 + tid;
-        const int pair = e >> 3, l = e & 7;
-        const bool valid = pair < kInit * ns;
-        const int w = valid ? pair / ns : 0, j = valid ? pair % ns : 0;
-        const int tv = valid ? sm.init_v[w] : -1;
-        const int g = tv >= 0 ? tv >> 7 : -1;
-        const uint32_t slot = (uint32_t)(r.slot0 + j);
-        const uint32_t av = (uint32_t)max(tv, 0);
-        const float xa = g >= 0 ? gm[g] : -INFINITY;
-        if constexpr (LAYOUT == 0) {
-            // lane l of the pair turns path node l's draw into (minimum increment,
-            // position); the chain then needs two shuffles per level
-            float val = 0.f;
-            uint32_t pos = 0u;
-            if (valid && l < 6) {
-                const Words wd = path_draw(l, av, slot, k0, k1);
-                if (l == 0) {
-                    val = exp1_f32(wd.w0) / (float)V;
-                    pos = uniform_position(wd.w1, wd.w2, V);
-                } else if (l <= 4) {
+        if (e < seed_lanes) {  // whole 8-lane groups: the shuffles stay within active lanes
+            const int pair = e >> 3, l = e & 7;
+            const int w = pair / ns, j = pair % ns;
+            const int tv = sm.init_v[w];
+            const int g = tv >= 0 ? tv >> 7 : -1;
+            const uint32_t slot = (uint32_t)(r.slot0 + j);
+            const uint32_t av = (uint32_t)max(tv, 0);
+            const float xa = g >= 0 ? gm[g] : -INFINITY;
+            if constexpr (LAYOUT == 0) {
+                // lane l turns node l's draw into (minimum increment, position): root
+                // E'/V, level-4..1 node E'/size at a uniform position in it, token E'
+                float val = 0.f;
+                uint32_t pos = 0u;
+                if (l < 6) {
+                    const Words wd = path_draw(l, av, slot, k0, k1);
                     const int sh = path_shift(l);
-                    const uint32_t i = av >> sh, cs = i << sh, n = node_end(sh, i, V) - cs;
-                    val = exp1_f32(wd.w0) / (float)n;
+                    const uint32_t cs = (l == 0 || l == 5) ? 0u : (av >> sh) << sh;
+                    const uint32_t n = l == 0 ? V : l == 5 ? 1u : node_end(sh, av >> sh, V) - cs;
+                    val = exp1_f32(l == 5 ? pick_word(wd.w0, wd.w1, wd.w2, wd.w3, av & 3u) : wd.w0) / (float)n;
                     pos = cs + uniform_position(wd.w1, wd.w2, n);
-                } else {
-                    val = exp1_f32(pick_word(wd.w0, wd.w1, wd.w2, wd.w3, av & 3u));
                 }
-            }
-            const int base = tid & ~7;
-            float m = __shfl(val, base), E = 0.f;
-            uint32_t p = (uint32_t)__shfl((int)pos, base);
-            const float rm = m;
-            const uint32_t rp = p;
+                const int base = tid & ~7;
+                float m = __shfl(val, base);
+                uint32_t p = (uint32_t)__shfl((int)pos, base);
 #pragma unroll
-            for (int q = 1; q <= 4; ++q) {
-                const float vq = __shfl(val, base + q);
-                const uint32_t pq = (uint32_t)__shfl((int)pos, base + q);
-                const int sh = path_shift(q);
-                const uint32_t i = av >> sh, cs = i << sh, ce = node_end(sh, i, V);
-                if (!(p >= cs && p < ce)) {
-                    m = m + vq;
-                    p = pq;
+                for (int q = 1; q <= 4; ++q) {
+                    const float vq = __shfl(val, base + q);
+                    const uint32_t pq = (uint32_t)__shfl((int)pos, base + q);
+                    const int sh = path_shift(q);
+                    const uint32_t i = av >> sh, cs = i << sh, ce = node_end(sh, i, V);
+                    if (!(p >= cs && p < ce)) {
+                        m = m + vq;
+                        p = pq;
+                    }
                 }
-            }
-            const float v5 = __shfl(val, base + 5);
-            E = (av == p) ? m : m + v5;
-            if (l == 0 && valid) {
-                if (w == 0) {
-                    sm.root_m[j] = rm;
-                    sm.root_p[j] = rp;
-                }
-                if (g >= 0) {
+                const float v5 = __shfl(val, base + 5);
+                const float E = (av == p) ? m : m + v5;
+                if (l == 0 && g >= 0) {
                     const float sc = ln_f32(E) - xa * r.invT;
                     if (sc < INFINITY) {
                         atomicMin(&sm.best_key, ordered_key(sc));
                         push_candidate(sm, a, (int)av, (int)slot, sc, xa);
                     }
                 }
-            }
-        } else {
-            if (l == 0 && g >= 0) {
-                const Words wd = philox(av >> 2, slot, 0u, kDomainFlat, k0, k1);
-                const float s = ln_f32(exp1_f32(word_at(wd, av & 3u))) - xa * r.invT;
-                if (s < INFINITY) {
-                    atomicMin(&sm.best_key, ordered_key(s));
-                    push_candidate(sm, a, (int)av, (int)slot, s, xa);
-                }
-            }
-        }
-    }
-    __syncthreads();
-    if (tid == 0) compact_candidates(sm);
-    __syncthreads();
-
-    if constexpr (LAYOUT == 0) {
-        // descent: level-4 children of the roots.
-        const int n4 = (int)((V + (1u << kShift4) - 1) >> kShift4);
-        for (int e = tid; e < ns * n4; e += kBlock) {
-            const int j = e / n4;
-            const uint32_t i4 = (uint32_t)(e % n4);
-            const float thr = current_threshold(sm);
-            if (ln_f32(sm.root_m[j]) - sm.m4[i4] * r.invT > thr) continue;
-            const uint32_t slot = (uint32_t)(r.slot0 + j);
-            float m;
-            uint32_t p;
-            child_min_f32(sm.root_m[j], sm.root_p[j], 4, i4, node_start(kShift4, i4), node_end(kShift4, i4, V), slot,
-                          k0, k1, m, p);
-            if (ln_f32(m) - sm.m4[i4] * r.invT <= thr) push_node(sm.l4, &sm.n_l4, kL4Cap, (slot << 20) | i4, m, p);
-        }
-        __syncthreads();
-        // level-3 children of the surviving level-4 nodes.
-        const int n3tot = min(sm.n_l4, kL4Cap) * 16;
-        const int n3 = (ng + 15) / 16;
-        for (int base = 0; base < n3tot; base += kBlock) {
-            const bool flush = sm.n_l3 > kL3Cap - kBlock;
-            __syncthreads();
-            if (flush) flush_l3<BF16, VEC>(a, r, sm, gm, k0, k1);
-            const int e = base + tid;
-            if (e < n3tot) {
-                const Node pa = sm.l4[e >> 4];
-                const uint32_t i3 = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
-                if ((int)i3 < n3) {
-                    const float thr = current_threshold(sm);
-                    if (ln_f32(pa.m) - sm.m3[i3] * r.invT <= thr) {
-                        const uint32_t slot = pa.id >> 20;
-                        float m;
-                        uint32_t p;
-                        child_min_f32(pa.m, pa.p, 3, i3, i3 << kShift3, node_end(kShift3, i3, V), slot, k0, k1, m, p);
-                        if (ln_f32(m) - sm.m3[i3] * r.invT <= thr)
-                            push_node(sm.l3, &sm.n_l3, kL3Cap, (slot << 20) | i3, m, p);
+            } else {
+                if (l == 0 && g >= 0) {
+                    const Words wd = philox(av >> 2, slot, 0u, kDomainFlat, k0, k1);
+                    const float sc = ln_f32(exp1_f32(word_at(wd, av & 3u))) - xa * r.invT;
+                    if (sc < INFINITY) {
+                        atomicMin(&sm.best_key, ordered_key(sc));
+                        push_candidate(sm, a, (int)av, (int)slot, sc, xa);
                     }
                 }
             }
+        } else if (LAYOUT == 0 && e < nA) {
+            // level-4 node i4 of slot j: root and node draws issued together
+            const int it = e - seed_lanes, j = it / n4;
+            const uint32_t i4 = (uint32_t)(it % n4);
+            const uint32_t slot = (uint32_t)(r.slot0 + j);
+            const Words wr = philox(0u, slot, 5u, kDomainTree, k0, k1);
+            const Words w4 = philox(i4, slot, 4u, kDomainTree, k0, k1);
+            const float rm = exp1_f32(wr.w0) / (float)V;
+            const uint32_t rp = uniform_position(wr.w1, wr.w2, V);
+            const uint32_t cs = i4 << kShift4, n = node_end(kShift4, i4, V) - cs;
+            const bool hold = rp >= cs && rp < cs + n;
+            sm.l4[it] = Node{(slot << 20) | i4, hold ? rm : rm + exp1_f32(w4.w0) / (float)n,
+                             hold ? rp : cs + uniform_position(w4.w1, w4.w2, n)};
+        }
+    }
+    __syncthreads();
+
+    if constexpr (LAYOUT == 0) {
+        // Pass B: level-3 children of the level-4 nodes that can still win.
+        const int nB = ns * n4 * 16;
+        const int n3 = (ng + 15) / 16;
+        for (int base = 0;; base += kBlock) {
+            const bool done = base >= nB;  // one call site of flush_l3 (see flush_l3)
+            const bool flush = done || sm.n_l3 > kL3Cap - kBlock;
+            __syncthreads();
+            if (flush) flush_l3<BF16, VEC>(a, r, sm, gm, k0, k1);
+            if (done) break;
+            const int e = base + tid;
+            if (e < nB) {
+                const Node pa = sm.l4[e >> 4];
+                const uint32_t i4 = pa.id & 0xFFFFFu;
+                const uint32_t i3 = i4 * 16u + (uint32_t)(e & 15);
+                const float thr = current_threshold(sm);
+                const float lnp = ln_f32(pa.m);
+                if ((int)i3 < n3 && lnp - sm.m4[i4] * r.invT <= thr && lnp - sm.m3[i3] * r.invT <= thr) {
+                    const uint32_t slot = pa.id >> 20;
+                    float m;
+                    uint32_t p;
+                    child_min_f32(pa.m, pa.p, 3, i3, i3 << kShift3, node_end(kShift3, i3, V), slot, k0, k1, m, p);
+                    if (ln_f32(m) - sm.m3[i3] * r.invT <= thr) push_node(sm.l3, &sm.n_l3, kL3Cap, (slot << 20) | i3, m, p);
+                }
+            }
             __syncthreads();
         }
-        flush_l3<BF16, VEC>(a, r, sm, gm, k0, k1);
     } else {
         // flat clocks: every (group, slot) whose floor bound can win.
         const int tot = ng * ns;
-        for (int base = 0; base < tot; base += kBlock) {
-            const bool flush = sm.n_l2 > kL2Cap - kBlock;
+        for (int base = 0;; base += kBlock) {
+            const bool done = base >= tot;  // one call site of flush_groups
+            const bool flush = done || sm.n_l2 > kL2Cap - kBlock;
             __syncthreads();
             if (flush) flush_groups<BF16, VEC, 1>(a, r, sm, gm, k0, k1);
+            if (done) break;
             const int e = base + tid;
             if (e < tot) {
                 const int g = e / ns;
@@ -714,7 +699,6 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
             }
             __syncthreads();
         }
-        flush_groups<BF16, VEC, 1>(a, r, sm, gm, k0, k1);
     }
 
     // decide: float64 scores of the candidates within the margin of the best; for
@@ -1063,6 +1047,10 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         float mx = -INFINITY;
         for (int t = 0; t < n3; ++t) mx = fmaxf(mx, sm.m3[t]);
         sm.rowmax = mx;
+        sm.n_l4 = sm.n_l3 = sm.n_l2 = sm.n_cand = 0;
+        sm.best_key = ordered_key(INFINITY);
+        sm.key_min = 0x7FFFFFFF;
+        sm.key_max = -1;
         if (prod >= 0) {
             const uint64_t* ks = (const uint64_t*)(a.ws + a.L.keys) + 2 * (size_t)prod;
             uint64_t w0 = ld_dev(ks), w1 = ld_dev(ks + 1);
@@ -1102,7 +1090,7 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         }
     }
     // The last row of a sequence in the work order walks its block.
-    if (r.kind == 1 && r.s == a.gamma && (a.target_rows == 1 || r.k == a.K - 1)) walk(a, sm, r.b, ep);
+    if (r.kind == a.walk_kind && r.s == a.walk_s && r.k == a.walk_k) walk(a, sm, r.b, ep);
     __builtin_amdgcn_s_setprio(0);
 }
 
@@ -1128,13 +1116,14 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
     for (int parity = 0;; parity ^= 1) {
         const int item = sm.tick[parity];
         if (item >= a.n_items) break;
-        int d = 0;
-        while (d + 1 < a.n_depth && item >= a.depth_first[d + 1]) ++d;
-        const int local = item - a.depth_first[d];
+        int ph = 0;
+        while (ph + 1 < a.n_phase && item >= a.phase_first[ph + 1]) ++ph;
+        const int local = item - a.phase_first[ph];
         const int rl = local / a.L.nseg, seg = local % a.L.nseg;
+        const int d = a.phase_depth[ph];
         Row r;
         r.s = d;
-        if (rl < a.depth_nd[d]) {
+        if (rl < a.phase_nd[ph]) {
             r.kind = 0;
             r.b = rl / a.K;
             r.k = rl % a.K;
@@ -1146,7 +1135,7 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
             r.invT = a.inv_T_draft;
             r.T = a.T_draft;
         } else {
-            const int rt = rl - a.depth_nd[d];
+            const int rt = rl - a.phase_nd[ph];
             r.kind = 1;
             size_t off;
             if (a.target_rows == 1) {
