@@ -51,6 +51,7 @@ constexpr int kL3Cap = 512;
 constexpr int kL2Cap = 512;
 constexpr int kRowEntries = 1;
 constexpr int kCandCap = 256;
+constexpr int kWorkCap = 1024;             // (level-3 node, group) items per prefilter round
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
 constexpr uint32_t kSpinLimit = 1u << 22;  // bounded waits for other workgroups' slots
 constexpr uint32_t kErrSpin = 1u, kErrCand = 2u;
@@ -65,7 +66,8 @@ struct Shared {
     float m3[256];
     float m4[16];
     int init_v[kInit];     // seed tokens of the race (-1: none)
-    int stop[64];          // top token of every segment (-1: none)
+    int stop[64];          // top group of every segment (-1: none)
+    float part[64];        // LSE partial sum of every segment
     Node l4[kL4Cap];
     Node l3[kL3Cap];
     Node l2[kL2Cap];
@@ -90,6 +92,8 @@ struct Shared {
     uint32_t next0, next1;  // partial context key of the path's next depth
     int win[32];            // context tokens (own window, next depth's window)
     int key_min, key_max;   // (token, slot) range of the candidates near the best
+    int work[kWorkCap];     // compacted work items
+    int n_work;
 };
 
 struct Row {
@@ -510,23 +514,39 @@ __device__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const 
     __syncthreads();
 }
 
-// Expand listed level-3 nodes into groups (tree clocks), evaluating the groups as the list fills.
+// Expand listed level-3 nodes into groups (tree clocks), evaluating the groups as
+// the list fills.  A draw-free prefilter (group maximum against the node's
+// minimum) first compacts the (node, group) items that can still win into a work
+// list, so that the draws run on full wavefronts.
 template <bool BF16, bool VEC>
 __device__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
     const int tid = threadIdx.x;
     const int n = min(sm.n_l3, kL3Cap) * 16;
     const uint32_t V = (uint32_t)a.V;
     const int ng = a.L.ng;
-    for (int base = 0; base < n; base += kBlock) {
-        // The count is read by every thread before any thread of this pass pushes.
-        const bool flush = sm.n_l2 > kL2Cap - kBlock;
+    for (int base = 0; base < n; base += kWorkCap) {
+        if (tid == 0) sm.n_work = 0;
         __syncthreads();
-        if (flush) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
-        const int e = base + tid;
-        if (e < n) {
-            const Node pa = sm.l3[e >> 4];
-            const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
-            if ((int)g < ng) {
+        {
+            const float thr = current_threshold(sm);
+            for (int e = base + tid; e < min(n, base + kWorkCap); e += kBlock) {
+                const Node pa = sm.l3[e >> 4];
+                const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
+                if ((int)g < ng && ln_f32(pa.m) - gm[g] * r.invT <= thr) sm.work[atomicAdd(&sm.n_work, 1)] = e;
+            }
+        }
+        __syncthreads();
+        const int nw = sm.n_work;
+        for (int wb = 0; wb < nw; wb += kBlock) {
+            // The count is read by every thread before any thread of this pass pushes.
+            const bool flush = sm.n_l2 > kL2Cap - kBlock;
+            __syncthreads();
+            if (flush) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
+            const int i = wb + tid;
+            if (i < nw) {
+                const int e = sm.work[i];
+                const Node pa = sm.l3[e >> 4];
+                const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
                 const float thr = current_threshold(sm);
                 if (ln_f32(pa.m) - gm[g] * r.invT <= thr) {
                     const uint32_t slot = pa.id >> 20;
@@ -536,8 +556,8 @@ __device__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const floa
                     if (ln_f32(m) - gm[g] * r.invT <= thr) push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | g, m, p);
                 }
             }
+            __syncthreads();
         }
-        __syncthreads();
     }
     if (sm.n_l2 > 0) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
     __syncthreads();
@@ -897,14 +917,18 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         const uint64_t* gslot = (const uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * ng;
         const uint64_t* m3slot = (const uint64_t*)(a.ws + a.L.m3) + (size_t)r.row_id * n3;
         const uint64_t* stop = (const uint64_t*)(a.ws + a.L.stop) + (size_t)r.row_id * a.L.nseg;
-        const int ne = ng + n3 + a.L.nseg;
+        const uint64_t* pslot = (const uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
+        const int ne = ng + n3 + 2 * a.L.nseg;
         for (int e0 = 0; e0 < ne; e0 += 4 * kBlock) {
             const uint64_t* src[4];
             uint64_t v[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int e = e0 + i * kBlock + tid;
-                src[i] = e < ng ? gslot + e : e < ng + n3 ? m3slot + (e - ng) : stop + min(e - ng - n3, a.L.nseg - 1);
+                src[i] = e < ng                     ? gslot + e
+                         : e < ng + n3                ? m3slot + (e - ng)
+                         : e < ng + n3 + a.L.nseg     ? stop + (e - ng - n3)
+                                                      : pslot + min(e - ng - n3 - a.L.nseg, a.L.nseg - 1);
                 v[i] = e < ne ? ld_dev(src[i]) : 0;
             }
 #pragma unroll
@@ -917,8 +941,10 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
                         gm[e] = __uint_as_float(w);
                     else if (e < ng + n3)
                         sm.m3[e - ng] = __uint_as_float(w);
-                    else
+                    else if (e < ng + n3 + a.L.nseg)
                         sm.stop[e - ng - n3] = (int)w;
+                    else
+                        sm.part[e - ng - n3 - a.L.nseg] = __uint_as_float(w);
                 }
             }
         }
@@ -986,11 +1012,10 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         constexpr int per = (BF16 ? kSegTokensBf16 : kSegTokensF32) / 2048;  // level-3 blocks per segment
         float mi = -INFINITY, si = 0.f;
         if (lane < a.L.nseg) {
-            const uint64_t v = wait_slot(a, (const uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg + lane, ep);
             float gmx = -INFINITY;
             for (int t = lane * per; t < min(n3, lane * per + per); ++t) gmx = fmaxf(gmx, sm.m3[t]);
             mi = gmx * c2;
-            si = __uint_as_float((uint32_t)v);
+            si = sm.part[lane];
         }
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
