@@ -47,7 +47,7 @@ psd_status check_params(const psd_params* p) {
 
 psd_status check_block(const psd_params* p, const psd_block* b) {
     if (!b) return fail(PSD_E_ARG, "block is NULL");
-    if (b->batch < 1) return fail(PSD_E_ARG, "batch %d < 1", b->batch);
+    if (b->batch < 1 || b->batch > PSD_MAX_BATCH) return fail(PSD_E_ARG, "batch %d outside [1, %d]", b->batch, PSD_MAX_BATCH);
     if (b->gamma < 1 || b->gamma > PSD_MAX_GAMMA) return fail(PSD_E_ARG, "gamma %d outside [1, %d]", b->gamma, PSD_MAX_GAMMA);
     if (!b->start_pos) return fail(PSD_E_ARG, "start_pos is NULL");
     if (p->ctx_window > 0 && !b->prefix_tokens) return fail(PSD_E_ARG, "prefix_tokens is NULL with ctx_window > 0");
@@ -85,9 +85,9 @@ psd::RaceArgs base_args(const psd_params* p, const psd_block* b) {
 
 // Work order.  Every row comes after the rows whose races it waits for.  With a
 // shared target chain and drafts in the same call, the two chains are
-// independent: the target rows (depth by depth) go first, so the longer chain
-// starts early, then the drafts depth by depth, and each sequence's last draft
-// row walks its block.  Otherwise rows go depth by depth, drafts before targets.
+// independent: the target chain, one depth longer, is queued one depth ahead of
+// the drafts, so its waits overlap draft streaming, and each sequence's last
+// draft row walks its block.  Otherwise rows go depth by depth, drafts before targets.
 void build_depths(psd::RaceArgs& a, int n_depth) {
     int first = 0, n = 0;
     auto add = [&](int d, int nd, int nt) {
@@ -101,8 +101,13 @@ void build_depths(psd::RaceArgs& a, int n_depth) {
     };
     const bool targets_first = a.target_rows == 1 && a.s_count > 0;
     if (targets_first) {
-        for (int d = 0; d <= a.gamma; ++d) add(d, 0, a.B);
-        for (int d = a.s_begin; d < a.s_begin + a.s_count; ++d) add(d, a.B * a.K, 0);
+        // the target chain runs one depth ahead: t0 t1 d0 t2 d1 ... t_gamma d_(gamma-1)
+        int dt = 0;
+        for (int d = a.s_begin; d < a.s_begin + a.s_count; ++d) {
+            while (dt <= a.gamma && dt <= d + 1) add(dt++, 0, a.B);
+            add(d, a.B * a.K, 0);
+        }
+        while (dt <= a.gamma) add(dt++, 0, a.B);
         a.walk_kind = 0;
         a.walk_s = a.s_begin + a.s_count - 1;
         a.walk_k = a.K - 1;
