@@ -60,7 +60,8 @@ def write_traffic(fetch_csv: str, write_csv: str, out: str = TRAFFIC_FILE) -> di
         rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
         race = [r for r in rows if "race_kernel<" in r["Kernel_Name"]]
         last = int(race[-1]["Dispatch_Id"])
-        copy = [r for r in rows if int(r["Dispatch_Id"]) > last and int(r["Grid_Size"]) >= 65536]
+        copy = [r for r in rows if int(r["Dispatch_Id"]) > last and "copyBuffer" in r["Kernel_Name"]
+                and int(r["Grid_Size"]) >= 65536]
         if not race or not copy:
             raise SystemExit(f"{path}: no race_kernel or calibration copy dispatches")
         kib = sum(float(r["Counter_Value"]) for r in race) / len(race)

@@ -49,7 +49,7 @@ constexpr int kInit = 8;                   // seed tokens of a race (segment top
 constexpr int kL4Cap = 512;                // <= 32 slots x 16 level-4 nodes
 constexpr int kL3Cap = 512;
 constexpr int kL2Cap = 512;
-constexpr int kRowEntries = 1;
+constexpr int kRowEntries = 2;             // group entries per 16-lane row and evaluation pass
 constexpr int kCandCap = 256;
 constexpr int kWorkCap = 1024;             // (level-3 node, group) items per prefilter round
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
@@ -1121,8 +1121,10 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
 
 // ---------------------------------------------------------------- kernel
 
+// Three workgroups per CU: 168 VGPRs, enough for the race without spills (four
+// workgroups cap registers at 128 and spill; the streaming rate is the same).
 template <bool BF16, bool VEC, int LAYOUT>
-__global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
+__global__ __launch_bounds__(kBlock, 3) void race_kernel(RaceArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Shared& sm = *reinterpret_cast<Shared*>(smem_raw);
     float* gm = reinterpret_cast<float*>(smem_raw + ((sizeof(Shared) + 15) & ~(size_t)15));
