@@ -910,6 +910,24 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
     const uint32_t ep = sm.epoch;
     const float c2 = r.invT * 1.4426950408889634f;
 
+    // Context-key inputs known before the call (prompt tokens, position) are loaded
+    // first, so their latency overlaps the gather.  Wave 3 lanes [0, m) take this
+    // row's own window (when no race of this call publishes its key), lanes
+    // [m, 2m - 1) the next depth's window without its newest token (when this race
+    // publishes the next key); positions index prefix (m tokens) || path.
+    const int prod = key_producer(a, r);
+    const bool cons = key_consumer(a, r);
+    int widx = -1, wtok = 0;
+    int64_t wpos = 0;
+    if (wave == 3) {
+        if (lane < a.m && prod < 0)
+            widx = r.s + lane;
+        else if (lane >= a.m && lane < 2 * a.m - 1 && cons)
+            widx = r.s + 1 + (lane - a.m);
+        if (widx >= 0 && widx < a.m) wtok = a.prefix[(size_t)r.b * a.m + widx];
+        wpos = a.start_pos[r.b];
+    }
+
     // ---- gather the row's slots (group maxima, block maxima, segment top tokens):
     // a batch of loads in flight per thread, then a wait only for slots not yet
     // published.
@@ -1034,24 +1052,14 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
             }
         }
     }
-    // ---- context keys.  Wave 3 fetches window tokens in parallel -- lanes [0, m)
-    // this row's own window (when no race of this call publishes its key), lanes
-    // [m, 2m - 1) the next depth's window without its newest token (when this race
-    // publishes the next key); positions index prefix (m tokens) || path -- and
-    // folds both chains at once: lane 0 this row's key, lane 1 the next depth's key
-    // up to its newest token (the winner of this race).  Meanwhile thread 0 waits
-    // for the key published by the race one depth up this path, if any.
-    const int prod = key_producer(a, r);
-    const bool cons = key_consumer(a, r);
+    // ---- context keys.  Wave 3 reads the window's path tokens (published by earlier
+    // races of this call, or inputs) and folds both chains at once: lane 0 this
+    // row's key, lane 1 the next depth's key up to its newest token (the winner of
+    // this race).  Meanwhile thread 0 waits for the key published by the race one
+    // depth up this path, if any.
     if (wave == 3) {
-        int idx = -1;
-        if (lane < a.m && prod < 0)
-            idx = r.s + lane;
-        else if (lane >= a.m && lane < 2 * a.m - 1 && cons)
-            idx = r.s + 1 + (lane - a.m);
-        int tk = 0;
-        if (idx >= 0) tk = idx < a.m ? a.prefix[(size_t)r.b * a.m + idx] : path_token(a, r, idx - a.m, ep);
-        const uint64_t t = (uint64_t)(a.start_pos[r.b] + r.s) + (uint64_t)(lane == 1);
+        const int tk = widx >= a.m ? path_token(a, r, widx - a.m, ep) : wtok;
+        const uint64_t t = (uint64_t)(wpos + r.s) + (uint64_t)(lane == 1);
         uint32_t c0 = (uint32_t)a.key, c1 = (uint32_t)(a.key >> 32);
         const bool chain = (lane == 0 && prod < 0) || (lane == 1 && cons);
         if (chain) fold(c0, c1, (uint32_t)t, (uint32_t)(t >> 32), 0u);
