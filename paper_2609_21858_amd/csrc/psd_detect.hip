@@ -6,8 +6,12 @@
 // E_j[w_t] exactly (float64), and adds A_t = -ln(1 - r_t) with
 // r_t = exp(-K min_j E_j[w_t]) -- the target's clock of w_t in the augmented
 // race is min_j E_j[w_t] ~ Exp(K), so r_t is uniform when the text does not
-// carry the key.  One workgroup per sequence; the per-sequence sum runs in
-// float64 in a fixed order (deterministic).
+// carry the key.  One workgroup of 1024 threads per sequence, two lanes per
+// token (each rebuilds the token's context key and half of its K clocks).  The
+// clocks are first computed in float to find the smallest; only slots whose float
+// clock lies within a bound of float error of that minimum are rebuilt exactly in
+// float64, so min_j E_j[w_t] is exact.  The per-sequence sum runs in float64 in a
+// fixed order (deterministic).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -19,52 +23,98 @@ namespace psd {
 
 namespace {
 
+constexpr int kDetBlock = 1024;  // threads per detection workgroup
+constexpr int kDetParts = 2;     // lanes per scored token (adjacent), each taking every other slot
+
 template <int LAYOUT>
-__global__ __launch_bounds__(kBlock) void detect_kernel(DetectArgs a) {
-    __shared__ double part[kBlock];
-    __shared__ int cnt[kBlock];
-    const int i = blockIdx.x, tid = threadIdx.x;
+__global__ __launch_bounds__(kDetBlock) void detect_kernel(DetectArgs a) {
+    __shared__ double part[kDetBlock / 64];
+    __shared__ int cnt[kDetBlock / 64];
+    const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+    const int sub = tid % kDetParts;
     const int32_t* toks = a.tokens + (size_t)i * a.seq_len;
     const int n0 = max(0, a.n0[i]);
     double acc = 0.0;
     int c = 0;
-    for (int t = tid; t < a.seq_len; t += kBlock) {
-        const int w = toks[t];
-        if (t < n0 || w < 0 || w >= a.V) {
-            if (a.out_per_token) a.out_per_token[(size_t)i * a.seq_len + t] = NAN;
-            continue;
+    for (int t0 = 0; t0 < a.seq_len; t0 += kDetBlock / kDetParts) {
+        // uniform trip count: both lanes of a token reach the shuffle
+        const int t = t0 + tid / kDetParts;
+        const int w = t < a.seq_len ? toks[t] : -1;
+        const bool scored = t < a.seq_len && t >= n0 && w >= 0 && w < a.V;
+        uint32_t k0 = 0u, k1 = 0u;
+        float emin = INFINITY, e2 = INFINITY;  // this lane's smallest and second-smallest float clocks
+        int jmin = -1;
+        if (scored) {
+            // context key: fold(key, t), then the m previous tokens oldest first (-1
+            // before the text)
+            k0 = (uint32_t)a.key;
+            k1 = (uint32_t)(a.key >> 32);
+            fold(k0, k1, (uint32_t)t, 0u, 0u);
+            for (int j = 0; j < a.m; ++j) {
+                const int idx = t - a.m + j;
+                fold(k0, k1, (uint32_t)(idx >= 0 ? toks[idx] : -1), (uint32_t)j, 1u);
+            }
+            for (int j = sub; j < a.K; j += kDetParts) {
+                const float e = LAYOUT == 0 ? tree_clock_f32((uint32_t)a.V, (uint32_t)j, (uint32_t)w, k0, k1)
+                                            : flat_clock_f32((uint32_t)j, (uint32_t)w, k0, k1);
+                if (e < emin) {
+                    e2 = emin;
+                    emin = e;
+                    jmin = j;
+                } else {
+                    e2 = fminf(e2, e);
+                }
+            }
         }
-        int32_t win[16];
-        for (int j = 0; j < a.m; ++j) {
-            const int idx = t - a.m + j;
-            win[j] = idx >= 0 ? toks[idx] : -1;
-        }
-        uint32_t k0, k1;
-        context_key(a.key, t, win, a.m, k0, k1);
+        // Float clocks err by less than 1e-6 relative plus 1e-6 absolute (a few
+        // roundings of positive terms, hardware log2); every slot within twice that
+        // of the token's float minimum is rebuilt exactly.
+        const float tmin = fminf(emin, __shfl_xor(emin, 1));
+        const float lim = tmin + (tmin * 2e-6f + 2e-6f);
         double cmin = INFINITY;
-        for (int j = 0; j < a.K; ++j) {
-            const double e = LAYOUT == 0 ? tree_clock_f64((uint32_t)a.V, (uint32_t)j, (uint32_t)w, k0, k1)
-                                         : flat_clock_f64((uint32_t)j, (uint32_t)w, k0, k1);
-            cmin = fmin(cmin, e);
+        if (scored && emin <= lim) {
+            if (e2 <= lim) {
+                // another slot of this lane is close: rebuild all of them (rare)
+                for (int j = sub; j < a.K; j += kDetParts)
+                    cmin = fmin(cmin, LAYOUT == 0 ? tree_clock_f64((uint32_t)a.V, (uint32_t)j, (uint32_t)w, k0, k1)
+                                                  : flat_clock_f64((uint32_t)j, (uint32_t)w, k0, k1));
+            } else {
+                cmin = LAYOUT == 0 ? tree_clock_f64((uint32_t)a.V, (uint32_t)jmin, (uint32_t)w, k0, k1)
+                                   : flat_clock_f64((uint32_t)jmin, (uint32_t)w, k0, k1);
+            }
         }
-        const double A = -log(-expm1(-(double)a.K * cmin));
-        acc += A;
-        ++c;
-        if (a.out_per_token) a.out_per_token[(size_t)i * a.seq_len + t] = (float)A;
+        cmin = fmin(cmin, __shfl_xor(cmin, 1));
+        if (sub == 0 && t < a.seq_len) {
+            if (scored) {
+                const double A = -log(-expm1(-(double)a.K * cmin));
+                acc += A;
+                ++c;
+                if (a.out_per_token) a.out_per_token[(size_t)i * a.seq_len + t] = (float)A;
+            } else if (a.out_per_token) {
+                a.out_per_token[(size_t)i * a.seq_len + t] = NAN;
+            }
+        }
     }
-    part[tid] = acc;
-    cnt[tid] = c;
+    // fixed-order reduction: within each wave, then over the waves
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        acc += __shfl_xor(acc, off);
+        c += __shfl_xor(c, off);
+    }
+    if (lane == 0) {
+        part[tid >> 6] = acc;
+        cnt[tid >> 6] = c;
+    }
     __syncthreads();
-    for (int s = kBlock / 2; s > 0; s >>= 1) {
-        if (tid < s) {
-            part[tid] += part[tid + s];
-            cnt[tid] += cnt[tid + s];
-        }
-        __syncthreads();
-    }
     if (tid == 0) {
-        a.out_score[i] = part[0];
-        a.out_count[i] = cnt[0];
+        double s = 0.0;
+        int n = 0;
+        for (int w = 0; w < kDetBlock / 64; ++w) {
+            s += part[w];
+            n += cnt[w];
+        }
+        a.out_score[i] = s;
+        a.out_count[i] = n;
     }
 }
 
@@ -114,9 +164,9 @@ inline unsigned blocks_for(long n, int per) { return (unsigned)((n + per - 1) / 
 hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream) {
     if (a.n_seq <= 0) return hipSuccess;
     if (layout == 0)
-        hipLaunchKernelGGL(detect_kernel<0>, dim3(a.n_seq), dim3(kBlock), 0, stream, a);
+        hipLaunchKernelGGL(detect_kernel<0>, dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
     else
-        hipLaunchKernelGGL(detect_kernel<1>, dim3(a.n_seq), dim3(kBlock), 0, stream, a);
+        hipLaunchKernelGGL(detect_kernel<1>, dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -156,21 +156,62 @@ __device__ __forceinline__ void root_min_f64(uint32_t V, uint32_t slot, uint32_t
     p = uniform_position(w.w1, w.w2, V);
 }
 
-// Exact clock of one token (tree layout), double: walk root -> token.
+// Exact clock of one token (tree layout), double: walk root -> token.  The six
+// draws of the path (root, levels 4..1, token words) are independent Philox calls,
+// issued together; the walk then uses a node's draw only where the parent's
+// minimum lies outside it.
 __device__ __forceinline__ double tree_clock_f64(uint32_t V, uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
-    double m;
-    uint32_t p;
-    root_min_f64(V, slot, k0, k1, m, p);
     const int shifts[4] = {kShift4, kShift3, kShift2, kShift1};
+    const Words wr = philox(0u, slot, 5u, kDomainTree, k0, k1);
+    Words wn[4];
+#pragma unroll
+    for (int l = 0; l < 4; ++l) wn[l] = philox(v >> shifts[l], slot, (uint32_t)(4 - l), kDomainTree, k0, k1);
+    const Words wt = philox(v >> 3, slot, 8u + ((v >> 2) & 1u), kDomainTree, k0, k1);
+    double m = exp1_f64(wr.w0) / (double)V;
+    uint32_t p = uniform_position(wr.w1, wr.w2, V);
 #pragma unroll
     for (int l = 0; l < 4; ++l) {
         const int sh = shifts[l];
-        const uint32_t i = v >> sh;
-        child_min_f64(m, p, 4 - l, i, node_start(sh, i), node_end(sh, i, V), slot, k0, k1, m, p);
+        const uint32_t i = v >> sh, cs = node_start(sh, i), ce = node_end(sh, i, V);
+        if (!(p >= cs && p < ce)) {
+            const uint32_t n = ce - cs;
+            m = m + exp1_f64(wn[l].w0) / (double)n;
+            p = cs + uniform_position(wn[l].w1, wn[l].w2, n);
+        }
     }
     if (v == p) return m;
-    const Words w = philox(v >> 3, slot, 8u + ((v >> 2) & 1u), kDomainTree, k0, k1);
-    return m + exp1_f64(word_at(w, v & 3u));
+    return m + exp1_f64(word_at(wt, v & 3u));
+}
+
+// The same walk in float (hardware log2): relative error a few ulp plus an absolute
+// error of about 2^-23 from logs of uniforms near 1; used to find the slot whose
+// exact clock is smallest.
+__device__ __forceinline__ float tree_clock_f32(uint32_t V, uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
+    const int shifts[4] = {kShift4, kShift3, kShift2, kShift1};
+    const Words wr = philox(0u, slot, 5u, kDomainTree, k0, k1);
+    Words wn[4];
+#pragma unroll
+    for (int l = 0; l < 4; ++l) wn[l] = philox(v >> shifts[l], slot, (uint32_t)(4 - l), kDomainTree, k0, k1);
+    const Words wt = philox(v >> 3, slot, 8u + ((v >> 2) & 1u), kDomainTree, k0, k1);
+    float m = exp1_f32(wr.w0) / (float)V;
+    uint32_t p = uniform_position(wr.w1, wr.w2, V);
+#pragma unroll
+    for (int l = 0; l < 4; ++l) {
+        const int sh = shifts[l];
+        const uint32_t i = v >> sh, cs = node_start(sh, i), ce = node_end(sh, i, V);
+        if (!(p >= cs && p < ce)) {
+            const uint32_t n = ce - cs;
+            m = m + exp1_f32(wn[l].w0) / (float)n;
+            p = cs + uniform_position(wn[l].w1, wn[l].w2, n);
+        }
+    }
+    if (v == p) return m;
+    return m + exp1_f32(word_at(wt, v & 3u));
+}
+
+__device__ __forceinline__ float flat_clock_f32(uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
+    const Words w = philox(v >> 2, slot, 0u, kDomainFlat, k0, k1);
+    return exp1_f32(word_at(w, v & 3u));
 }
 
 __device__ __forceinline__ double flat_clock_f64(uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
