@@ -345,3 +345,27 @@ def test_detect_parity_cpu_text(psd, layout):
     z = (score - count) / np.sqrt(np.maximum(count, 1))
     assert np.all(z[[0, 2, 3]] > 3.0), z
     assert np.all(np.abs(z[4:]) < 4.5), z
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_detect_exact_minimum_many_tokens(psd, layout):
+    """The detector finds each token's smallest clock over K = 16 slots from float
+    clocks and rebuilds only the near-minimum slots exactly: over 64 x 512 scored
+    tokens (a few dozen near-ties expected) every per-token A_t must equal the
+    oracle's, rounded to float32, within 2 ulp -- far tighter than the error a
+    wrong slot would cause -- and every score within 1e-12 relative."""
+    w5 = workloads.WORKLOADS[5]
+    n_seq, n_pos = 64, 512
+    toks = workloads.uniform_tokens(n_seq, w5.m + n_pos, w5.V, seed=77)
+    n0 = torch.full((n_seq,), w5.m, dtype=torch.int32)
+    p = psd.make_params(w5.key, w5.V, w5.K, w5.m, dtype=w5.torch_dtype, clocks=layout)
+    score, count, per = psd.detect(p, toks.to(DEV), n0.to(DEV), per_token=True)
+    _sync()
+    score, count, per, tk = _np(score), _np(count), _np(per), _np(toks)
+    for i in range(n_seq):
+        S, M, ref_per = oracle.detect_sequence(w5.key, w5.m, w5.K, w5.V, tk[i], w5.m, layout)
+        assert count[i] == M == n_pos
+        assert abs(score[i] - S) <= 1e-12 * abs(S), (i, score[i], S)
+        ref32 = ref_per[w5.m:].astype(np.float32)
+        got = per[i][w5.m:]
+        assert np.all(np.abs(got - ref32) <= 2 * np.spacing(np.abs(ref32))), (i, np.max(np.abs(got - ref32)))
