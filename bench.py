@@ -126,7 +126,8 @@ def detect_leg(psd, torch, clocks_id, dev, launches=20):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / launches
     draws = 6 if clocks_id == psd.PSD_CLOCKS_TREE else 1
-    calls = (w5.m + 1) + w5.K * draws
+    # key folds, the K float clocks, and the exact rebuild of the smallest one
+    calls = (w5.m + 1) + w5.K * draws + draws
     return {"workload": f"detection: {n_seq} sequences x {n_pos} scored tokens, K={w5.K}, V={w5.V}, m={w5.m}",
             "tokens_per_s": n_seq * n_pos / (ms / 1e3), "ms_per_launch": ms, "launches": launches,
             "philox_calls_per_token": calls,
