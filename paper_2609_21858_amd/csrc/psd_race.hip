@@ -52,6 +52,8 @@ constexpr int kL2Cap = 512;
 constexpr int kRowEntries = 2;             // group entries per 16-lane row and evaluation pass
 constexpr int kCandCap = 256;
 constexpr int kWorkCap = 1024;             // (level-3 node, group) items per prefilter round
+constexpr int kChunkJobCap = 256;          // chunk draws listed by one evaluation pass
+constexpr int kHalfCap = 256;              // 4-token halves listed by one evaluation pass
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
 constexpr uint32_t kSpinLimit = 1u << 22;  // bounded waits for other workgroups' slots
 constexpr uint32_t kErrSpin = 1u, kErrCand = 2u;
@@ -60,6 +62,15 @@ struct Node {
     uint32_t id;  // (slot << 20) | node index
     float m;      // float32 minimum clock of the node
     uint32_t p;   // token holding that minimum
+};
+
+// A 4-token half of a chunk that can still win: entry (local index), chunk, half
+// and token mask packed in desc; cref the chunk draw it needs (-1: the chunk holds
+// the group minimum); its logits.
+struct Half {
+    uint32_t desc;  // entry << 9 | chunk << 5 | half << 4 | token mask (4 bits)
+    int cref;
+    float x[4];
 };
 
 struct Shared {
@@ -94,6 +105,11 @@ struct Shared {
     int key_min, key_max;   // (token, slot) range of the candidates near the best
     int work[kWorkCap];     // compacted work items
     int n_work;
+    uint32_t n_ev;                    // listed chunk draws (low 16 bits) and halves (high 16 bits)
+    uint32_t cjob[kChunkJobCap];      // chunk draw: entry << 4 | chunk
+    float cj_m[kChunkJobCap];         // its minimum clock
+    uint32_t cj_p[kChunkJobCap];      // and position
+    Half half[kHalfCap];
 };
 
 struct Row {
@@ -124,7 +140,7 @@ __device__ __forceinline__ T ld_dev(const T* p) {
 
 // Bounded wait for a slot whose tag (high 32 bits) equals the epoch.  On timeout an
 // error bit is recorded and the stale value is returned, so every wave terminates.
-__device__ uint64_t wait_slot(const RaceArgs& a, const uint64_t* p, uint32_t epoch) {
+__device__ __forceinline__ uint64_t wait_slot(const RaceArgs& a, const uint64_t* p, uint32_t epoch) {
     uint64_t v = ld_dev(p);
     for (uint32_t i = 0; (uint32_t)(v >> 32) != epoch; ++i) {
         if (i >= kSpinLimit) {
@@ -277,7 +293,7 @@ __device__ __forceinline__ void lse_merge_finite(float& m, float& s, float om, f
 // workgroups), thread 0 takes its next ticket while the loads are in flight: a
 // ticket held through such a wait would stall the rows that need that segment.
 template <bool BF16, bool VEC>
-__device__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared& sm, int parity, bool prefetch) {
+__device__ __forceinline__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared& sm, int parity, bool prefetch) {
     constexpr int NU = BF16 ? 8 : 4;        // 2048-token units per segment
     constexpr int UT = kBlock * 8;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -404,17 +420,54 @@ __device__ __forceinline__ void compact_candidates(Shared& sm) {
     sm.n_cand = o;
 }
 
+// Score the tokens of mask (bits t = tokens base + 4h + t) of one 4-token half,
+// given the chunk's minimum (mc, pc) and the half's Philox words, and list the
+// scores within the threshold as candidates.
+template <int LAYOUT>
+__device__ __forceinline__ void score_half(const RaceArgs& a, const Row& r, Shared& sm, uint32_t base4, uint32_t mask,
+                                           const float (&x)[4], float mc, uint32_t pc, const Words& w, uint32_t slot) {
+    const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
+    const float thr = current_threshold(sm);
+    const float lnmc = LAYOUT == 0 ? ln_f32(mc) : 0.f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        if (!((mask >> t) & 1u)) continue;
+        const uint32_t v = base4 + (uint32_t)t;
+        float sc;
+        if constexpr (LAYOUT == 0) {
+            if (v == pc)
+                sc = lnmc - x[t] * r.invT;
+            else if (lnmc - x[t] * r.invT <= thr)
+                sc = ln_f32(mc + exp1_f32(ws[t])) - x[t] * r.invT;
+            else
+                sc = INFINITY;
+        } else {
+            sc = ln_f32(exp1_f32(ws[t])) - x[t] * r.invT;
+        }
+        if (sc <= thr) {
+            atomicMin(&sm.best_key, ordered_key(sc));
+            push_candidate(sm, a, (int)v, (int)slot, sc, x[t]);
+        }
+    }
+}
+
 // Evaluate listed group entries [first, first + n): 16 lanes hold the 16 chunks of
-// one entry; each row takes kRowEntries entries, whose loads are issued together.
-// A chunk and its token words are drawn together when any of its tokens can still
-// win against the group minimum (chunk and token minima are never below it).
+// one entry (8 tokens each); each row takes kRowEntries entries, whose loads are
+// issued together.  Only a few chunks of a surviving group hold a token that can
+// still win against the group minimum (chunk and token minima are never below
+// it), so the work is listed rather than done by each chunk's lane (a wave runs
+// every branch any of its lanes takes): the chunk draws and the 4-token halves
+// that need token words go to LDS lists, the chunk draws are made one per thread,
+// then the halves are scored one per thread.  Items beyond the lists' capacity are
+// done by their chunk's lane.
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ void eval_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, int first, int n,
-                            uint32_t k0, uint32_t k1) {
-    const int tid = threadIdx.x;
+__device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, int first,
+                                            int n, uint32_t k0, uint32_t k1) {
+    const int tid = threadIdx.x, lane = tid & 63;
     const int c = tid & 15;
     const int row = tid >> 4;  // 16 rows of 16 lanes
     const uint32_t V = (uint32_t)a.V;
+    constexpr uint32_t kDomain = LAYOUT == 0 ? kDomainTree : kDomainFlat;
     float x[kRowEntries][8];
     Node nd[kRowEntries];
     bool act[kRowEntries];
@@ -426,88 +479,153 @@ __device__ void eval_groups(const RaceArgs& a, const Row& r, Shared& sm, const f
         const uint32_t g = nd[q].id & 0xFFFFFu;
         load8<BF16, VEC>(r.ptr, act[q] ? (int)V : 0, (int)(g * kGroupTokens + (uint32_t)c * 8u), x[q]);
     }
+    // What each chunk needs: its own draw (unless it holds the group minimum) and
+    // the words of each half with a token that can still win.
+    const float thr0 = current_threshold(sm);
+    uint32_t hm[kRowEntries][2];
+    bool cj[kRowEntries];
+    int ncj = 0, nh = 0;
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
-        if (!act[q]) continue;  // uniform over the 16-lane row
-        const uint32_t slot = nd[q].id >> 20;
         const uint32_t g = nd[q].id & 0xFFFFFu;
-        const float thr = current_threshold(sm);
-        const float lnm = LAYOUT == 0 ? ln_f32(nd[q].m) : kLnClockFloor;
-        if (lnm - gm[g] * r.invT > thr) continue;  // uniform over the row
         const uint32_t base = g * kGroupTokens + (uint32_t)c * 8u;
-        float sc[8];
+        const float lnm = LAYOUT == 0 ? ln_f32(nd[q].m) : kLnClockFloor;
+        hm[q][0] = hm[q][1] = 0u;
+        cj[q] = false;
+        if (act[q] && lnm - gm[g] * r.invT <= thr0) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) sc[i] = INFINITY;
-        bool need[2] = {false, false};
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            if (base + (uint32_t)i < V && lnm - x[q][i] * r.invT <= thr) need[i >> 2] = true;
-        if (need[0] || need[1]) {
-            if constexpr (LAYOUT == 0) {
-                const uint32_t chunk = g * 16u + (uint32_t)c;
-                const uint32_t ce = node_end(kShift1, chunk, V);
-                // chunk draw and token words are independent Philox calls: issue together
-                const bool inherit = nd[q].p >= base && nd[q].p < ce;
-                Words wc = Words{0u, 0u, 0u, 0u}, w0 = wc, w1 = wc;
-                if (!inherit) wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
-                if (need[0]) w0 = philox(chunk, slot, 8u, kDomainTree, k0, k1);
-                if (need[1]) w1 = philox(chunk, slot, 9u, kDomainTree, k0, k1);
-                float mc = nd[q].m;
-                uint32_t pc = nd[q].p;
-                if (!inherit) {
-                    mc = nd[q].m + exp1_f32(wc.w0) / (float)(ce - base);
-                    pc = base + uniform_position(wc.w1, wc.w2, ce - base);
-                }
-                const float lnmc = ln_f32(mc);
-                const uint32_t ws[8] = {w0.w0, w0.w1, w0.w2, w0.w3, w1.w0, w1.w1, w1.w2, w1.w3};
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    const uint32_t v = base + (uint32_t)i;
-                    if (v >= V || x[q][i] == -INFINITY || !need[i >> 2]) continue;
-                    if (v == pc)
-                        sc[i] = lnmc - x[q][i] * r.invT;
-                    else if (lnmc - x[q][i] * r.invT <= thr)
-                        sc[i] = ln_f32(mc + exp1_f32(ws[i])) - x[q][i] * r.invT;
-                }
-            } else {
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    if (!need[h]) continue;
-                    const Words w = philox((base >> 2) + (uint32_t)h, slot, 0u, kDomainFlat, k0, k1);
-                    const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int t = 4 * h + i;
-                        if (base + (uint32_t)t < V && x[q][t] != -INFINITY)
-                            sc[t] = ln_f32(exp1_f32(ws[i])) - x[q][t] * r.invT;
-                    }
-                }
+            for (int i = 0; i < 8; ++i)
+                if (base + (uint32_t)i < V && x[q][i] != -INFINITY && lnm - x[q][i] * r.invT <= thr0)
+                    hm[q][i >> 2] |= 1u << (i & 3);
+            if (LAYOUT == 0 && (hm[q][0] | hm[q][1])) {
+                const uint32_t ce = node_end(kShift1, g * 16u + (uint32_t)c, V);
+                cj[q] = !(nd[q].p >= base && nd[q].p < ce);
             }
         }
-        float lm = sc[0];
+        ncj += (int)cj[q];
+        nh += (int)(hm[q][0] != 0u) + (int)(hm[q][1] != 0u);
+    }
+    // list positions: wave prefix sum of (draws | halves << 16), one atomic per wave
+    const uint32_t mine = (uint32_t)ncj | ((uint32_t)nh << 16);
+    uint32_t incl = mine;
 #pragma unroll
-        for (int i = 1; i < 8; ++i) lm = fminf(lm, sc[i]);
-        const float rm = row16_min(lm);  // every lane of the row reaches this point
-        if (!(rm <= thr) || rm == INFINITY) continue;
-        if (lm == rm) atomicMin(&sm.best_key, ordered_key(rm));
-        const float lim = fminf(thr, rm + kMargin);
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = (uint32_t)__shfl_up((int)incl, off);
+        if (lane >= off) incl += o;
+    }
+    const uint32_t wtot = (uint32_t)__shfl((int)incl, 63);
+    uint32_t wbase = 0u;
+    if (lane == 0 && wtot != 0u) wbase = atomicAdd(&sm.n_ev, wtot);
+    const uint32_t mb = (uint32_t)__shfl((int)wbase, 0) + incl - mine;
+    int jc = (int)(mb & 0xFFFFu), jh = (int)(mb >> 16);
+    int cref[kRowEntries];
+    int hidx[kRowEntries][2];
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-            if (sc[i] <= lim && sc[i] < INFINITY)
-                push_candidate(sm, a, (int)(base + (uint32_t)i), (int)slot, sc[i], x[q][i]);
+    for (int q = 0; q < kRowEntries; ++q) {
+        const int le = row * kRowEntries + q;
+        cref[q] = -1;
+        if (cj[q]) {
+            cref[q] = jc;
+            if (jc < kChunkJobCap) sm.cjob[jc] = ((uint32_t)le << 4) | (uint32_t)c;
+            ++jc;
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            hidx[q][h] = -1;
+            if (hm[q][h]) {
+                hidx[q][h] = jh;
+                if (jh < kHalfCap) {
+                    Half& hf = sm.half[jh];
+                    hf.desc = ((uint32_t)le << 9) | ((uint32_t)c << 5) | ((uint32_t)h << 4) | hm[q][h];
+                    hf.cref = cref[q];
+                    hf.x[0] = x[q][4 * h];
+                    hf.x[1] = x[q][4 * h + 1];
+                    hf.x[2] = x[q][4 * h + 2];
+                    hf.x[3] = x[q][4 * h + 3];
+                }
+                ++jh;
+            }
+        }
+    }
+    __syncthreads();
+    // chunk draws, one per thread
+    {
+        const int nj = min((int)(sm.n_ev & 0xFFFFu), kChunkJobCap);
+        for (int j = tid; j < nj; j += kBlock) {
+            const uint32_t d = sm.cjob[j];
+            const Node pn = sm.l2[first + (int)(d >> 4)];
+            const uint32_t g = pn.id & 0xFFFFFu, chunk = g * 16u + (d & 15u);
+            const uint32_t base = chunk * 8u, ce = node_end(kShift1, chunk, V);
+            const Words w = philox(chunk, pn.id >> 20, 1u, kDomainTree, k0, k1);
+            sm.cj_m[j] = pn.m + exp1_f32(w.w0) / (float)(ce - base);
+            sm.cj_p[j] = base + uniform_position(w.w1, w.w2, ce - base);
+        }
+    }
+    __syncthreads();
+    // halves, one per thread
+    {
+        const int nj = min((int)(sm.n_ev >> 16), kHalfCap);
+        for (int j = tid; j < nj; j += kBlock) {
+            const Half hf = sm.half[j];
+            const Node pn = sm.l2[first + (int)(hf.desc >> 9)];
+            const uint32_t slot = pn.id >> 20, g = pn.id & 0xFFFFFu;
+            const uint32_t chunk = g * 16u + ((hf.desc >> 5) & 15u), h = (hf.desc >> 4) & 1u;
+            const uint32_t base4 = chunk * 8u + 4u * h;
+            float mc = pn.m;
+            uint32_t pc = pn.p;
+            if (LAYOUT == 0 && hf.cref >= 0) {
+                if (hf.cref < kChunkJobCap) {
+                    mc = sm.cj_m[hf.cref];
+                    pc = sm.cj_p[hf.cref];
+                } else {
+                    const uint32_t ce = node_end(kShift1, chunk, V);
+                    const Words wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
+                    mc = pn.m + exp1_f32(wc.w0) / (float)(ce - chunk * 8u);
+                    pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
+                }
+            }
+            const Words w = LAYOUT == 0 ? philox(chunk, slot, 8u + h, kDomainTree, k0, k1)
+                                        : philox(base4 >> 2, slot, 0u, kDomainFlat, k0, k1);
+            score_half<LAYOUT>(a, r, sm, base4, hf.desc & 15u, hf.x, mc, pc, w, slot);
+        }
+    }
+    // halves beyond the list's capacity: their chunk's lane
+#pragma unroll
+    for (int q = 0; q < kRowEntries; ++q) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            if (hidx[q][h] < kHalfCap) continue;  // not listed (-1) or listed
+            const uint32_t slot = nd[q].id >> 20, g = nd[q].id & 0xFFFFFu;
+            const uint32_t chunk = g * 16u + (uint32_t)c, base4 = chunk * 8u + 4u * (uint32_t)h;
+            float mc = nd[q].m;
+            uint32_t pc = nd[q].p;
+            if (LAYOUT == 0 && cref[q] >= 0) {
+                const uint32_t ce = node_end(kShift1, chunk, V);
+                const Words wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
+                mc = nd[q].m + exp1_f32(wc.w0) / (float)(ce - chunk * 8u);
+                pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
+            }
+            const Words w = LAYOUT == 0 ? philox(chunk, slot, 8u + (uint32_t)h, kDomainTree, k0, k1)
+                                        : philox(base4 >> 2, slot, 0u, kDomainFlat, k0, k1);
+            const float xs[4] = {x[q][4 * h], x[q][4 * h + 1], x[q][4 * h + 2], x[q][4 * h + 3]};
+            score_half<LAYOUT>(a, r, sm, base4, hm[q][h], xs, mc, pc, w, slot);
+        }
     }
 }
 
 // Evaluate and empty the group list.  Callers read the list count after a barrier
 // and before any push of the current pass.
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0,
+__device__ __forceinline__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0,
                              uint32_t k1) {
     const int n = min(sm.n_l2, kL2Cap);
     for (int first = 0; first < n; first += 16 * kRowEntries) {
         eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, 16 * kRowEntries), k0, k1);
         __syncthreads();
-        if (threadIdx.x == 0) compact_candidates(sm);
+        if (threadIdx.x == 0) {
+            compact_candidates(sm);
+            sm.n_ev = 0;
+        }
         __syncthreads();
     }
     if (threadIdx.x == 0) sm.n_l2 = 0;
@@ -519,7 +637,7 @@ __device__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const 
 // minimum) first compacts the (node, group) items that can still win into a work
 // list, so that the draws run on full wavefronts.
 template <bool BF16, bool VEC>
-__device__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
+__device__ __forceinline__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
     const int tid = threadIdx.x;
     const int n = min(sm.n_l3, kL3Cap) * 16;
     const uint32_t V = (uint32_t)a.V;
@@ -588,7 +706,7 @@ __device__ __forceinline__ uint32_t pick_word(uint32_t a0, uint32_t a1, uint32_t
 }
 
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
+__device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
     // (lists, candidates and the best score were reset by the caller)
     const int tid = threadIdx.x;
     const uint32_t V = (uint32_t)a.V;
@@ -820,7 +938,7 @@ __device__ void race(const RaceArgs& a, const Row& r, Shared& sm, const float* g
 
 // ---------------------------------------------------------------- walk
 
-__device__ int walk_draft(const RaceArgs& a, int b, int k, int s, uint32_t ep) {
+__device__ __forceinline__ int walk_draft(const RaceArgs& a, int b, int k, int s, uint32_t ep) {
     if (a.s_count > 0 && s >= a.s_begin) return wait_token(a, draft_row_id(a, b, k, s), ep);
     return a.draft_tokens[((size_t)b * a.K + k) * a.gamma + s];
 }
@@ -828,7 +946,7 @@ __device__ int walk_draft(const RaceArgs& a, int b, int k, int s, uint32_t ep) {
 // Realised-path walk of sequence b; every token it reads carries this call's epoch.
 // Called by every thread: the tokens the walk may read are fetched in parallel
 // first (into the candidate arrays, free once the race is decided); thread 0 walks.
-__device__ void walk(const RaceArgs& a, Shared& sm, int b, uint32_t ep) {
+__device__ __forceinline__ void walk(const RaceArgs& a, Shared& sm, int b, uint32_t ep) {
     const int K = a.K, G = a.gamma, tid = threadIdx.x;
     const int ntp = a.target_rows == 1 ? 1 : K;
     const int nt = ntp * (G + 1), n = nt + K * G;
@@ -900,7 +1018,7 @@ __device__ __forceinline__ bool key_consumer(const RaceArgs& a, const Row& r) {
 }
 
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* gm) {
+__device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* gm) {
     // The race is a latency chain (the next depth of this path waits for it) while
     // the other waves on the same SIMDs stream: raise this wave's issue priority.
     __builtin_amdgcn_s_setprio(3);
@@ -1081,6 +1199,7 @@ __device__ void finish_row(const RaceArgs& a, const Row& r, Shared& sm, float* g
         for (int t = 0; t < n3; ++t) mx = fmaxf(mx, sm.m3[t]);
         sm.rowmax = mx;
         sm.n_l4 = sm.n_l3 = sm.n_l2 = sm.n_cand = 0;
+        sm.n_ev = 0;
         sm.best_key = ordered_key(INFINITY);
         sm.key_min = 0x7FFFFFFF;
         sm.key_max = -1;
