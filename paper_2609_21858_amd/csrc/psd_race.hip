@@ -105,7 +105,7 @@ struct Shared {
     int key_min, key_max;   // (token, slot) range of the candidates near the best
     int work[kWorkCap];     // compacted work items
     int n_work;
-    uint32_t n_ev;                    // listed chunk draws (low 16 bits) and halves (high 16 bits)
+    uint32_t n_ev[2];                 // listed chunk draws (low 16 bits) and halves (high 16 bits), per pass parity
     uint32_t cjob[kChunkJobCap];      // chunk draw: entry << 4 | chunk
     float cj_m[kChunkJobCap];         // its minimum clock
     uint32_t cj_p[kChunkJobCap];      // and position
@@ -420,35 +420,45 @@ __device__ __forceinline__ void compact_candidates(Shared& sm) {
     sm.n_cand = o;
 }
 
-// Score the tokens of mask (bits t = tokens base + 4h + t) of one 4-token half,
-// given the chunk's minimum (mc, pc) and the half's Philox words, and list the
-// scores within the threshold as candidates.
+// Scores of the tokens of mask (bit t: token base4 + t) of one 4-token half, given
+// the chunk's minimum (mc, pc) and the half's Philox words; INFINITY elsewhere and
+// where the token cannot beat thr.
 template <int LAYOUT>
-__device__ __forceinline__ void score_half(const RaceArgs& a, const Row& r, Shared& sm, uint32_t base4, uint32_t mask,
-                                           const float (&x)[4], float mc, uint32_t pc, const Words& w, uint32_t slot) {
+__device__ __forceinline__ void half_scores(const Row& r, uint32_t base4, uint32_t mask, const float (&x)[4], float mc,
+                                            uint32_t pc, const Words& w, float thr, float (&sc)[4]) {
     const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
-    const float thr = current_threshold(sm);
     const float lnmc = LAYOUT == 0 ? ln_f32(mc) : 0.f;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
+        sc[t] = INFINITY;
         if (!((mask >> t) & 1u)) continue;
         const uint32_t v = base4 + (uint32_t)t;
-        float sc;
         if constexpr (LAYOUT == 0) {
             if (v == pc)
-                sc = lnmc - x[t] * r.invT;
+                sc[t] = lnmc - x[t] * r.invT;
             else if (lnmc - x[t] * r.invT <= thr)
-                sc = ln_f32(mc + exp1_f32(ws[t])) - x[t] * r.invT;
-            else
-                sc = INFINITY;
+                sc[t] = ln_f32(mc + exp1_f32(ws[t])) - x[t] * r.invT;
         } else {
-            sc = ln_f32(exp1_f32(ws[t])) - x[t] * r.invT;
-        }
-        if (sc <= thr) {
-            atomicMin(&sm.best_key, ordered_key(sc));
-            push_candidate(sm, a, (int)v, (int)slot, sc, x[t]);
+            sc[t] = ln_f32(exp1_f32(ws[t])) - x[t] * r.invT;
         }
     }
+}
+
+// Lower the best score to the half's smallest score.
+__device__ __forceinline__ void offer_best(Shared& sm, const float (&sc)[4]) {
+    const float mn = fminf(fminf(sc[0], sc[1]), fminf(sc[2], sc[3]));
+    if (mn < INFINITY) atomicMin(&sm.best_key, ordered_key(mn));
+}
+
+// List the half's scores within the margin of the best as candidates.  Callers
+// offer every half of the round first and separate the two steps by a barrier, so
+// that only near-ties of the best are listed.
+__device__ __forceinline__ void list_near(Shared& sm, const RaceArgs& a, uint32_t base4, uint32_t slot,
+                                          const float (&sc)[4], const float (&x)[4]) {
+    const float thr = current_threshold(sm);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+        if (sc[t] <= thr) push_candidate(sm, a, (int)(base4 + (uint32_t)t), (int)slot, sc[t], x[t]);
 }
 
 // Evaluate listed group entries [first, first + n): 16 lanes hold the 16 chunks of
@@ -460,9 +470,18 @@ __device__ __forceinline__ void score_half(const RaceArgs& a, const Row& r, Shar
 // that need token words go to LDS lists, the chunk draws are made one per thread,
 // then the halves are scored one per thread.  Items beyond the lists' capacity are
 // done by their chunk's lane.
+// The scored half a thread holds at the end of an evaluation pass (its logits stay
+// in the half's list entry).
+struct HalfOut {
+    float sc[4];
+    uint32_t base4, slot;
+    bool valid;
+};
+
 template <bool BF16, bool VEC, int LAYOUT>
 __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, int first,
-                                            int n, uint32_t k0, uint32_t k1) {
+                                            int n, int par, uint32_t k0, uint32_t k1, HalfOut& ho,
+                                            uint32_t& ovf) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int c = tid & 15;
     const int row = tid >> 4;  // 16 rows of 16 lanes
@@ -515,42 +534,43 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
     }
     const uint32_t wtot = (uint32_t)__shfl((int)incl, 63);
     uint32_t wbase = 0u;
-    if (lane == 0 && wtot != 0u) wbase = atomicAdd(&sm.n_ev, wtot);
+    if (lane == 0 && wtot != 0u) wbase = atomicAdd(&sm.n_ev[par], wtot);
     const uint32_t mb = (uint32_t)__shfl((int)wbase, 0) + incl - mine;
     int jc = (int)(mb & 0xFFFFu), jh = (int)(mb >> 16);
-    int cref[kRowEntries];
-    int hidx[kRowEntries][2];
+    ovf = 0u;  // halves beyond the list (bit 8q + 4h + t: token t of half h of entry q)
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
         const int le = row * kRowEntries + q;
-        cref[q] = -1;
+        int cref = -1;
         if (cj[q]) {
-            cref[q] = jc;
+            cref = jc;
             if (jc < kChunkJobCap) sm.cjob[jc] = ((uint32_t)le << 4) | (uint32_t)c;
             ++jc;
         }
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            hidx[q][h] = -1;
             if (hm[q][h]) {
-                hidx[q][h] = jh;
                 if (jh < kHalfCap) {
                     Half& hf = sm.half[jh];
                     hf.desc = ((uint32_t)le << 9) | ((uint32_t)c << 5) | ((uint32_t)h << 4) | hm[q][h];
-                    hf.cref = cref[q];
+                    hf.cref = cref;
                     hf.x[0] = x[q][4 * h];
                     hf.x[1] = x[q][4 * h + 1];
                     hf.x[2] = x[q][4 * h + 2];
                     hf.x[3] = x[q][4 * h + 3];
+                } else {
+                    ovf |= hm[q][h] << (8 * q + 4 * h);
                 }
                 ++jh;
             }
         }
     }
     __syncthreads();
+    // the other parity's counts were read in the previous pass: clear them for the next
+    if (tid == 0) sm.n_ev[par ^ 1] = 0u;
     // chunk draws, one per thread
     {
-        const int nj = min((int)(sm.n_ev & 0xFFFFu), kChunkJobCap);
+        const int nj = min((int)(sm.n_ev[par] & 0xFFFFu), kChunkJobCap);
         for (int j = tid; j < nj; j += kBlock) {
             const uint32_t d = sm.cjob[j];
             const Node pn = sm.l2[first + (int)(d >> 4)];
@@ -562,15 +582,23 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
         }
     }
     __syncthreads();
-    // halves, one per thread
+    // halves, one per thread (at most one: kHalfCap == kBlock): scores, and the best
+    // lowered to each half's smallest; the caller lists near-ties after a barrier
+    static_assert(kHalfCap == kBlock, "one listed half per thread");
     {
-        const int nj = min((int)(sm.n_ev >> 16), kHalfCap);
-        for (int j = tid; j < nj; j += kBlock) {
-            const Half hf = sm.half[j];
+        const int nj = min((int)(sm.n_ev[par] >> 16), kHalfCap);
+        const float thr = current_threshold(sm);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) ho.sc[t] = INFINITY;
+        ho.base4 = ho.slot = 0u;
+        ho.valid = tid < nj;
+        if (ho.valid) {
+            const Half hf = sm.half[tid];
             const Node pn = sm.l2[first + (int)(hf.desc >> 9)];
-            const uint32_t slot = pn.id >> 20, g = pn.id & 0xFFFFFu;
+            ho.slot = pn.id >> 20;
+            const uint32_t g = pn.id & 0xFFFFFu;
             const uint32_t chunk = g * 16u + ((hf.desc >> 5) & 15u), h = (hf.desc >> 4) & 1u;
-            const uint32_t base4 = chunk * 8u + 4u * h;
+            ho.base4 = chunk * 8u + 4u * h;
             float mc = pn.m;
             uint32_t pc = pn.p;
             if (LAYOUT == 0 && hf.cref >= 0) {
@@ -579,36 +607,59 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
                     pc = sm.cj_p[hf.cref];
                 } else {
                     const uint32_t ce = node_end(kShift1, chunk, V);
-                    const Words wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
+                    const Words wc = philox(chunk, ho.slot, 1u, kDomainTree, k0, k1);
                     mc = pn.m + exp1_f32(wc.w0) / (float)(ce - chunk * 8u);
                     pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
                 }
             }
-            const Words w = LAYOUT == 0 ? philox(chunk, slot, 8u + h, kDomainTree, k0, k1)
-                                        : philox(base4 >> 2, slot, 0u, kDomainFlat, k0, k1);
-            score_half<LAYOUT>(a, r, sm, base4, hf.desc & 15u, hf.x, mc, pc, w, slot);
+            const Words w = LAYOUT == 0 ? philox(chunk, ho.slot, 8u + h, kDomainTree, k0, k1)
+                                        : philox(ho.base4 >> 2, ho.slot, 0u, kDomainFlat, k0, k1);
+            half_scores<LAYOUT>(r, ho.base4, hf.desc & 15u, hf.x, mc, pc, w, thr, ho.sc);
+            offer_best(sm, ho.sc);
         }
     }
-    // halves beyond the list's capacity: their chunk's lane
+}
+
+// Halves an evaluation pass could not list (more than kHalfCap): each is scored by
+// its chunk's lane (logits read again), one (entry, half) combination at a time,
+// with the same offer / barrier / list steps.  Called by every thread.
+template <bool BF16, int LAYOUT>
+__device__ __forceinline__ void eval_overflow(const RaceArgs& a, const Row& r, Shared& sm, int first, uint32_t ovf,
+                                              uint32_t k0, uint32_t k1) {
+    const int tid = threadIdx.x, c = tid & 15, row = tid >> 4;
+    const uint32_t V = (uint32_t)a.V;
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            if (hidx[q][h] < kHalfCap) continue;  // not listed (-1) or listed
-            const uint32_t slot = nd[q].id >> 20, g = nd[q].id & 0xFFFFFu;
-            const uint32_t chunk = g * 16u + (uint32_t)c, base4 = chunk * 8u + 4u * (uint32_t)h;
-            float mc = nd[q].m;
-            uint32_t pc = nd[q].p;
-            if (LAYOUT == 0 && cref[q] >= 0) {
+            const uint32_t mask = (ovf >> (8 * q + 4 * h)) & 15u;
+            float sc[4] = {INFINITY, INFINITY, INFINITY, INFINITY}, xs[4] = {0.f, 0.f, 0.f, 0.f};
+            uint32_t base4 = 0u, slot = 0u;
+            if (mask != 0u) {
+                const Node pn = sm.l2[first + row * kRowEntries + q];
+                slot = pn.id >> 20;
+                const uint32_t g = pn.id & 0xFFFFFu;
+                const uint32_t chunk = g * 16u + (uint32_t)c;
+                base4 = chunk * 8u + 4u * (uint32_t)h;
+                float mc = pn.m;
+                uint32_t pc = pn.p;
                 const uint32_t ce = node_end(kShift1, chunk, V);
-                const Words wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
-                mc = nd[q].m + exp1_f32(wc.w0) / (float)(ce - chunk * 8u);
-                pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
+                if (LAYOUT == 0 && !(pn.p >= chunk * 8u && pn.p < ce)) {
+                    const Words wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
+                    mc = pn.m + exp1_f32(wc.w0) / (float)(ce - chunk * 8u);
+                    pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
+                }
+                const Words w = LAYOUT == 0 ? philox(chunk, slot, 8u + (uint32_t)h, kDomainTree, k0, k1)
+                                            : philox(base4 >> 2, slot, 0u, kDomainFlat, k0, k1);
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    xs[t] = (mask >> t) & 1u ? load_logit<BF16>(r.ptr, (int)(base4 + (uint32_t)t)) : -INFINITY;
+                half_scores<LAYOUT>(r, base4, mask, xs, mc, pc, w, current_threshold(sm), sc);
+                offer_best(sm, sc);
             }
-            const Words w = LAYOUT == 0 ? philox(chunk, slot, 8u + (uint32_t)h, kDomainTree, k0, k1)
-                                        : philox(base4 >> 2, slot, 0u, kDomainFlat, k0, k1);
-            const float xs[4] = {x[q][4 * h], x[q][4 * h + 1], x[q][4 * h + 2], x[q][4 * h + 3]};
-            score_half<LAYOUT>(a, r, sm, base4, hm[q][h], xs, mc, pc, w, slot);
+            __syncthreads();
+            if (mask != 0u) list_near(sm, a, base4, slot, sc, xs);
+            __syncthreads();
         }
     }
 }
@@ -617,18 +668,25 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
 // and before any push of the current pass.
 template <bool BF16, bool VEC, int LAYOUT>
 __device__ __forceinline__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0,
-                             uint32_t k1) {
+                                             uint32_t k1) {
     const int n = min(sm.n_l2, kL2Cap);
-    for (int first = 0; first < n; first += 16 * kRowEntries) {
-        eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, 16 * kRowEntries), k0, k1);
+    int par = 0;
+    for (int first = 0; first < n; first += 16 * kRowEntries, par ^= 1) {
+        HalfOut ho;
+        uint32_t ovf;
+        eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, 16 * kRowEntries), par, k0, k1, ho, ovf);
         __syncthreads();
-        if (threadIdx.x == 0) {
-            compact_candidates(sm);
-            sm.n_ev = 0;
-        }
+        // every half of the pass has lowered the best: list the near-ties
+        if (ho.valid) list_near(sm, a, ho.base4, ho.slot, ho.sc, sm.half[threadIdx.x].x);
+        if ((sm.n_ev[par] >> 16) > (uint32_t)kHalfCap) eval_overflow<BF16, LAYOUT>(a, r, sm, first, ovf, k0, k1);
         __syncthreads();
+        // (the next pass touches the candidates only after two more barriers)
+        if (threadIdx.x == 0) compact_candidates(sm);
     }
-    if (threadIdx.x == 0) sm.n_l2 = 0;
+    if (threadIdx.x == 0) {
+        sm.n_l2 = 0;
+        sm.n_ev[0] = sm.n_ev[1] = 0u;
+    }
     __syncthreads();
 }
 
@@ -1199,7 +1257,7 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
         for (int t = 0; t < n3; ++t) mx = fmaxf(mx, sm.m3[t]);
         sm.rowmax = mx;
         sm.n_l4 = sm.n_l3 = sm.n_l2 = sm.n_cand = 0;
-        sm.n_ev = 0;
+        sm.n_ev[0] = sm.n_ev[1] = 0;
         sm.best_key = ordered_key(INFINITY);
         sm.key_min = 0x7FFFFFFF;
         sm.key_max = -1;

@@ -205,6 +205,23 @@ def test_temperatures_and_neg_inf(psd):
         assert math.isinf(float(out["target_lse"][1, 2]))
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_flat_and_two_level_rows(psd, layout, dtype):
+    """Rows whose logits are all equal, or take two values, leave almost every group
+    and chunk able to win: the evaluation lists overflow their LDS capacity and the
+    overflow is scored by each chunk's own lane."""
+    w = workloads.custom(20000, 4, 2, 2, dtype=dtype, m=3)
+    blk = workloads.make_block(w, 31)
+    tl, dl = blk["target_logits"], blk["draft_logits"]
+    tl[0, 0, :] = 0.0
+    tl[0, 1, :] = 0.5
+    tl[1, 0, :] = torch.where(torch.arange(w.V) % 3 == 0, 1.0, 0.0).to(tl.dtype)
+    dl[0, 0, 0, :] = 0.0
+    dl[1, 2, 1, :] = torch.where(torch.arange(w.V) % 5 == 0, 2.0, 1.0).to(dl.dtype)
+    run_block(psd, w, 31, layout, blk=blk)
+
+
 def test_determinism_and_workspace_reuse(psd):
     w = workloads.custom(6000, 3, 3, 4, dtype="bf16", m=4)
     blk = workloads.make_block(w, 8)
