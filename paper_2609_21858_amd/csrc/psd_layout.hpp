@@ -16,11 +16,12 @@ constexpr int kMaxPhases = 2 * kMaxDepth;
 inline int seg_tokens(int dtype_bf16) { return dtype_bf16 ? kSegTokensBf16 : kSegTokensF32; }
 
 // Control words at the start of every workspace (fixed positions for every call shape).
-constexpr int kCtrlWords = 1024;   // 4 KiB
+constexpr int kCtrlWords = 2048;   // 8 KiB
 constexpr int kCtrlExited = 1;     // workgroups that left the kernel
 constexpr int kCtrlErrors = 2;     // sticky error bits
 constexpr int kCtrlEpoch = 5;      // epoch of the last completed call
-constexpr int kMaxQueues = 8;      // work queues (one per XCD), counters 256 B apart
+constexpr int kMaxQueues = 8;      // work queues (one per XCD) of each kind, counters 256 B apart
+// counter of segment queue q (q < kMaxQueues) or of row queue q - kMaxQueues
 inline constexpr int ctrl_queue(int q) { return 64 * (q + 1); }
 
 // Every slot a call publishes is (epoch << 32) | 32-bit payload, with the call's

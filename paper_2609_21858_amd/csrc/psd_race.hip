@@ -89,14 +89,14 @@ struct Shared {
     double red_s[kBlock / 64];
     int red_v[kBlock / 64];
     int red_j[kBlock / 64];
-    float red_a[kBlock / 64];
-    float red_b[kBlock / 64];
+    float red_a[2][kBlock / 64];  // per-wave LSE partials of the streamed segment (by parity)
+    float red_b[2][kBlock / 64];
     int n_l4, n_l3, n_l2, n_cand;
     int best_key;
     int tick[2];
+    int ph_first[kMaxPhases], ph_depth[kMaxPhases], ph_nd[kMaxPhases];  // work-order phases
     uint32_t epoch;
-    int queue, n_queues;
-    float gst[128];   // group maxima of the segment being streamed
+    float gst[2][128];  // group maxima of the streamed segment (by parity)
     int win_token, win_slot;
     float rowmax;
     uint32_t kappa0, kappa1;
@@ -173,6 +173,14 @@ __device__ __forceinline__ int take_item(const RaceArgs& a, int q, int nq) {
     const uint32_t t = atomicAdd(ctrl_of(a) + ctrl_queue(q), 1u);
     const uint32_t R = (uint32_t)q + (uint32_t)nq * (t / (uint32_t)a.L.nseg);
     return R >= (uint32_t)a.n_rows ? a.n_items : (int)(R * (uint32_t)a.L.nseg + t % (uint32_t)a.L.nseg);
+}
+
+// Next row of row queue q (of nq) for a finishing workgroup: rows R = q, q + nq, ...
+// in work order.  Returns n_rows when the queue is exhausted.
+__device__ __forceinline__ int take_row(const RaceArgs& a, int q, int nq) {
+    const uint32_t t = atomicAdd(ctrl_of(a) + ctrl_queue(kMaxQueues + q), 1u);
+    const uint32_t R = (uint32_t)q + (uint32_t)nq * t;
+    return R >= (uint32_t)a.n_rows ? a.n_rows : (int)R;
 }
 
 // ---------------------------------------------------------------- logits access
@@ -292,18 +300,31 @@ __device__ __forceinline__ void lse_merge_finite(float& m, float& s, float om, f
 // maximum).  Unless the workgroup is about to finish a row (which can wait on other
 // workgroups), thread 0 takes its next ticket while the loads are in flight: a
 // ticket held through such a wait would stall the rows that need that segment.
+template <bool BF16>
+constexpr int units_per_segment() {
+    return BF16 ? 8 : 4;  // 2048-token units
+}
+
+// Issue the loads of one segment (one 8-token unit per thread and unit).
 template <bool BF16, bool VEC>
-__device__ __forceinline__ void stream_segment(const RaceArgs& a, const Row& r, int seg, Shared& sm, int parity, bool prefetch) {
-    constexpr int NU = BF16 ? 8 : 4;        // 2048-token units per segment
+__device__ __forceinline__ void issue_segment(const RaceArgs& a, const Row& r, int seg,
+                                              Unit<BF16, VEC> (&u)[units_per_segment<BF16>()]) {
+    constexpr int NU = units_per_segment<BF16>();
+    const int seg0 = seg * (BF16 ? kSegTokensBf16 : kSegTokensF32);
+#pragma unroll
+    for (int q = 0; q < NU; ++q) load_unit<BF16, VEC>(r.ptr, a.V, seg0 + q * kBlock * 8 + 8 * threadIdx.x, u[q]);
+}
+
+// Consume a loaded segment: per-wave LSE partials and the maximum of every
+// 128-token group, staged in LDS (parity p) for publish_segment.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void consume_segment(const RaceArgs& a, const Row& r, int seg, Shared& sm, int p,
+                                                const Unit<BF16, VEC> (&u)[units_per_segment<BF16>()]) {
+    constexpr int NU = units_per_segment<BF16>();
     constexpr int UT = kBlock * 8;
     const int tid = threadIdx.x, lane = tid & 63;
     const int V = a.V;
     const int seg0 = seg * (BF16 ? kSegTokensBf16 : kSegTokensF32);
-    const uint64_t ep = (uint64_t)sm.epoch << 32;
-    Unit<BF16, VEC> u[NU];
-#pragma unroll
-    for (int q = 0; q < NU; ++q) load_unit<BF16, VEC>(r.ptr, V, seg0 + q * UT + 8 * tid, u[q]);
-    if (tid == 0 && prefetch) sm.tick[parity ^ 1] = take_item(a, sm.queue, sm.n_queues);
     const float c2 = r.invT * 1.4426950408889634f;
     float mrun = kNegBig, srun = 0.f;
 #pragma unroll
@@ -319,7 +340,7 @@ __device__ __forceinline__ void stream_segment(const RaceArgs& a, const Row& r, 
         }
         const float um = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
         const float g = row16_max(um);
-        if ((lane & 15) == 0) sm.gst[q * 16 + (tid >> 4)] = g;
+        if ((lane & 15) == 0) sm.gst[p][q * 16 + (tid >> 4)] = g;
         const float mn = fmaxf(mrun, um * c2);
         float acc = srun * __builtin_amdgcn_exp2f(mrun - mn);
 #pragma unroll
@@ -329,32 +350,39 @@ __device__ __forceinline__ void stream_segment(const RaceArgs& a, const Row& r, 
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) lse_merge_finite(mrun, srun, __shfl_xor(mrun, off), __shfl_xor(srun, off));
-    const int wave = tid >> 6;
     if (lane == 0) {
-        sm.red_a[wave] = mrun;
-        sm.red_b[wave] = srun;
+        sm.red_a[p][tid >> 6] = mrun;
+        sm.red_b[p][tid >> 6] = srun;
     }
-    __syncthreads();
-    // publish: one 64-bit slot per group and per 2048-token block (one unit each),
-    // written by consecutive lanes
+}
+
+// Publish a consumed segment (after a barrier): one 64-bit slot per group and per
+// 2048-token block, written by consecutive lanes, the segment's top group and its
+// LSE partial.
+template <bool BF16>
+__device__ __forceinline__ void publish_segment(const RaceArgs& a, int row_id, int seg, Shared& sm, int p) {
+    constexpr int NU = units_per_segment<BF16>();
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int seg0 = seg * (BF16 ? kSegTokensBf16 : kSegTokensF32);
+    const uint64_t ep = (uint64_t)sm.epoch << 32;
     const int g0 = seg0 >> 7;
     if (tid < NU * 16 && g0 + tid < a.L.ng) {
-        uint64_t* gslot = (uint64_t*)(a.ws + a.L.gmax) + (size_t)r.row_id * a.L.ng;
-        st_dev(gslot + g0 + tid, ep | __float_as_uint(sm.gst[tid]));
+        uint64_t* gslot = (uint64_t*)(a.ws + a.L.gmax) + (size_t)row_id * a.L.ng;
+        st_dev(gslot + g0 + tid, ep | __float_as_uint(sm.gst[p][tid]));
     } else if (tid >= 128 && tid < 128 + NU && (seg0 >> 11) + (tid - 128) < a.L.n3) {
         const int q = tid - 128;
-        float mx = sm.gst[16 * q];
+        float mx = sm.gst[p][16 * q];
 #pragma unroll
-        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sm.gst[16 * q + i]);
-        uint64_t* m3slot = (uint64_t*)(a.ws + a.L.m3) + (size_t)r.row_id * a.L.n3;
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sm.gst[p][16 * q + i]);
+        uint64_t* m3slot = (uint64_t*)(a.ws + a.L.m3) + (size_t)row_id * a.L.n3;
         st_dev(m3slot + (seg0 >> 11) + q, ep | __float_as_uint(mx));
     }
     if (tid < 64) {
         // the segment's top group: its largest group, lowest index on ties
-        float bv = lane < NU * 16 ? sm.gst[lane] : -INFINITY;
+        float bv = lane < NU * 16 ? sm.gst[p][lane] : -INFINITY;
         int bi = lane;
-        if (lane + 64 < NU * 16 && sm.gst[lane + 64] > bv) {
-            bv = sm.gst[lane + 64];
+        if (lane + 64 < NU * 16 && sm.gst[p][lane + 64] > bv) {
+            bv = sm.gst[p][lane + 64];
             bi = lane + 64;
         }
 #pragma unroll
@@ -367,14 +395,14 @@ __device__ __forceinline__ void stream_segment(const RaceArgs& a, const Row& r, 
             }
         }
         if (lane == 0) {
-            uint64_t* stop = (uint64_t*)(a.ws + a.L.stop) + (size_t)r.row_id * a.L.nseg;
+            uint64_t* stop = (uint64_t*)(a.ws + a.L.stop) + (size_t)row_id * a.L.nseg;
             st_dev(stop + seg, ep | (uint32_t)(bv == -INFINITY ? -1 : g0 + bi));
         }
     }
     if (tid == 0) {
-        float m = sm.red_a[0], s = sm.red_b[0];
-        for (int w = 1; w < kBlock / 64; ++w) lse_merge_finite(m, s, sm.red_a[w], sm.red_b[w]);
-        uint64_t* part = (uint64_t*)(a.ws + a.L.part) + (size_t)r.row_id * a.L.nseg;
+        float m = sm.red_a[p][0], s = sm.red_b[p][0];
+        for (int w = 1; w < kBlock / 64; ++w) lse_merge_finite(m, s, sm.red_a[p][w], sm.red_b[p][w]);
+        uint64_t* part = (uint64_t*)(a.ws + a.L.part) + (size_t)row_id * a.L.nseg;
         st_dev(part + seg, ep | __float_as_uint(s));
     }
 }
@@ -1306,8 +1334,66 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
 
 // ---------------------------------------------------------------- kernel
 
+// Row and segment of a work item (phases of rows, each at one depth: its draft
+// rows, then its target rows, each row segment by segment).
+template <bool BF16>
+__device__ __forceinline__ void decode_item(const RaceArgs& a, const Shared& sm, int item, Row& r, int& seg) {
+    const size_t esize = BF16 ? 2 : 4;
+    const int D = a.B * a.K * a.gamma;
+    // the phase holding the item: the number of later phase starts at or below it
+    // (phases start in increasing order; phase 0 starts at 0)
+    static_assert(kMaxPhases <= 2 * 64, "phase starts fit two lanes per wave");
+    const int lane = threadIdx.x & 63;
+    const bool s0 = lane + 1 < a.n_phase && sm.ph_first[lane + 1] <= item;
+    const bool s1 = lane + 65 < a.n_phase && sm.ph_first[lane + 65] <= item;
+    const int ph = (int)__builtin_popcountll(__ballot(s0)) + (int)__builtin_popcountll(__ballot(s1));
+    const int local = item - sm.ph_first[ph];
+    const int rl = local / a.L.nseg;
+    seg = local % a.L.nseg;
+    const int d = sm.ph_depth[ph];
+    r.s = d;
+    if (rl < sm.ph_nd[ph]) {
+        r.kind = 0;
+        r.b = rl / a.K;
+        r.k = rl % a.K;
+        r.row_id = (r.b * a.K + r.k) * a.gamma + d;
+        r.ptr = (const unsigned char*)a.draft_logits +
+                (((size_t)r.b * a.K + r.k) * a.s_count + (size_t)(d - a.s_begin)) * (size_t)a.V * esize;
+        r.slot0 = r.k;
+        r.nslots = 1;
+        r.invT = a.inv_T_draft;
+        r.T = a.T_draft;
+    } else {
+        const int rt = rl - sm.ph_nd[ph];
+        r.kind = 1;
+        size_t off;
+        if (a.target_rows == 1) {
+            r.b = rt;
+            r.k = 0;
+            r.row_id = D + r.b * (a.gamma + 1) + d;
+            off = (size_t)r.b * (a.gamma + 1) + d;
+        } else {
+            r.b = rt / a.K;
+            r.k = rt % a.K;
+            r.row_id = D + (r.b * a.K + r.k) * (a.gamma + 1) + d;
+            off = ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + d;
+        }
+        r.ptr = (const unsigned char*)a.target_logits + off * (size_t)a.V * esize;
+        r.slot0 = 0;
+        r.nslots = a.K;
+        r.invT = a.inv_T_target;
+        r.T = a.T_target;
+    }
+}
+
 // Three workgroups per CU: 168 VGPRs, enough for the race without spills (four
-// workgroups cap registers at 128 and spill; the streaming rate is the same).
+// workgroups cap registers at 128 and spill).  Every third workgroup finishes rows;
+// the others only stream segments, so the streaming loop (software-pipelined) and
+// the races neither share a loop nor wait for each other.  Both kinds take work in
+// order from per-XCD queues (row R goes to queue R mod nq for both): streaming
+// never waits, and a finishing workgroup waits only for segments (streamed without
+// waiting) and for races of rows earlier in the order (taken earlier by running
+// finishing workgroups), so every wait ends.
 template <bool BF16, bool VEC, int LAYOUT>
 __global__ __launch_bounds__(kBlock, 3) void race_kernel(RaceArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -1315,72 +1401,60 @@ __global__ __launch_bounds__(kBlock, 3) void race_kernel(RaceArgs a) {
     float* gm = reinterpret_cast<float*>(smem_raw + ((sizeof(Shared) + 15) & ~(size_t)15));
     const int tid = threadIdx.x;
     uint32_t* ctrl = ctrl_of(a);
-    const size_t esize = BF16 ? 2 : 4;
-    const int D = a.B * a.K * a.gamma;
+    // roles: blocks 2, 5, 8, ... finish rows (the launch has at least 3 blocks); with
+    // 24 or more blocks every XCD queue (block mod 8) has both kinds
+    const bool finisher = blockIdx.x % 3u == 2u;
+    const int nq = gridDim.x >= 24u ? kMaxQueues : 1;
+    const int q = (int)(blockIdx.x % (unsigned)nq);
     if (tid == 0) {
         const uint32_t last = ld_dev(ctrl + kCtrlEpoch);
         sm.epoch = last == 0xFFFFFFFFu ? 1u : last + 1u;  // 1 .. 2^32-1
-        sm.n_queues = min((int)gridDim.x, kMaxQueues);
-        sm.queue = (int)(blockIdx.x % (unsigned)sm.n_queues);
-        sm.tick[0] = take_item(a, sm.queue, sm.n_queues);
+        sm.tick[0] = finisher ? take_row(a, q, nq) : take_item(a, q, nq);
+    }
+    for (int i = tid; i < a.n_phase; i += kBlock) {
+        sm.ph_first[i] = a.phase_first[i];
+        sm.ph_depth[i] = a.phase_depth[i];
+        sm.ph_nd[i] = a.phase_nd[i];
     }
     __syncthreads();
-    for (int parity = 0;; parity ^= 1) {
-        const int item = sm.tick[parity];
-        if (item >= a.n_items) break;
-        int ph = 0;
-        while (ph + 1 < a.n_phase && item >= a.phase_first[ph + 1]) ++ph;
-        const int local = item - a.phase_first[ph];
-        const int rl = local / a.L.nseg, seg = local % a.L.nseg;
-        const int d = a.phase_depth[ph];
-        Row r;
-        r.s = d;
-        if (rl < a.phase_nd[ph]) {
-            r.kind = 0;
-            r.b = rl / a.K;
-            r.k = rl % a.K;
-            r.row_id = (r.b * a.K + r.k) * a.gamma + d;
-            r.ptr = (const unsigned char*)a.draft_logits +
-                    (((size_t)r.b * a.K + r.k) * a.s_count + (size_t)(d - a.s_begin)) * (size_t)a.V * esize;
-            r.slot0 = r.k;
-            r.nslots = 1;
-            r.invT = a.inv_T_draft;
-            r.T = a.T_draft;
-        } else {
-            const int rt = rl - a.phase_nd[ph];
-            r.kind = 1;
-            size_t off;
-            if (a.target_rows == 1) {
-                r.b = rt;
-                r.k = 0;
-                r.row_id = D + r.b * (a.gamma + 1) + d;
-                off = (size_t)r.b * (a.gamma + 1) + d;
-            } else {
-                r.b = rt / a.K;
-                r.k = rt % a.K;
-                r.row_id = D + (r.b * a.K + r.k) * (a.gamma + 1) + d;
-                off = ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + d;
-            }
-            r.ptr = (const unsigned char*)a.target_logits + off * (size_t)a.V * esize;
-            r.slot0 = 0;
-            r.nslots = a.K;
-            r.invT = a.inv_T_target;
-            r.T = a.T_target;
-        }
-        const bool last = seg == a.L.nseg - 1;
-        stream_segment<BF16, VEC>(a, r, seg, sm, parity, !last);
-        // the workgroup holding the row's last segment (highest ticket) finishes it
-        if (last) {
+    if (finisher) {
+        for (int R = sm.tick[0]; R < a.n_rows;) {
+            Row r;
+            int seg;
+            decode_item<BF16>(a, sm, R * a.L.nseg + a.L.nseg - 1, r, seg);
             finish_row<BF16, VEC, LAYOUT>(a, r, sm, gm);
-            if (tid == 0) sm.tick[parity ^ 1] = take_item(a, sm.queue, sm.n_queues);
+            if (tid == 0) sm.tick[0] = take_row(a, q, nq);
+            __syncthreads();
+            R = sm.tick[0];
         }
-        __syncthreads();
+    } else {
+        // Software-pipelined: the next segment's loads are issued before the current
+        // one is published.
+        Unit<BF16, VEC> u[units_per_segment<BF16>()];
+        int item = sm.tick[0], seg = 0;
+        Row r;
+        if (item < a.n_items) {
+            decode_item<BF16>(a, sm, item, r, seg);
+            issue_segment<BF16, VEC>(a, r, seg, u);
+        }
+        for (int parity = 0; item < a.n_items; parity ^= 1) {
+            if (tid == 0) sm.tick[parity ^ 1] = take_item(a, q, nq);
+            consume_segment<BF16, VEC>(a, r, seg, sm, parity, u);
+            __syncthreads();
+            const int pub_row = r.row_id, pub_seg = seg;
+            item = sm.tick[parity ^ 1];
+            if (item < a.n_items) {
+                decode_item<BF16>(a, sm, item, r, seg);
+                issue_segment<BF16, VEC>(a, r, seg, u);
+            }
+            publish_segment<BF16>(a, pub_row, pub_seg, sm, parity);
+        }
     }
     // The last workgroup to leave resets the queues and advances the epoch.
     if (tid == 0) {
         const uint32_t old = __hip_atomic_fetch_add(ctrl + kCtrlExited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (old == gridDim.x - 1) {
-            for (int q = 0; q < kMaxQueues; ++q) st_dev(ctrl + ctrl_queue(q), 0u);
+            for (int i = 0; i < 2 * kMaxQueues; ++i) st_dev(ctrl + ctrl_queue(i), 0u);
             st_dev(ctrl + kCtrlExited, 0u);
             st_dev(ctrl + kCtrlEpoch, sm.epoch);
         }
@@ -1400,9 +1474,10 @@ hipError_t launch_one(const RaceArgs& a, hipStream_t stream) {
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
     if (per_cu < 1) per_cu = 1;
+    // both kinds of workgroup: at least 3 (every third finishes rows)
     long grid = (long)per_cu * cus;
-    if (grid > a.n_items) grid = a.n_items;
-    if (grid < 1) grid = 1;
+    if (grid > 3L * a.n_items) grid = 3L * a.n_items;
+    if (grid < 3) grid = 3;
     hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(kBlock), smem, stream, a);
     return hipGetLastError();
 }
