@@ -52,6 +52,8 @@ constexpr int kL2Cap = 512;
 constexpr int kRowEntries = 2;             // group entries per 16-lane row and evaluation pass
 constexpr int kCandCap = 256;
 constexpr int kWorkCap = 1024;             // (level-3 node, group) items per prefilter round
+constexpr int kRolePeriod = 5;            // workgroup roles: of every kRolePeriod blocks,
+constexpr int kRoleFinish = 2;             // kRoleFinish finish rows and the others stream
 constexpr int kChunkJobCap = 256;          // chunk draws listed by one evaluation pass
 constexpr int kHalfCap = 256;              // 4-token halves listed by one evaluation pass
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
@@ -1401,10 +1403,11 @@ __global__ __launch_bounds__(kBlock, 3) void race_kernel(RaceArgs a) {
     float* gm = reinterpret_cast<float*>(smem_raw + ((sizeof(Shared) + 15) & ~(size_t)15));
     const int tid = threadIdx.x;
     uint32_t* ctrl = ctrl_of(a);
-    // roles: blocks 2, 5, 8, ... finish rows (the launch has at least 3 blocks); with
-    // 24 or more blocks every XCD queue (block mod 8) has both kinds
-    const bool finisher = blockIdx.x % 3u == 2u;
-    const int nq = gridDim.x >= 24u ? kMaxQueues : 1;
+    // roles: of every kRolePeriod consecutive blocks the last kRoleFinish finish rows
+    // (the launch has at least kRolePeriod blocks); kRolePeriod is odd, so with
+    // 8 kRolePeriod or more blocks every XCD queue (block mod 8) has both kinds
+    const bool finisher = blockIdx.x % (unsigned)kRolePeriod >= (unsigned)(kRolePeriod - kRoleFinish);
+    const int nq = gridDim.x >= 8u * kRolePeriod ? kMaxQueues : 1;
     const int q = (int)(blockIdx.x % (unsigned)nq);
     if (tid == 0) {
         const uint32_t last = ld_dev(ctrl + kCtrlEpoch);
@@ -1474,10 +1477,10 @@ hipError_t launch_one(const RaceArgs& a, hipStream_t stream) {
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
     if (per_cu < 1) per_cu = 1;
-    // both kinds of workgroup: at least 3 (every third finishes rows)
+    // both kinds of workgroup: at least kRolePeriod blocks
     long grid = (long)per_cu * cus;
-    if (grid > 3L * a.n_items) grid = 3L * a.n_items;
-    if (grid < 3) grid = 3;
+    if (grid > (long)kRolePeriod * a.n_items) grid = (long)kRolePeriod * a.n_items;
+    if (grid < kRolePeriod) grid = kRolePeriod;
     hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(kBlock), smem, stream, a);
     return hipGetLastError();
 }
