@@ -500,6 +500,22 @@ __device__ __forceinline__ void list_near(Shared& sm, const RaceArgs& a, uint32_
 // that need token words go to LDS lists, the chunk draws are made one per thread,
 // then the halves are scored one per thread.  Items beyond the lists' capacity are
 // done by their chunk's lane.
+// Raw logits of this lane's chunk of the entries of the pass starting at `first`
+// (list end `end`; nothing is loaded past it).  Words past V are never used.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void load_pass(const RaceArgs& a, const Row& r, const Shared& sm, int first, int end,
+                                          Unit<BF16, VEC> (&ux)[kRowEntries]) {
+    const int c = threadIdx.x & 15, row = threadIdx.x >> 4;
+#pragma unroll
+    for (int q = 0; q < kRowEntries; ++q) {
+        const int e = first + row * kRowEntries + q;
+        if (e < end) {
+            const uint32_t g = sm.l2[e].id & 0xFFFFFu;
+            load_unit<BF16, VEC, false>(r.ptr, a.V, (int)(g * kGroupTokens + (uint32_t)c * 8u), ux[q]);
+        }
+    }
+}
+
 // The scored half a thread holds at the end of an evaluation pass (its logits stay
 // in the half's list entry).
 struct HalfOut {
@@ -510,13 +526,14 @@ struct HalfOut {
 
 template <bool BF16, bool VEC, int LAYOUT>
 __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, int first,
-                                            int n, int par, uint32_t k0, uint32_t k1, HalfOut& ho,
-                                            uint32_t& ovf) {
+                                            int n, int end, int par, uint32_t k0, uint32_t k1, HalfOut& ho,
+                                            uint32_t& ovf, Unit<BF16, VEC> (&ux)[kRowEntries]) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int c = tid & 15;
     const int row = tid >> 4;  // 16 rows of 16 lanes
     const uint32_t V = (uint32_t)a.V;
     constexpr uint32_t kDomain = LAYOUT == 0 ? kDomainTree : kDomainFlat;
+    // this pass's logits were loaded into ux by the caller or the previous pass
     float x[kRowEntries][8];
     Node nd[kRowEntries];
     bool act[kRowEntries];
@@ -525,8 +542,7 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
         const int e = first + row * kRowEntries + q;
         act[q] = e < first + n;
         nd[q] = act[q] ? sm.l2[e] : Node{0u, 0.f, 0u};
-        const uint32_t g = nd[q].id & 0xFFFFFu;
-        load8<BF16, VEC>(r.ptr, act[q] ? (int)V : 0, (int)(g * kGroupTokens + (uint32_t)c * 8u), x[q]);
+        unpack_unit<BF16, VEC>(ux[q], x[q]);
     }
     // What each chunk needs: its own draw (unless it holds the group minimum) and
     // the words of each half with a token that can still win.
@@ -595,6 +611,8 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
             }
         }
     }
+    // the next pass's logits, in flight while this pass draws and scores
+    load_pass<BF16, VEC>(a, r, sm, first + 16 * kRowEntries, end, ux);
     __syncthreads();
     // the other parity's counts were read in the previous pass: clear them for the next
     if (tid == 0) sm.n_ev[par ^ 1] = 0u;
@@ -701,10 +719,13 @@ __device__ __forceinline__ void flush_groups(const RaceArgs& a, const Row& r, Sh
                                              uint32_t k1) {
     const int n = min(sm.n_l2, kL2Cap);
     int par = 0;
+    Unit<BF16, VEC> ux[kRowEntries];
+    load_pass<BF16, VEC>(a, r, sm, 0, n, ux);
     for (int first = 0; first < n; first += 16 * kRowEntries, par ^= 1) {
         HalfOut ho;
         uint32_t ovf;
-        eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, 16 * kRowEntries), par, k0, k1, ho, ovf);
+        eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, 16 * kRowEntries), n, par, k0, k1, ho, ovf,
+                                       ux);
         __syncthreads();
         // every half of the pass has lowered the best: list the near-ties
         if (ho.valid) list_near(sm, a, ho.base4, ho.slot, ho.sc, sm.half[threadIdx.x].x);
