@@ -78,7 +78,8 @@ struct Half {
 struct Shared {
     float m3[256];
     float m4[16];
-    int init_v[kInit];     // seed tokens of the race (-1: none)
+    int init_v[kInit];     // seed groups of the race (-1: none)
+    int seed_tok[kInit];   // seed tokens of the race (-1: none)
     int stop[64];          // top group of every segment (-1: none)
     float part[64];        // LSE partial sum of every segment
     Node l4[kL4Cap];
@@ -833,7 +834,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
         if (e < seed_lanes) {  // whole 8-lane groups: the shuffles stay within active lanes
             const int pair = e >> 3, l = e & 7;
             const int w = pair / ns, j = pair % ns;
-            const int tv = sm.init_v[w];
+            const int tv = sm.seed_tok[w];
             const int g = tv >= 0 ? tv >> 7 : -1;
             const uint32_t slot = (uint32_t)(r.slot0 + j);
             const uint32_t av = (uint32_t)max(tv, 0);
@@ -1227,31 +1228,32 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
         }
     }
     __syncthreads();
-    {
-        // 32 lanes per seed group, 4 tokens each: the group's lowest token holding its maximum
-        static_assert(kInit * 32 == kBlock, "one pass over the seed groups");
-        const int i = tid >> 5, sub = tid & 31;
+    // Waves 0-1: the seed tokens, 16 lanes per seed group with 8 tokens each (the
+    // group's lowest token holding its maximum); wave 2: level-4 maxima, LSE, row
+    // maximum; wave 3: the context keys.  The four run side by side.
+    if (wave < 2) {
+        static_assert(kInit * 16 == 128, "one 16-lane row per seed group in waves 0-1");
+        const int i = tid >> 4, sub = tid & 15;
         const int g = sm.init_v[i];
         int tk = 0x7FFFFFFF;
         if (g >= 0) {
+            float x[8];
+            const int base = g * kGroupTokens + sub * 8;
+            load8<BF16, VEC>(r.ptr, a.V, base, x);
             const float gmax = gm[g];
 #pragma unroll
-            for (int t = 3; t >= 0; --t) {
-                const int v = g * kGroupTokens + 4 * sub + t;
-                if (v < a.V && load_logit<BF16>(r.ptr, v) == gmax) tk = v;
-            }
+            for (int t = 7; t >= 0; --t)
+                if (base + t < a.V && x[t] == gmax) tk = base + t;
         }
 #pragma unroll
-        for (int off = 16; off > 0; off >>= 1) tk = min(tk, __shfl_xor(tk, off));
-        __syncthreads();
-        if (sub == 0) sm.init_v[i] = g >= 0 && tk != 0x7FFFFFFF ? tk : -1;
-    }
-    if (tid < n4) {
-        float mx = -INFINITY;
-        for (int t = 16 * tid; t < min(n3, 16 * tid + 16); ++t) mx = fmaxf(mx, sm.m3[t]);
-        sm.m4[tid] = mx;
-    }
-    if (wave == 1) {
+        for (int off = 8; off > 0; off >>= 1) tk = min(tk, __shfl_xor(tk, off));
+        if (sub == 0) sm.seed_tok[i] = g >= 0 && tk != 0x7FFFFFFF ? tk : -1;
+    } else if (wave == 2) {
+        if (lane < n4) {
+            float mx = -INFINITY;
+            for (int t = 16 * lane; t < min(n3, 16 * lane + 16); ++t) mx = fmaxf(mx, sm.m3[t]);
+            sm.m4[lane] = mx;
+        }
         // LSE: segment i's maximum is the maximum of its groups (the same float product
         // the segment used), merged with the segments' sums in float32.
         constexpr int per = (BF16 ? kSegTokensBf16 : kSegTokensF32) / 2048;  // level-3 blocks per segment
@@ -1268,6 +1270,11 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
             const float os = __shfl_xor(si, off);
             lse_combine(mi, si, om, os);
         }
+        // row maximum over the level-3 maxima
+        float rm = -INFINITY;
+        for (int t = lane; t < n3; t += 64) rm = fmaxf(rm, sm.m3[t]);
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) rm = fmaxf(rm, __shfl_xor(rm, off));
         if (lane == 0) {
             const float lse = mi == -INFINITY ? -INFINITY : (mi + __builtin_amdgcn_logf(si)) * 0.69314718055994531f;
             if (r.kind == 0) {
@@ -1277,14 +1284,19 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
                                                     : ((size_t)r.b * a.K + r.k) * (a.gamma + 1) + r.s;
                 a.target_lse[o] = lse;
             }
+            sm.rowmax = rm;
+            sm.n_l4 = sm.n_l3 = sm.n_l2 = sm.n_cand = 0;
+            sm.n_ev[0] = sm.n_ev[1] = 0;
+            sm.best_key = ordered_key(INFINITY);
+            sm.key_min = 0x7FFFFFFF;
+            sm.key_max = -1;
         }
-    }
-    // ---- context keys.  Wave 3 reads the window's path tokens (published by earlier
-    // races of this call, or inputs) and folds both chains at once: lane 0 this
-    // row's key, lane 1 the next depth's key up to its newest token (the winner of
-    // this race).  Meanwhile thread 0 waits for the key published by the race one
-    // depth up this path, if any.
-    if (wave == 3) {
+    } else {
+        // Context keys: the window's path tokens (published by earlier races of this
+        // call, or inputs), both chains folded at once -- lane 0 this row's key, lane 1
+        // the next depth's key up to its newest token (the winner of this race) --
+        // then lane 0 waits for the key published by the race one depth up this path,
+        // if any.
         const int tk = widx >= a.m ? path_token(a, r, widx - a.m, ep) : wtok;
         const uint64_t t = (uint64_t)(wpos + r.s) + (uint64_t)(lane == 1);
         uint32_t c0 = (uint32_t)a.key, c1 = (uint32_t)(a.key >> 32);
@@ -1302,17 +1314,7 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
             sm.next0 = c0;
             sm.next1 = c1;
         }
-    }
-    if (tid == 0) {
-        float mx = -INFINITY;
-        for (int t = 0; t < n3; ++t) mx = fmaxf(mx, sm.m3[t]);
-        sm.rowmax = mx;
-        sm.n_l4 = sm.n_l3 = sm.n_l2 = sm.n_cand = 0;
-        sm.n_ev[0] = sm.n_ev[1] = 0;
-        sm.best_key = ordered_key(INFINITY);
-        sm.key_min = 0x7FFFFFFF;
-        sm.key_max = -1;
-        if (prod >= 0) {
+        if (lane == 0 && prod >= 0) {
             const uint64_t* ks = (const uint64_t*)(a.ws + a.L.keys) + 2 * (size_t)prod;
             uint64_t w0 = ld_dev(ks), w1 = ld_dev(ks + 1);
             if ((uint32_t)(w0 >> 32) != ep) w0 = wait_slot(a, ks, ep);
