@@ -52,8 +52,8 @@ constexpr int kL2Cap = 512;
 constexpr int kRowEntries = 2;             // group entries per 16-lane row and evaluation pass
 constexpr int kCandCap = 256;
 constexpr int kWorkCap = 1024;             // (level-3 node, group) items per prefilter round
-constexpr int kRolePeriod = 5;            // workgroup roles: of every kRolePeriod blocks,
-constexpr int kRoleFinish = 2;             // kRoleFinish finish rows and the others stream
+constexpr int kRolePeriod = 11;            // workgroup roles: of every kRolePeriod blocks,
+constexpr int kRoleFinish = 4;             // kRoleFinish finish rows and the others stream
 constexpr int kChunkJobCap = 256;          // chunk draws listed by one evaluation pass
 constexpr int kHalfCap = 256;              // 4-token halves listed by one evaluation pass
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
@@ -1411,16 +1411,16 @@ __device__ __forceinline__ void decode_item(const RaceArgs& a, const Shared& sm,
     }
 }
 
-// Three workgroups per CU: 168 VGPRs, enough for the race without spills (four
-// workgroups cap registers at 128 and spill).  Every third workgroup finishes rows;
-// the others only stream segments, so the streaming loop (software-pipelined) and
-// the races neither share a loop nor wait for each other.  Both kinds take work in
-// order from per-XCD queues (row R goes to queue R mod nq for both): streaming
-// never waits, and a finishing workgroup waits only for segments (streamed without
-// waiting) and for races of rows earlier in the order (taken earlier by running
-// finishing workgroups), so every wait ends.
+// Four workgroups per CU (128 VGPRs).  Of every kRolePeriod blocks, kRoleFinish
+// finish rows and the others only stream segments, so the streaming loop
+// (software-pipelined) and the races neither share a loop nor wait for each other
+// (the share of finishing blocks was measured: about 0.36 balances the two).  Both
+// kinds take work in order from per-XCD queues (row R goes to queue R mod nq for
+// both): streaming never waits, and a finishing workgroup waits only for segments
+// (streamed without waiting) and for races of rows earlier in the order (taken
+// earlier by running finishing workgroups), so every wait ends.
 template <bool BF16, bool VEC, int LAYOUT>
-__global__ __launch_bounds__(kBlock, 3) void race_kernel(RaceArgs a) {
+__global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Shared& sm = *reinterpret_cast<Shared*>(smem_raw);
     float* gm = reinterpret_cast<float*>(smem_raw + ((sizeof(Shared) + 15) & ~(size_t)15));
