@@ -46,7 +46,6 @@ namespace psd {
 namespace {
 
 constexpr int kInit = 8;                   // seed tokens of a race (segment top tokens)
-constexpr int kL4Cap = 512;                // <= 32 slots x 16 level-4 nodes
 constexpr int kL3Cap = 512;
 constexpr int kL2Cap = 512;
 constexpr int kRowEntries = 2;             // group entries per 16-lane row and evaluation pass
@@ -82,7 +81,6 @@ struct Shared {
     int seed_tok[kInit];   // seed tokens of the race (-1: none)
     int stop[64];          // top group of every segment (-1: none)
     float part[64];        // LSE partial sum of every segment
-    Node l4[kL4Cap];
     Node l3[kL3Cap];
     Node l2[kL2Cap];
     int cand_v[kCandCap];
@@ -114,6 +112,12 @@ struct Shared {
     uint32_t cj_p[kChunkJobCap];      // and position
     Half half[kHalfCap];
 };
+
+// Dynamic LDS after Shared: the group maxima gm (ng floats, rounded up to 4), then
+// the level-4 node list of a race (K slots x level-4 nodes; sized at launch).
+__device__ __forceinline__ Node* level4_list(const float* gm, int ng) {
+    return (Node*)(gm + ((ng + 3) & ~3));
+}
 
 struct Row {
     int kind;  // 0 draft, 1 target
@@ -896,7 +900,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
             const uint32_t rp = uniform_position(wr.w1, wr.w2, V);
             const uint32_t cs = i4 << kShift4, n = node_end(kShift4, i4, V) - cs;
             const bool hold = rp >= cs && rp < cs + n;
-            sm.l4[it] = Node{(slot << 20) | i4, hold ? rm : rm + exp1_f32(w4.w0) / (float)n,
+            level4_list(gm, ng)[it] = Node{(slot << 20) | i4, hold ? rm : rm + exp1_f32(w4.w0) / (float)n,
                              hold ? rp : cs + uniform_position(w4.w1, w4.w2, n)};
         }
     }
@@ -914,7 +918,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
             if (done) break;
             const int e = base + tid;
             if (e < nB) {
-                const Node pa = sm.l4[e >> 4];
+                const Node pa = level4_list(gm, ng)[e >> 4];
                 const uint32_t i4 = pa.id & 0xFFFFFu;
                 const uint32_t i3 = i4 * 16u + (uint32_t)(e & 15);
                 const float thr = current_threshold(sm);
@@ -1487,11 +1491,16 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
     }
 }
 
-size_t shared_bytes(int ng) { return ((sizeof(Shared) + 15) & ~(size_t)15) + (size_t)ng * sizeof(float); }
+// Shared, the group maxima and the level-4 list (K slots x level-4 nodes, 256 groups
+// each), in the order level4_list assumes.
+size_t shared_bytes(int ng, int K) {
+    return ((sizeof(Shared) + 15) & ~(size_t)15) + (size_t)((ng + 3) & ~3) * sizeof(float) +
+           (size_t)K * (size_t)((ng + 255) / 256) * sizeof(Node);
+}
 
 template <bool BF16, bool VEC, int LAYOUT>
 hipError_t launch_one(const RaceArgs& a, hipStream_t stream) {
-    const size_t smem = shared_bytes(a.L.ng);
+    const size_t smem = shared_bytes(a.L.ng, a.K);
     auto fn = race_kernel<BF16, VEC, LAYOUT>;
     int per_cu = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, smem);
@@ -1519,6 +1528,5 @@ hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipSt
     return layout == 0 ? launch_one<false, false, 0>(a, stream) : launch_one<false, false, 1>(a, stream);
 }
 
-size_t race_shared_bytes(int ng) { return shared_bytes(ng); }
 
 }  // namespace psd
