@@ -55,7 +55,10 @@ constexpr int kRolePeriod = 11;            // workgroup roles: of every kRolePer
 constexpr int kRoleFinish = 4;             // kRoleFinish finish rows and the others stream
 constexpr int kChunkJobCap = 256;          // chunk draws listed by one evaluation pass
 constexpr int kHalfCap = 256;              // 4-token halves listed by one evaluation pass
+constexpr int kPassGroups = 16 * kRowEntries;  // group entries of one evaluation pass
+constexpr int kBuckets = 32;               // bound buckets of the group list's evaluation order
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
+constexpr float kCutSlack = 1e-3f;         // slack of the per-token logit cut (score units)
 constexpr uint32_t kSpinLimit = 1u << 22;  // bounded waits for other workgroups' slots
 constexpr uint32_t kErrSpin = 1u, kErrCand = 2u;
 
@@ -111,7 +114,13 @@ struct Shared {
     float cj_m[kChunkJobCap];         // its minimum clock
     uint32_t cj_p[kChunkJobCap];      // and position
     Half half[kHalfCap];
+    // evaluation order of the group list (order_groups)
+    float ord_wmin[kBlock / 64];          // per-wave smallest bound
+    int ord_hist[kBuckets];               // entries per bound bucket
+    int ord_bmin[kBuckets];               // smallest bound per bucket (ordered key)
+    int ord_pass[kL2Cap / kPassGroups];   // bucket of each pass's first entry
 };
+static_assert(sizeof(Half) * kHalfCap >= sizeof(Node) * kL2Cap, "the reordering stages the group list in half[]");
 
 // Dynamic LDS after Shared: the group maxima gm (ng floats, rounded up to 4), then
 // the level-4 node list of a race (K slots x level-4 nodes; sized at launch).
@@ -563,11 +572,18 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
         hm[q][0] = hm[q][1] = 0u;
         cj[q] = false;
         if (act[q] && lnm - gm[g] * r.invT <= thr0) {
+            // a token can reach thr0 only if lnm - x / T <= thr0, i.e. x >= (lnm -
+            // thr0) T; the cut is lowered by kCutSlack, far more than the rounding of
+            // either form, so the listed tokens include every such token
+            const float xc = (lnm - thr0 - kCutSlack) * r.T;
+            uint32_t m8 = 0u;
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-                if (base + (uint32_t)i < V && x[q][i] != -INFINITY && lnm - x[q][i] * r.invT <= thr0)
-                    hm[q][i >> 2] |= 1u << (i & 3);
-            if (LAYOUT == 0 && (hm[q][0] | hm[q][1])) {
+            for (int i = 0; i < 8; ++i) m8 |= (uint32_t)(x[q][i] >= xc) << i;
+            const int nv = (int)V - (int)base;  // tokens of this chunk inside the row
+            if (nv < 8) m8 &= nv > 0 ? (1u << nv) - 1u : 0u;
+            hm[q][0] = m8 & 15u;
+            hm[q][1] = m8 >> 4;
+            if (LAYOUT == 0 && m8) {
                 const uint32_t ce = node_end(kShift1, g * 16u + (uint32_t)c, V);
                 cj[q] = !(nd[q].p >= base && nd[q].p < ce);
             }
@@ -577,16 +593,11 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
     }
     // list positions: wave prefix sum of (draws | halves << 16), one atomic per wave
     const uint32_t mine = (uint32_t)ncj | ((uint32_t)nh << 16);
-    uint32_t incl = mine;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t o = (uint32_t)__shfl_up((int)incl, off);
-        if (lane >= off) incl += o;
-    }
-    const uint32_t wtot = (uint32_t)__shfl((int)incl, 63);
+    const uint32_t incl = wave_incl_sum(mine);
+    const uint32_t wtot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
     uint32_t wbase = 0u;
     if (lane == 0 && wtot != 0u) wbase = atomicAdd(&sm.n_ev[par], wtot);
-    const uint32_t mb = (uint32_t)__shfl((int)wbase, 0) + incl - mine;
+    const uint32_t mb = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 0) + incl - mine;
     int jc = (int)(mb & 0xFFFFu), jh = (int)(mb >> 16);
     ovf = 0u;  // halves beyond the list (bit 8q + 4h + t: token t of half h of entry q)
 #pragma unroll
@@ -617,7 +628,7 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
         }
     }
     // the next pass's logits, in flight while this pass draws and scores
-    load_pass<BF16, VEC>(a, r, sm, first + 16 * kRowEntries, end, ux);
+    load_pass<BF16, VEC>(a, r, sm, first + kPassGroups, end, ux);
     __syncthreads();
     // the other parity's counts were read in the previous pass: clear them for the next
     if (tid == 0) sm.n_ev[par ^ 1] = 0u;
@@ -717,20 +728,100 @@ __device__ __forceinline__ void eval_overflow(const RaceArgs& a, const Row& r, S
     }
 }
 
+// Reorder the first n entries of the group list by their bounds (ln of the group
+// minimum minus the scaled group maximum), counting-sorted into kBuckets buckets
+// between the smallest bound and the threshold; entries above the threshold are
+// dropped.  Evaluating the most promising groups first lowers the threshold
+// early, and a pass whose first entry's bucket lies above the threshold ends the
+// evaluation (later buckets hold larger bounds).  Returns the kept count.  The
+// sort stages the list in half[], which is free between evaluation passes.
+// Called by every thread.
+template <int LAYOUT>
+__device__ __forceinline__ int order_groups(const Row& r, Shared& sm, const float* gm, int n) {
+    static_assert(kL2Cap <= 2 * kBlock, "two entries per thread");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const float thr = current_threshold(sm);
+    Node nd[2];
+    float b[2];
+    float wmin = INFINITY;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int e = tid + i * kBlock;
+        nd[i] = e < n ? sm.l2[e] : Node{0u, 0.f, 0u};
+        const float lnm = LAYOUT == 0 ? ln_f32(nd[i].m) : kLnClockFloor;
+        b[i] = e < n ? lnm - gm[nd[i].id & 0xFFFFFu] * r.invT : INFINITY;
+        if (b[i] <= thr) wmin = fminf(wmin, b[i]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) wmin = fminf(wmin, __shfl_xor(wmin, off));
+    if (lane == 0) sm.ord_wmin[tid >> 6] = wmin;
+    if (tid < kBuckets) {
+        sm.ord_hist[tid] = 0;
+        sm.ord_bmin[tid] = ordered_key(INFINITY);
+    }
+    __syncthreads();
+    float bmin = sm.ord_wmin[0];
+#pragma unroll
+    for (int w = 1; w < kBlock / 64; ++w) bmin = fminf(bmin, sm.ord_wmin[w]);
+    // bucket = floor((b - bmin) * scale), non-decreasing in b
+    const float scale = thr > bmin ? (float)kBuckets / (thr - bmin) : 0.f;
+    int k[2], rank[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        k[i] = -1;
+        rank[i] = 0;
+        if (b[i] <= thr) {
+            k[i] = min(kBuckets - 1, (int)((b[i] - bmin) * scale));
+            rank[i] = atomicAdd(&sm.ord_hist[k[i]], 1);
+            atomicMin(&sm.ord_bmin[k[i]], ordered_key(b[i]));
+        }
+    }
+    __syncthreads();
+    // bucket starts: a prefix sum over the kBuckets counts in every wave
+    const int h = lane < kBuckets ? sm.ord_hist[lane] : 0;
+    int incl = h;
+#pragma unroll
+    for (int off = 1; off < kBuckets; off <<= 1) {
+        const int o = __shfl_up(incl, off);
+        if (lane >= off) incl += o;
+    }
+    const int excl = incl - h;
+    const int kept = __shfl(incl, kBuckets - 1);
+    Node* tmp = reinterpret_cast<Node*>(sm.half);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int start = __shfl(excl, max(k[i], 0));
+        if (k[i] >= 0) {
+            const int dst = start + rank[i];
+            tmp[dst] = nd[i];
+            if (dst % kPassGroups == 0) sm.ord_pass[dst / kPassGroups] = k[i];
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < kept; e += kBlock) sm.l2[e] = tmp[e];
+    __syncthreads();
+    return kept;
+}
+
 // Evaluate and empty the group list.  Callers read the list count after a barrier
 // and before any push of the current pass.
 template <bool BF16, bool VEC, int LAYOUT>
 __device__ __forceinline__ void flush_groups(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0,
                                              uint32_t k1) {
-    const int n = min(sm.n_l2, kL2Cap);
+    int n = min(sm.n_l2, kL2Cap);
+    const bool ordered = n > kPassGroups;
+    if (ordered) n = order_groups<LAYOUT>(r, sm, gm, n);
     int par = 0;
     Unit<BF16, VEC> ux[kRowEntries];
     load_pass<BF16, VEC>(a, r, sm, 0, n, ux);
-    for (int first = 0; first < n; first += 16 * kRowEntries, par ^= 1) {
+    for (int first = 0; first < n; first += kPassGroups, par ^= 1) {
+        // every later entry's bound is at least its bucket's smallest (the threshold
+        // and the buckets are read after the previous pass's last barrier)
+        if (ordered && first > 0 && ordered_value(sm.ord_bmin[sm.ord_pass[first / kPassGroups]]) > current_threshold(sm))
+            break;
         HalfOut ho;
         uint32_t ovf;
-        eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, 16 * kRowEntries), n, par, k0, k1, ho, ovf,
-                                       ux);
+        eval_groups<BF16, VEC, LAYOUT>(a, r, sm, gm, first, min(n - first, kPassGroups), n, par, k0, k1, ho, ovf, ux);
         __syncthreads();
         // every half of the pass has lowered the best: list the near-ties
         if (ho.valid) list_near(sm, a, ho.base4, ho.slot, ho.sc, sm.half[threadIdx.x].x);
@@ -806,13 +897,15 @@ __device__ __forceinline__ int path_shift(int l) {
     return l == 1 ? kShift4 : l == 2 ? kShift3 : l == 3 ? kShift2 : kShift1;
 }
 
-// Philox words of path node l of token v (tree clocks): 0 = root, 1..4 = the
-// token's level-4..1 ancestors, 5 = the token's own word block.  The counter is
-// selected per lane, so lanes of one token draw their nodes in a single call.
+// Counter words (c0, c2) of path node l of token v (tree clocks): 0 = root, 1..4 =
+// the token's level-4..1 ancestors, 5 = the token's own word block.  The counter
+// is selected per lane, so lanes of one token draw their nodes in a single call.
+__device__ __forceinline__ uint32_t path_c0(int l, uint32_t v) { return l == 0 ? 0u : l == 5 ? v >> 3 : v >> path_shift(l); }
+__device__ __forceinline__ uint32_t path_c2(int l, uint32_t v) {
+    return l == 0 ? 5u : l == 5 ? 8u + ((v >> 2) & 1u) : (uint32_t)(5 - l);
+}
 __device__ __forceinline__ Words path_draw(int l, uint32_t v, uint32_t slot, uint32_t k0, uint32_t k1) {
-    const uint32_t c0 = l == 0 ? 0u : l == 5 ? v >> 3 : v >> path_shift(l);
-    const uint32_t c2 = l == 0 ? 5u : l == 5 ? 8u + ((v >> 2) & 1u) : (uint32_t)(5 - l);
-    return philox(c0, slot, c2, kDomainTree, k0, k1);
+    return philox(path_c0(l, v), slot, path_c2(l, v), kDomainTree, k0, k1);
 }
 
 __device__ __forceinline__ uint32_t pick_word(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3, uint32_t i) {
@@ -828,11 +921,14 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
     const int ns = r.nslots;
     const int n4 = (int)((V + (1u << kShift4) - 1) >> kShift4);
     // Pass A: the seed tokens (each the largest logit of its group) in every slot --
-    // tree clocks: 8 lanes per (token, slot), lane l drawing path node l -- and, for
-    // tree clocks, the minimum of every (slot, level-4 node), one item per lane.
+    // tree clocks: 8 lanes per (token, slot), lane l < 6 drawing path node l -- and,
+    // for tree clocks, the minimum of every (slot, level-4 node): lanes 6 and 7 of the
+    // seed lanes of slot j take its first 2 kInit level-4 nodes (with the root drawn
+    // by lane 0), lanes past the seed lanes the rest, one item per lane.
     const int nseed = kInit;
     const int seed_lanes = nseed * ns * 8;
-    const int nA = seed_lanes + (LAYOUT == 0 ? ns * n4 : 0);
+    const int n4x = max(0, n4 - 2 * nseed);  // level-4 nodes per slot past the seed lanes
+    const int nA = seed_lanes + (LAYOUT == 0 ? ns * n4x : 0);
     for (int e0 = 0; e0 < nA; e0 += kBlock) {
         const int e = e0 + tid;
         if (e < seed_lanes) {  // whole 8-lane groups: the shuffles stay within active lanes
@@ -848,17 +944,27 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
                 // E'/V, level-4..1 node E'/size at a uniform position in it, token E'
                 float val = 0.f;
                 uint32_t pos = 0u;
-                if (l < 6) {
-                    const Words wd = path_draw(l, av, slot, k0, k1);
-                    const int sh = path_shift(l);
-                    const uint32_t cs = (l == 0 || l == 5) ? 0u : (av >> sh) << sh;
-                    const uint32_t n = l == 0 ? V : l == 5 ? 1u : node_end(sh, av >> sh, V) - cs;
+                const uint32_t i4 = (uint32_t)(2 * w + (l - 6));  // level-4 node of lanes 6 and 7
+                const bool l4 = l >= 6 && (int)i4 < n4;
+                if (l < 6 || l4) {
+                    const Words wd = philox(l4 ? i4 : path_c0(l, av), slot, l4 ? 4u : path_c2(l, av), kDomainTree, k0, k1);
+                    const int sh = l4 ? kShift4 : path_shift(l);
+                    const uint32_t node = l4 ? i4 : av >> sh;
+                    const uint32_t cs = (l == 0 || l == 5) ? 0u : node << sh;
+                    const uint32_t n = l == 0 ? V : l == 5 ? 1u : node_end(sh, node, V) - cs;
                     val = exp1_f32(l == 5 ? pick_word(wd.w0, wd.w1, wd.w2, wd.w3, av & 3u) : wd.w0) / (float)n;
                     pos = cs + uniform_position(wd.w1, wd.w2, n);
                 }
                 const int base = tid & ~7;
                 float m = __shfl(val, base);
                 uint32_t p = (uint32_t)__shfl((int)pos, base);
+                if (l4) {
+                    // the root (lane 0) or this node holds the level-4 node's minimum
+                    const uint32_t cs = i4 << kShift4, ce = node_end(kShift4, i4, V);
+                    const bool hold = p >= cs && p < ce;
+                    level4_list(gm, ng)[j * n4 + (int)i4] =
+                        Node{(slot << 20) | i4, hold ? m : m + val, hold ? p : pos};
+                }
 #pragma unroll
                 for (int q = 1; q <= 4; ++q) {
                     const float vq = __shfl(val, base + q);
@@ -890,9 +996,10 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
                 }
             }
         } else if (LAYOUT == 0 && e < nA) {
-            // level-4 node i4 of slot j: root and node draws issued together
-            const int it = e - seed_lanes, j = it / n4;
-            const uint32_t i4 = (uint32_t)(it % n4);
+            // level-4 node i4 of slot j past the seed lanes: root and node draws
+            // issued together
+            const int it = e - seed_lanes, j = it / n4x;
+            const uint32_t i4 = (uint32_t)(2 * nseed + it % n4x);
             const uint32_t slot = (uint32_t)(r.slot0 + j);
             const Words wr = philox(0u, slot, 5u, kDomainTree, k0, k1);
             const Words w4 = philox(i4, slot, 4u, kDomainTree, k0, k1);
@@ -900,7 +1007,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
             const uint32_t rp = uniform_position(wr.w1, wr.w2, V);
             const uint32_t cs = i4 << kShift4, n = node_end(kShift4, i4, V) - cs;
             const bool hold = rp >= cs && rp < cs + n;
-            level4_list(gm, ng)[it] = Node{(slot << 20) | i4, hold ? rm : rm + exp1_f32(w4.w0) / (float)n,
+            level4_list(gm, ng)[j * n4 + (int)i4] = Node{(slot << 20) | i4, hold ? rm : rm + exp1_f32(w4.w0) / (float)n,
                              hold ? rp : cs + uniform_position(w4.w1, w4.w2, n)};
         }
     }
