@@ -15,7 +15,11 @@ ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
          "-packed-fp32-ops", "-Wno-unused-command-line-argument"]
 # The race kernel treats NaN logits as undefined input, so float max needs no NaN quieting.
-EXTRA = {"psd_race.hip": ["-fno-honor-nans"]}
+# Its LDS atomics (the best score, list counters) are issued as they are: the default
+# atomic optimizer turns a same-address atomic with per-lane values into a scalar
+# loop over the active lanes (about 70 cycles per lane), far slower than the LDS
+# serialising the lanes' atomics itself.
+EXTRA = {"psd_race.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
 
 
 def hipcc() -> str:
