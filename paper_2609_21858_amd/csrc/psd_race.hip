@@ -692,9 +692,10 @@ __device__ __forceinline__ void eval_overflow(const RaceArgs& a, const Row& r, S
                                               uint32_t k0, uint32_t k1) {
     const int tid = threadIdx.x, c = tid & 15, row = tid >> 4;
     const uint32_t V = (uint32_t)a.V;
-#pragma unroll
+    // (rare: one copy of the code, not unrolled)
+#pragma unroll 1
     for (int q = 0; q < kRowEntries; ++q) {
-#pragma unroll
+#pragma unroll 1
         for (int h = 0; h < 2; ++h) {
             const uint32_t mask = (ovf >> (8 * q + 4 * h)) & 15u;
             float sc[4] = {INFINITY, INFINITY, INFINITY, INFINITY}, xs[4] = {0.f, 0.f, 0.f, 0.f};
@@ -840,50 +841,56 @@ __device__ __forceinline__ void flush_groups(const RaceArgs& a, const Row& r, Sh
 // Expand listed level-3 nodes into groups (tree clocks), evaluating the groups as
 // the list fills.  A draw-free prefilter (group maximum against the node's
 // minimum) first compacts the (node, group) items that can still win into a work
-// list, so that the draws run on full wavefronts.
+// list, so that the draws run on full wavefronts.  One loop with a single
+// evaluation call site: it refills the work list when it is used up, evaluates the
+// group list when it may overflow or at the end, and draws kBlock items per step.
 template <bool BF16, bool VEC>
 __device__ __forceinline__ void flush_l3(const RaceArgs& a, const Row& r, Shared& sm, const float* gm, uint32_t k0, uint32_t k1) {
     const int tid = threadIdx.x;
     const int n = min(sm.n_l3, kL3Cap) * 16;
     const uint32_t V = (uint32_t)a.V;
     const int ng = a.L.ng;
-    for (int base = 0; base < n; base += kWorkCap) {
-        if (tid == 0) sm.n_work = 0;
-        __syncthreads();
-        {
+    int base = 0, nw = 0, wb = 0;  // next prefilter item; work list size; next work item
+    for (;;) {
+        // (uniform: nw is read by every thread after a barrier; a list found empty
+        // is 0 when thread 0 clears it again)
+        while (wb >= nw && base < n) {
+            if (tid == 0) sm.n_work = 0;
+            __syncthreads();
             const float thr = current_threshold(sm);
             for (int e = base + tid; e < min(n, base + kWorkCap); e += kBlock) {
                 const Node pa = sm.l3[e >> 4];
                 const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
                 if ((int)g < ng && ln_f32(pa.m) - gm[g] * r.invT <= thr) sm.work[atomicAdd(&sm.n_work, 1)] = e;
             }
+            __syncthreads();
+            nw = sm.n_work;
+            wb = 0;
+            base += kWorkCap;
         }
+        const bool done = wb >= nw;
+        // The count is read by every thread before any thread of this step pushes.
+        const bool flush = done ? sm.n_l2 > 0 : sm.n_l2 > kL2Cap - kBlock;
         __syncthreads();
-        const int nw = sm.n_work;
-        for (int wb = 0; wb < nw; wb += kBlock) {
-            // The count is read by every thread before any thread of this pass pushes.
-            const bool flush = sm.n_l2 > kL2Cap - kBlock;
-            __syncthreads();
-            if (flush) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
-            const int i = wb + tid;
-            if (i < nw) {
-                const int e = sm.work[i];
-                const Node pa = sm.l3[e >> 4];
-                const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
-                const float thr = current_threshold(sm);
-                if (ln_f32(pa.m) - gm[g] * r.invT <= thr) {
-                    const uint32_t slot = pa.id >> 20;
-                    float m;
-                    uint32_t p;
-                    child_min_f32(pa.m, pa.p, 2, g, g << kShift2, node_end(kShift2, g, V), slot, k0, k1, m, p);
-                    if (ln_f32(m) - gm[g] * r.invT <= thr) push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | g, m, p);
-                }
+        if (flush) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
+        if (done) break;
+        const int i = wb + tid;
+        if (i < nw) {
+            const int e = sm.work[i];
+            const Node pa = sm.l3[e >> 4];
+            const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
+            const float thr = current_threshold(sm);
+            if (ln_f32(pa.m) - gm[g] * r.invT <= thr) {
+                const uint32_t slot = pa.id >> 20;
+                float m;
+                uint32_t p;
+                child_min_f32(pa.m, pa.p, 2, g, g << kShift2, node_end(kShift2, g, V), slot, k0, k1, m, p);
+                if (ln_f32(m) - gm[g] * r.invT <= thr) push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | g, m, p);
             }
-            __syncthreads();
         }
+        wb += kBlock;
+        __syncthreads();
     }
-    if (sm.n_l2 > 0) flush_groups<BF16, VEC, 0>(a, r, sm, gm, k0, k1);
-    __syncthreads();
     if (tid == 0) sm.n_l3 = 0;
     __syncthreads();
 }
