@@ -118,7 +118,7 @@ struct Shared {
     float ord_wmin[kBlock / 64];          // per-wave smallest bound
     int ord_hist[kBuckets];               // entries per bound bucket
     int ord_bmin[kBuckets];               // smallest bound per bucket (ordered key)
-    int ord_pass[(kL2Cap + kPassGroups - 1) / kPassGroups];  // bucket of each pass's first entry
+    int ord_pass[kL2Cap / kPassGroups];   // bucket of each pass's first entry
 };
 static_assert(sizeof(Half) * kHalfCap >= sizeof(Node) * kL2Cap, "the reordering stages the group list in half[]");
 
@@ -522,29 +522,11 @@ __device__ __forceinline__ void load_pass(const RaceArgs& a, const Row& r, const
     const int c = threadIdx.x & 15, row = threadIdx.x >> 4;
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
-        const int e = first + q * 16 + row;
+        const int e = first + row * kRowEntries + q;
         if (e < end) {
             const uint32_t g = sm.l2[e].id & 0xFFFFFu;
             load_unit<BF16, VEC, false>(r.ptr, a.V, (int)(g * kGroupTokens + (uint32_t)c * 8u), ux[q]);
         }
-    }
-}
-
-// Logits of half h (tokens 4h .. 4h + 3) of a loaded unit.
-template <bool BF16, bool VEC>
-__device__ __forceinline__ void unit_half(const Unit<BF16, VEC>& u, int h, float (&x)[4]) {
-    if constexpr (BF16) {
-        const uint32_t w0 = h ? u.w[0].z : u.w[0].x, w1 = h ? u.w[0].w : u.w[0].y;
-        x[0] = bf16_lo(w0);
-        x[1] = bf16_hi(w0);
-        x[2] = bf16_lo(w1);
-        x[3] = bf16_hi(w1);
-    } else {
-        const uint4 w = h ? u.w[1] : u.w[0];
-        x[0] = __uint_as_float(w.x);
-        x[1] = __uint_as_float(w.y);
-        x[2] = __uint_as_float(w.z);
-        x[3] = __uint_as_float(w.w);
     }
 }
 
@@ -565,45 +547,49 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
     const int row = tid >> 4;  // 16 rows of 16 lanes
     const uint32_t V = (uint32_t)a.V;
     constexpr uint32_t kDomain = LAYOUT == 0 ? kDomainTree : kDomainFlat;
-    // This pass's logits were loaded into ux by the caller or the previous pass;
-    // entry q * 16 + row of the pass is held by 16-lane row `row`, so a short pass
-    // occupies whole rows of low q.  First, per entry, what each chunk needs: its own
-    // draw (unless it holds the group minimum) and the words of each half with a
-    // token that can still win (bits 8q + 4h + t of hms, bit q of cjs).
+    // this pass's logits were loaded into ux by the caller or the previous pass
+    float x[kRowEntries][8];
+    Node nd[kRowEntries];
+    bool act[kRowEntries];
+#pragma unroll
+    for (int q = 0; q < kRowEntries; ++q) {
+        const int e = first + row * kRowEntries + q;
+        act[q] = e < first + n;
+        nd[q] = act[q] ? sm.l2[e] : Node{0u, 0.f, 0u};
+        unpack_unit<BF16, VEC>(ux[q], x[q]);
+    }
+    // What each chunk needs: its own draw (unless it holds the group minimum) and
+    // the words of each half with a token that can still win.
     const float thr0 = current_threshold(sm);
-    uint32_t hms = 0u, cjs = 0u;
+    uint32_t hm[kRowEntries][2];
+    bool cj[kRowEntries];
     int ncj = 0, nh = 0;
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
-        const int le = q * 16 + row;
-        if (le < n) {
-            const Node nd = sm.l2[first + le];
-            const uint32_t g = nd.id & 0xFFFFFu;
-            const uint32_t base = g * kGroupTokens + (uint32_t)c * 8u;
-            const float lnm = LAYOUT == 0 ? ln_f32(nd.m) : kLnClockFloor;
-            if (lnm - gm[g] * r.invT <= thr0) {
-                // a token can reach thr0 only if lnm - x / T <= thr0, i.e. x >= (lnm -
-                // thr0) T; the cut is lowered by kCutSlack, far more than the rounding
-                // of either form, so the listed tokens include every such token
-                const float xc = (lnm - thr0 - kCutSlack) * r.T;
-                float x[8];
-                unpack_unit<BF16, VEC>(ux[q], x);
-                uint32_t m8 = 0u;
+        const uint32_t g = nd[q].id & 0xFFFFFu;
+        const uint32_t base = g * kGroupTokens + (uint32_t)c * 8u;
+        const float lnm = LAYOUT == 0 ? ln_f32(nd[q].m) : kLnClockFloor;
+        hm[q][0] = hm[q][1] = 0u;
+        cj[q] = false;
+        if (act[q] && lnm - gm[g] * r.invT <= thr0) {
+            // a token can reach thr0 only if lnm - x / T <= thr0, i.e. x >= (lnm -
+            // thr0) T; the cut is lowered by kCutSlack, far more than the rounding of
+            // either form, so the listed tokens include every such token
+            const float xc = (lnm - thr0 - kCutSlack) * r.T;
+            uint32_t m8 = 0u;
 #pragma unroll
-                for (int i = 0; i < 8; ++i) m8 |= (uint32_t)(x[i] >= xc) << i;
-                const int nv = (int)V - (int)base;  // tokens of this chunk inside the row
-                if (nv < 8) m8 &= nv > 0 ? (1u << nv) - 1u : 0u;
-                hms |= m8 << (8 * q);
-                nh += (int)((m8 & 15u) != 0u) + (int)((m8 >> 4) != 0u);
-                if (LAYOUT == 0 && m8) {
-                    const uint32_t ce = node_end(kShift1, g * 16u + (uint32_t)c, V);
-                    if (!(nd.p >= base && nd.p < ce)) {
-                        cjs |= 1u << q;
-                        ++ncj;
-                    }
-                }
+            for (int i = 0; i < 8; ++i) m8 |= (uint32_t)(x[q][i] >= xc) << i;
+            const int nv = (int)V - (int)base;  // tokens of this chunk inside the row
+            if (nv < 8) m8 &= nv > 0 ? (1u << nv) - 1u : 0u;
+            hm[q][0] = m8 & 15u;
+            hm[q][1] = m8 >> 4;
+            if (LAYOUT == 0 && m8) {
+                const uint32_t ce = node_end(kShift1, g * 16u + (uint32_t)c, V);
+                cj[q] = !(nd[q].p >= base && nd[q].p < ce);
             }
         }
+        ncj += (int)cj[q];
+        nh += (int)(hm[q][0] != 0u) + (int)(hm[q][1] != 0u);
     }
     // list positions: wave prefix sum of (draws | halves << 16), one atomic per wave
     const uint32_t mine = (uint32_t)ncj | ((uint32_t)nh << 16);
@@ -613,32 +599,29 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
     if (lane == 0 && wtot != 0u) wbase = atomicAdd(&sm.n_ev[par], wtot);
     const uint32_t mb = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 0) + incl - mine;
     int jc = (int)(mb & 0xFFFFu), jh = (int)(mb >> 16);
-    ovf = hms;  // halves beyond the list keep their bits (8q + 4h + t)
+    ovf = 0u;  // halves beyond the list (bit 8q + 4h + t: token t of half h of entry q)
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
-        if (((hms >> (8 * q)) & 0xFFu) == 0u) continue;
-        const int le = q * 16 + row;
+        const int le = row * kRowEntries + q;
         int cref = -1;
-        if ((cjs >> q) & 1u) {
+        if (cj[q]) {
             cref = jc;
             if (jc < kChunkJobCap) sm.cjob[jc] = ((uint32_t)le << 4) | (uint32_t)c;
             ++jc;
         }
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            const uint32_t hm = (hms >> (8 * q + 4 * h)) & 15u;
-            if (hm) {
+            if (hm[q][h]) {
                 if (jh < kHalfCap) {
                     Half& hf = sm.half[jh];
-                    hf.desc = ((uint32_t)le << 9) | ((uint32_t)c << 5) | ((uint32_t)h << 4) | hm;
+                    hf.desc = ((uint32_t)le << 9) | ((uint32_t)c << 5) | ((uint32_t)h << 4) | hm[q][h];
                     hf.cref = cref;
-                    float xs[4];
-                    unit_half<BF16, VEC>(ux[q], h, xs);
-                    hf.x[0] = xs[0];
-                    hf.x[1] = xs[1];
-                    hf.x[2] = xs[2];
-                    hf.x[3] = xs[3];
-                    ovf &= ~(hm << (8 * q + 4 * h));
+                    hf.x[0] = x[q][4 * h];
+                    hf.x[1] = x[q][4 * h + 1];
+                    hf.x[2] = x[q][4 * h + 2];
+                    hf.x[3] = x[q][4 * h + 3];
+                } else {
+                    ovf |= hm[q][h] << (8 * q + 4 * h);
                 }
                 ++jh;
             }
@@ -718,7 +701,7 @@ __device__ __forceinline__ void eval_overflow(const RaceArgs& a, const Row& r, S
             float sc[4] = {INFINITY, INFINITY, INFINITY, INFINITY}, xs[4] = {0.f, 0.f, 0.f, 0.f};
             uint32_t base4 = 0u, slot = 0u;
             if (mask != 0u) {
-                const Node pn = sm.l2[first + q * 16 + row];
+                const Node pn = sm.l2[first + row * kRowEntries + q];
                 slot = pn.id >> 20;
                 const uint32_t g = pn.id & 0xFFFFFu;
                 const uint32_t chunk = g * 16u + (uint32_t)c;
