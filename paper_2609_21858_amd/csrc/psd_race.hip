@@ -50,7 +50,7 @@ constexpr int kL3Cap = 512;
 constexpr int kL2Cap = 512;
 constexpr int kRowEntries = 2;             // group entries per 16-lane row and evaluation pass
 constexpr int kCandCap = 256;
-constexpr int kWorkCap = 1024;             // (level-3 node, group) items per prefilter round
+constexpr int kWorkCap = 2048;             // (level-3 node, group) items per prefilter round
 constexpr int kRolePeriod = 11;            // workgroup roles: of every kRolePeriod blocks,
 constexpr int kRoleFinish = 4;             // kRoleFinish finish rows and the others stream
 constexpr int kChunkJobCap = 256;          // chunk draws listed by one evaluation pass
@@ -107,7 +107,7 @@ struct Shared {
     uint32_t next0, next1;  // partial context key of the path's next depth
     int win[32];            // context tokens (own window, next depth's window)
     int key_min, key_max;   // (token, slot) range of the candidates near the best
-    int work[kWorkCap];     // compacted work items
+    uint16_t work[kWorkCap];  // compacted work items (level-3 list index * 16 + group)
     int n_work;
     uint32_t n_ev[2];                 // listed chunk draws (low 16 bits) and halves (high 16 bits), per pass parity
     uint32_t cjob[kChunkJobCap];      // chunk draw: entry << 4 | chunk
@@ -940,7 +940,8 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
         const int e = e0 + tid;
         if (e < seed_lanes) {  // whole 8-lane groups: the shuffles stay within active lanes
             const int pair = e >> 3, l = e & 7;
-            const int w = pair / ns, j = pair % ns;
+            static_assert(kInit == 8, "seed index = low 3 bits of the 8-lane group index");
+            const int w = pair & 7, j = pair >> 3;  // seed w, slot j
             const int tv = sm.seed_tok[w];
             const int g = tv >= 0 ? tv >> 7 : -1;
             const uint32_t slot = (uint32_t)(r.slot0 + j);
