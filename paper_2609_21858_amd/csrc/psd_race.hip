@@ -97,7 +97,7 @@ struct Shared {
     float red_b[2][kBlock / 64];
     int n_l4, n_l3, n_l2, n_cand;
     int best_key;
-    int tick[2];
+    int tick[4];
     int ph_first[kMaxPhases], ph_depth[kMaxPhases], ph_nd[kMaxPhases];  // work-order phases
     uint32_t epoch;
     float gst[2][128];  // group maxima of the streamed segment (by parity)
@@ -1563,6 +1563,27 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
     }
     __syncthreads();
     if (finisher) {
+        // Before its first row, a finishing workgroup streams segments from its queue
+        // until that row's segments are all taken: at the start the streaming is
+        // behind and the first rows' races wait for it.  (It never waits here.)
+        if (sm.tick[0] < a.n_rows) {
+            const int last = sm.tick[0] * a.L.nseg + a.L.nseg - 1;
+            for (int p = 0;; p ^= 1) {
+                if (tid == 0) sm.tick[2 + p] = take_item(a, q, nq);
+                __syncthreads();
+                const int item = sm.tick[2 + p];
+                if (item >= a.n_items) break;
+                Row rs;
+                int ss;
+                decode_item<BF16>(a, sm, item, rs, ss);
+                Unit<BF16, VEC> u[units_per_segment<BF16>()];
+                issue_segment<BF16, VEC>(a, rs, ss, u);
+                consume_segment<BF16, VEC>(a, rs, ss, sm, p, u);
+                __syncthreads();
+                publish_segment<BF16>(a, rs.row_id, ss, sm, p);
+                if (item >= last) break;
+            }
+        }
         for (int R = sm.tick[0]; R < a.n_rows;) {
             Row r;
             int seg;
