@@ -96,6 +96,11 @@ __device__ __forceinline__ double exp1_f64(uint32_t w) { return -log(uniform_f64
 
 __device__ __forceinline__ float ln_f32(float x) { return __builtin_amdgcn_logf(x) * 0.69314718055994531f; }
 
+// e / n for a node of n tokens, with the hardware reciprocal: one rounding more than
+// a division, and the float clocks only feed bounds that carry margins (the
+// decisions and detection's minimum are rebuilt in float64).
+__device__ __forceinline__ float div_n(float e, uint32_t n) { return e * __builtin_amdgcn_rcpf((float)n); }
+
 // Uniform position in [0, n): floor(n * W / 2^64), W = (w1 << 32) | w2, exact integer arithmetic.
 __device__ __forceinline__ uint32_t uniform_position(uint32_t w1, uint32_t w2, uint32_t n) {
     const uint64_t t = (uint64_t)w2 * n;
@@ -123,7 +128,7 @@ __device__ __forceinline__ void child_min_f32(float pm, uint32_t pp, int level, 
     }
     const Words w = philox(i, slot, (uint32_t)level, kDomainTree, k0, k1);
     const uint32_t n = ce - cs;
-    m = pm + exp1_f32(w.w0) / (float)n;
+    m = pm + div_n(exp1_f32(w.w0), n);
     p = cs + uniform_position(w.w1, w.w2, n);
 }
 
@@ -145,7 +150,7 @@ __device__ __forceinline__ void child_min_f64(double pm, uint32_t pp, int level,
 __device__ __forceinline__ void root_min_f32(uint32_t V, uint32_t slot, uint32_t k0, uint32_t k1, float& m,
                                              uint32_t& p) {
     const Words w = philox(0u, slot, 5u, kDomainTree, k0, k1);
-    m = exp1_f32(w.w0) / (float)V;
+    m = div_n(exp1_f32(w.w0), V);
     p = uniform_position(w.w1, w.w2, V);
 }
 
@@ -193,7 +198,7 @@ __device__ __forceinline__ float tree_clock_f32(uint32_t V, uint32_t slot, uint3
 #pragma unroll
     for (int l = 0; l < 4; ++l) wn[l] = philox(v >> shifts[l], slot, (uint32_t)(4 - l), kDomainTree, k0, k1);
     const Words wt = philox(v >> 3, slot, 8u + ((v >> 2) & 1u), kDomainTree, k0, k1);
-    float m = exp1_f32(wr.w0) / (float)V;
+    float m = div_n(exp1_f32(wr.w0), V);
     uint32_t p = uniform_position(wr.w1, wr.w2, V);
 #pragma unroll
     for (int l = 0; l < 4; ++l) {
@@ -201,7 +206,7 @@ __device__ __forceinline__ float tree_clock_f32(uint32_t V, uint32_t slot, uint3
         const uint32_t i = v >> sh, cs = node_start(sh, i), ce = node_end(sh, i, V);
         if (!(p >= cs && p < ce)) {
             const uint32_t n = ce - cs;
-            m = m + exp1_f32(wn[l].w0) / (float)n;
+            m = m + div_n(exp1_f32(wn[l].w0), n);
             p = cs + uniform_position(wn[l].w1, wn[l].w2, n);
         }
     }

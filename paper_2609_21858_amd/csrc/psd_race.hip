@@ -641,7 +641,7 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
             const uint32_t g = pn.id & 0xFFFFFu, chunk = g * 16u + (d & 15u);
             const uint32_t base = chunk * 8u, ce = node_end(kShift1, chunk, V);
             const Words w = philox(chunk, pn.id >> 20, 1u, kDomainTree, k0, k1);
-            sm.cj_m[j] = pn.m + exp1_f32(w.w0) / (float)(ce - base);
+            sm.cj_m[j] = pn.m + div_n(exp1_f32(w.w0), ce - base);
             sm.cj_p[j] = base + uniform_position(w.w1, w.w2, ce - base);
         }
     }
@@ -672,7 +672,7 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
                 } else {
                     const uint32_t ce = node_end(kShift1, chunk, V);
                     const Words wc = philox(chunk, ho.slot, 1u, kDomainTree, k0, k1);
-                    mc = pn.m + exp1_f32(wc.w0) / (float)(ce - chunk * 8u);
+                    mc = pn.m + div_n(exp1_f32(wc.w0), ce - chunk * 8u);
                     pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
                 }
             }
@@ -711,7 +711,7 @@ __device__ __forceinline__ void eval_overflow(const RaceArgs& a, const Row& r, S
                 const uint32_t ce = node_end(kShift1, chunk, V);
                 if (LAYOUT == 0 && !(pn.p >= chunk * 8u && pn.p < ce)) {
                     const Words wc = philox(chunk, slot, 1u, kDomainTree, k0, k1);
-                    mc = pn.m + exp1_f32(wc.w0) / (float)(ce - chunk * 8u);
+                    mc = pn.m + div_n(exp1_f32(wc.w0), ce - chunk * 8u);
                     pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
                 }
                 const Words w = LAYOUT == 0 ? philox(chunk, slot, 8u + (uint32_t)h, kDomainTree, k0, k1)
@@ -960,7 +960,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
                     const uint32_t node = l4 ? i4 : av >> sh;
                     const uint32_t cs = (l == 0 || l == 5) ? 0u : node << sh;
                     const uint32_t n = l == 0 ? V : l == 5 ? 1u : node_end(sh, node, V) - cs;
-                    val = exp1_f32(l == 5 ? pick_word(wd.w0, wd.w1, wd.w2, wd.w3, av & 3u) : wd.w0) / (float)n;
+                    val = div_n(exp1_f32(l == 5 ? pick_word(wd.w0, wd.w1, wd.w2, wd.w3, av & 3u) : wd.w0), n);
                     pos = cs + uniform_position(wd.w1, wd.w2, n);
                 }
                 const int base = tid & ~7;
@@ -1011,11 +1011,11 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
             const uint32_t slot = (uint32_t)(r.slot0 + j);
             const Words wr = philox(0u, slot, 5u, kDomainTree, k0, k1);
             const Words w4 = philox(i4, slot, 4u, kDomainTree, k0, k1);
-            const float rm = exp1_f32(wr.w0) / (float)V;
+            const float rm = div_n(exp1_f32(wr.w0), V);
             const uint32_t rp = uniform_position(wr.w1, wr.w2, V);
             const uint32_t cs = i4 << kShift4, n = node_end(kShift4, i4, V) - cs;
             const bool hold = rp >= cs && rp < cs + n;
-            level4_list(gm, ng)[j * n4 + (int)i4] = Node{(slot << 20) | i4, hold ? rm : rm + exp1_f32(w4.w0) / (float)n,
+            level4_list(gm, ng)[j * n4 + (int)i4] = Node{(slot << 20) | i4, hold ? rm : rm + div_n(exp1_f32(w4.w0), n),
                              hold ? rp : cs + uniform_position(w4.w1, w4.w2, n)};
         }
     }
