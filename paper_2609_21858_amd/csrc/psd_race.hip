@@ -1491,12 +1491,15 @@ __device__ __forceinline__ void decode_item(const RaceArgs& a, const Shared& sm,
     const bool s0 = lane + 1 < a.n_phase && sm.ph_first[lane + 1] <= item;
     const bool s1 = lane + 65 < a.n_phase && sm.ph_first[lane + 65] <= item;
     const int ph = (int)__builtin_popcountll(__ballot(s0)) + (int)__builtin_popcountll(__ballot(s1));
-    const int local = item - sm.ph_first[ph];
+    // (the item is uniform: the table entries are made scalar, so the divisions
+    // below run on the scalar unit rather than on every lane)
+    const int local = __builtin_amdgcn_readfirstlane(item) - __builtin_amdgcn_readfirstlane(sm.ph_first[ph]);
     const int rl = local / a.L.nseg;
     seg = local % a.L.nseg;
-    const int d = sm.ph_depth[ph];
+    const int d = __builtin_amdgcn_readfirstlane(sm.ph_depth[ph]);
+    const int nd = __builtin_amdgcn_readfirstlane(sm.ph_nd[ph]);
     r.s = d;
-    if (rl < sm.ph_nd[ph]) {
+    if (rl < nd) {
         r.kind = 0;
         r.b = rl / a.K;
         r.k = rl % a.K;
@@ -1508,7 +1511,7 @@ __device__ __forceinline__ void decode_item(const RaceArgs& a, const Shared& sm,
         r.invT = a.inv_T_draft;
         r.T = a.T_draft;
     } else {
-        const int rt = rl - sm.ph_nd[ph];
+        const int rt = rl - nd;
         r.kind = 1;
         size_t off;
         if (a.target_rows == 1) {
