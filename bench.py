@@ -152,7 +152,7 @@ def main():
         print(json.dumps(write_traffic(*args.traffic_from)))
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path has no "
+        print(f"bench.py: the race kernel runs on one GPU only (asked for --gpus {args.gpus}); it has no "
               f"inter-GPU collectives.  Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
