@@ -53,7 +53,6 @@ constexpr int kCandCap = 256;
 constexpr int kWorkCap = 2048;             // (level-3 node, group) items per prefilter round
 constexpr int kRolePeriod = 11;            // workgroup roles: of every kRolePeriod blocks,
 constexpr int kRoleFinish = 4;             // kRoleFinish finish rows and the others stream
-constexpr int kChunkJobCap = 256;          // chunk draws listed by one evaluation pass
 constexpr int kHalfCap = 256;              // 4-token halves listed by one evaluation pass
 constexpr int kPassGroups = 16 * kRowEntries;  // group entries of one evaluation pass
 constexpr int kBuckets = 32;               // bound buckets of the group list's evaluation order
@@ -69,8 +68,8 @@ struct Node {
 };
 
 // A 4-token half of a chunk that can still win: entry (local index), chunk, half
-// and token mask packed in desc; cref the chunk draw it needs (-1: the chunk holds
-// the group minimum); its logits.
+// and token mask packed in desc; cref 0 when the chunk needs its own minimum drawn
+// (-1: the chunk holds the group minimum); its logits.
 struct Half {
     uint32_t desc;  // entry << 9 | chunk << 5 | half << 4 | token mask (4 bits)
     int cref;
@@ -109,10 +108,7 @@ struct Shared {
     int key_min, key_max;   // (token, slot) range of the candidates near the best
     uint16_t work[kWorkCap];  // compacted work items (level-3 list index * 16 + group)
     int n_work;
-    uint32_t n_ev[2];                 // listed chunk draws (low 16 bits) and halves (high 16 bits), per pass parity
-    uint32_t cjob[kChunkJobCap];      // chunk draw: entry << 4 | chunk
-    float cj_m[kChunkJobCap];         // its minimum clock
-    uint32_t cj_p[kChunkJobCap];      // and position
+    uint32_t n_ev[2];                 // listed halves, per pass parity
     Half half[kHalfCap];
     // evaluation order of the group list (order_groups)
     float ord_wmin[kBlock / 64];          // per-wave smallest bound
@@ -510,10 +506,10 @@ __device__ __forceinline__ void list_near(Shared& sm, const RaceArgs& a, uint32_
 // issued together.  Only a few chunks of a surviving group hold a token that can
 // still win against the group minimum (chunk and token minima are never below
 // it), so the work is listed rather than done by each chunk's lane (a wave runs
-// every branch any of its lanes takes): the chunk draws and the 4-token halves
-// that need token words go to LDS lists, the chunk draws are made one per thread,
-// then the halves are scored one per thread.  Items beyond the lists' capacity are
-// done by their chunk's lane.
+// every branch any of its lanes takes): the 4-token halves that need token words
+// go to an LDS list and are scored one per thread, each drawing its chunk's
+// minimum too when the chunk does not hold the group's (two independent Philox
+// calls).  Halves beyond the list's capacity are done by their chunk's lane.
 // Raw logits of this lane's chunk of the entries of the pass starting at `first`
 // (list end `end`; nothing is loaded past it).  Words past V are never used.
 template <bool BF16, bool VEC>
@@ -563,7 +559,7 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
     const float thr0 = current_threshold(sm);
     uint32_t hm[kRowEntries][2];
     bool cj[kRowEntries];
-    int ncj = 0, nh = 0;
+    int nh = 0;
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
         const uint32_t g = nd[q].id & 0xFFFFFu;
@@ -588,27 +584,21 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
                 cj[q] = !(nd[q].p >= base && nd[q].p < ce);
             }
         }
-        ncj += (int)cj[q];
         nh += (int)(hm[q][0] != 0u) + (int)(hm[q][1] != 0u);
     }
-    // list positions: wave prefix sum of (draws | halves << 16), one atomic per wave
-    const uint32_t mine = (uint32_t)ncj | ((uint32_t)nh << 16);
+    // list positions: wave prefix sum of the halves, one atomic per wave
+    const uint32_t mine = (uint32_t)nh;
     const uint32_t incl = wave_incl_sum(mine);
     const uint32_t wtot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
     uint32_t wbase = 0u;
     if (lane == 0 && wtot != 0u) wbase = atomicAdd(&sm.n_ev[par], wtot);
     const uint32_t mb = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 0) + incl - mine;
-    int jc = (int)(mb & 0xFFFFu), jh = (int)(mb >> 16);
+    int jh = (int)mb;
     ovf = 0u;  // halves beyond the list (bit 8q + 4h + t: token t of half h of entry q)
 #pragma unroll
     for (int q = 0; q < kRowEntries; ++q) {
         const int le = row * kRowEntries + q;
-        int cref = -1;
-        if (cj[q]) {
-            cref = jc;
-            if (jc < kChunkJobCap) sm.cjob[jc] = ((uint32_t)le << 4) | (uint32_t)c;
-            ++jc;
-        }
+        const int cref = cj[q] ? 0 : -1;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             if (hm[q][h]) {
@@ -632,25 +622,11 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
     __syncthreads();
     // the other parity's counts were read in the previous pass: clear them for the next
     if (tid == 0) sm.n_ev[par ^ 1] = 0u;
-    // chunk draws, one per thread
-    {
-        const int nj = min((int)(sm.n_ev[par] & 0xFFFFu), kChunkJobCap);
-        for (int j = tid; j < nj; j += kBlock) {
-            const uint32_t d = sm.cjob[j];
-            const Node pn = sm.l2[first + (int)(d >> 4)];
-            const uint32_t g = pn.id & 0xFFFFFu, chunk = g * 16u + (d & 15u);
-            const uint32_t base = chunk * 8u, ce = node_end(kShift1, chunk, V);
-            const Words w = philox(chunk, pn.id >> 20, 1u, kDomainTree, k0, k1);
-            sm.cj_m[j] = pn.m + div_n(exp1_f32(w.w0), ce - base);
-            sm.cj_p[j] = base + uniform_position(w.w1, w.w2, ce - base);
-        }
-    }
-    __syncthreads();
     // halves, one per thread (at most one: kHalfCap == kBlock): scores, and the best
     // lowered to each half's smallest; the caller lists near-ties after a barrier
     static_assert(kHalfCap == kBlock, "one listed half per thread");
     {
-        const int nj = min((int)(sm.n_ev[par] >> 16), kHalfCap);
+        const int nj = min((int)sm.n_ev[par], kHalfCap);
         const float thr = current_threshold(sm);
 #pragma unroll
         for (int t = 0; t < 4; ++t) ho.sc[t] = INFINITY;
@@ -666,15 +642,12 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
             float mc = pn.m;
             uint32_t pc = pn.p;
             if (LAYOUT == 0 && hf.cref >= 0) {
-                if (hf.cref < kChunkJobCap) {
-                    mc = sm.cj_m[hf.cref];
-                    pc = sm.cj_p[hf.cref];
-                } else {
-                    const uint32_t ce = node_end(kShift1, chunk, V);
-                    const Words wc = philox(chunk, ho.slot, 1u, kDomainTree, k0, k1);
-                    mc = pn.m + div_n(exp1_f32(wc.w0), ce - chunk * 8u);
-                    pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
-                }
+                // the chunk's own minimum (its draw is independent of the half's words,
+                // so the two Philox calls overlap)
+                const uint32_t ce = node_end(kShift1, chunk, V);
+                const Words wc = philox(chunk, ho.slot, 1u, kDomainTree, k0, k1);
+                mc = pn.m + div_n(exp1_f32(wc.w0), ce - chunk * 8u);
+                pc = chunk * 8u + uniform_position(wc.w1, wc.w2, ce - chunk * 8u);
             }
             const Words w = LAYOUT == 0 ? philox(chunk, ho.slot, 8u + h, kDomainTree, k0, k1)
                                         : philox(ho.base4 >> 2, ho.slot, 0u, kDomainFlat, k0, k1);
@@ -826,7 +799,7 @@ __device__ __forceinline__ void flush_groups(const RaceArgs& a, const Row& r, Sh
         __syncthreads();
         // every half of the pass has lowered the best: list the near-ties
         if (ho.valid) list_near(sm, a, ho.base4, ho.slot, ho.sc, sm.half[threadIdx.x].x);
-        if ((sm.n_ev[par] >> 16) > (uint32_t)kHalfCap) eval_overflow<BF16, LAYOUT>(a, r, sm, first, ovf, k0, k1);
+        if (sm.n_ev[par] > (uint32_t)kHalfCap) eval_overflow<BF16, LAYOUT>(a, r, sm, first, ovf, k0, k1);
         __syncthreads();
         // (the next pass touches the candidates only after two more barriers)
         if (threadIdx.x == 0) compact_candidates(sm);
