@@ -194,6 +194,40 @@ def detect_sequence(key: int, m: int, K: int, V: int, tokens, n0: int, layout: i
     return S, int(cnt.value), per
 
 
+def gamma_tail_log_p(S: float, M: int) -> float:
+    """ln p_A with p_A = P(Gamma(M, 1) >= S_A) = Gamma(M, S_A) / Gamma(M) (App. "Gumbel
+    Watermark": under the null the M scored A_t are iid Exp(1), so S_A ~ Gamma(M, 1)).
+
+    M is a count, so the regularised upper incomplete gamma is the Poisson sum
+    Q(M, S) = sum_{k<M} e^{-S} S^k / k!  (the M-th arrival of a unit-rate Poisson
+    process comes after S iff fewer than M arrivals fall in [0, S]); it is summed here
+    in the log domain, ln k! as a running sum of ln i.  M = 0 (nothing scored) gives
+    p = 1; S <= 0 gives p = 1; NaN S or negative M give NaN.
+    """
+    M = int(M)
+    S = float(S)
+    if M < 0 or np.isnan(S):
+        return float("nan")
+    if M == 0 or S <= 0.0:
+        return 0.0
+    if np.isinf(S):
+        return float("-inf")
+    k = np.arange(M, dtype=np.float64)
+    log_fact = np.concatenate(([0.0], np.cumsum(np.log(np.arange(1, M, dtype=np.float64)))))
+    terms = -S + k * np.log(S) - log_fact
+    top = terms.max()
+    # a probability: rounding of a sum that is 1 to double precision stays at ln 1
+    return min(0.0, float(top + np.log(np.exp(terms - top).sum())))
+
+
+def anlppt(S: float, M: int) -> float:
+    """ANLPPT_A = -(1/M) ln p_A (App. "Gumbel Watermark"); NaN when M = 0."""
+    M = int(M)
+    if M <= 0:
+        return float("nan")
+    return -gamma_tail_log_p(S, M) / M
+
+
 # ---------------------------------------------------------------- block level
 
 def window_of(prefix, path, m: int):

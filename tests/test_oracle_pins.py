@@ -466,3 +466,63 @@ def test_detection_skips_out_of_range_tokens():
     S, M, per = oracle.detect_sequence(1, 2, 2, 10, toks, 1, oracle.LAYOUT_TREE)
     assert M == 3 and np.isnan(per[0]) and np.isnan(per[3]) and np.isnan(per[4])
     assert S == pytest.approx(np.nansum(per[1:]))
+
+
+# ---------------------------------------------------------------- Gamma-tail p-value
+
+# (M, S) grid: small and large counts, S from far below to far above the null mean M
+PVALUE_GRID = [(M, f * M + d) for M in (1, 2, 3, 10, 100, 512, 5000)
+               for f, d in ((0.0, 0.3), (0.5, 0.0), (1.0, -1.0), (1.0, 0.0), (1.0, 1.0), (1.5, 0.0),
+                            (3.0, 0.0), (20.0, 0.0)) if f * M + d > 0]
+
+
+def _tail_tol(S, M):
+    """Absolute accuracy of an fp64 log-domain Poisson sum: its terms -S + k ln S - ln k!
+    are formed to a few ulps of their magnitude, which cancels down to ln p."""
+    return 4e-15 * (S + M * abs(math.log(S)) + math.lgamma(M + 1)) + 1e-14
+
+
+@pytest.mark.parametrize("M,S", PVALUE_GRID)
+def test_gamma_tail_matches_arbitrary_precision(M, S):
+    """ln Gamma(M, S)/Gamma(M) against mpmath's regularised incomplete gamma at 40 digits
+    (a different method: hypergeometric series / asymptotics, not the Poisson sum)."""
+    mpmath = pytest.importorskip("mpmath")
+    mpmath.mp.dps = 40
+    ref = float(mpmath.log(mpmath.gammainc(M, S, mpmath.inf, regularized=True)))
+    got = oracle.gamma_tail_log_p(S, M)
+    assert got == pytest.approx(ref, rel=1e-11, abs=_tail_tol(S, M))
+
+
+@pytest.mark.parametrize("M,S", [(M, S) for M, S in PVALUE_GRID if S < 3 * M])
+def test_gamma_tail_matches_scipy(M, S):
+    """scipy's gammaincc and the chi-square tail P(chi2_{2M} >= 2S), where they do not underflow."""
+    tol = _tail_tol(S, M)
+    assert oracle.gamma_tail_log_p(S, M) == pytest.approx(math.log(special.gammaincc(M, S)), rel=1e-9, abs=tol)
+    assert oracle.gamma_tail_log_p(S, M) == pytest.approx(stats.chi2.logsf(2 * S, 2 * M), rel=1e-9, abs=tol)
+
+
+def test_gamma_tail_special_cases():
+    # M = 1: Gamma(1, 1) is Exp(1), p = e^{-S}
+    for S in (0.5, 3.0, 700.0, 1e5):
+        assert oracle.gamma_tail_log_p(S, 1) == pytest.approx(-S, rel=1e-15)
+    # M = 2: p = (1 + S) e^{-S}
+    for S in (0.5, 3.0, 700.0):
+        assert oracle.gamma_tail_log_p(S, 2) == pytest.approx(math.log1p(S) - S, rel=1e-14)
+    # nothing scored, or no evidence: p = 1; invalid inputs: NaN
+    assert oracle.gamma_tail_log_p(5.0, 0) == 0.0 and oracle.gamma_tail_log_p(0.0, 7) == 0.0
+    assert math.isnan(oracle.gamma_tail_log_p(float("nan"), 3)) and math.isnan(oracle.gamma_tail_log_p(1.0, -1))
+    assert math.isnan(oracle.anlppt(1.0, 0))
+    assert oracle.anlppt(600.0, 512) == pytest.approx(-oracle.gamma_tail_log_p(600.0, 512) / 512)
+    # the tail decreases in S (strictly once p is no longer 1 to double precision)
+    v = [oracle.gamma_tail_log_p(S, 50) for S in np.linspace(1, 400, 60)]
+    assert all(b <= a for a, b in zip(v, v[1:]))
+    assert all(b < a for a, b in zip(v, v[1:]) if a < -1e-12)
+
+
+def test_gamma_tail_null_is_uniform():
+    """Under the null (A_t iid Exp(1)) the p-value is Uniform(0, 1)."""
+    rng = np.random.default_rng(7)
+    M = 40
+    S = rng.exponential(size=(2000, M)).sum(axis=1)
+    p = np.exp([oracle.gamma_tail_log_p(s, M) for s in S])
+    assert stats.kstest(p, "uniform").pvalue > P_MIN
