@@ -125,13 +125,25 @@ def detect_leg(psd, torch, clocks_id, dev, launches=20):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / launches
+    # the Gamma-tail p-value and ANLPPT of the scores (one fp64 thread per sequence)
+    score, count, _ = psd.detect(p5, toks, n0)
+    for _ in range(3):
+        psd.detect_pvalue(score, count)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(launches):
+        psd.detect_pvalue(score, count)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_p = e0.elapsed_time(e1) / launches
     draws = 6 if clocks_id == psd.PSD_CLOCKS_TREE else 1
     # key folds, the K float clocks, and the exact rebuild of the smallest one
     calls = (w5.m + 1) + w5.K * draws + draws
     return {"workload": f"detection: {n_seq} sequences x {n_pos} scored tokens, K={w5.K}, V={w5.V}, m={w5.m}",
             "tokens_per_s": n_seq * n_pos / (ms / 1e3), "ms_per_launch": ms, "launches": launches,
             "philox_calls_per_token": calls,
-            "philox_calls_per_s": n_seq * n_pos * calls / (ms / 1e3)}
+            "philox_calls_per_s": n_seq * n_pos * calls / (ms / 1e3),
+            "pvalue_ms_per_launch": ms_p}
 
 
 def main():

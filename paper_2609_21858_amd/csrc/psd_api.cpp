@@ -246,6 +246,15 @@ psd_status psd_detect(const psd_params* params, int32_t n_seq, int32_t seq_len, 
     return PSD_OK;
 }
 
+psd_status psd_detect_pvalue(int32_t n_seq, const double* score, const int32_t* count, double* out_log_p,
+                             double* out_anlppt, hipStream_t stream) {
+    if (n_seq < 0) return fail(PSD_E_ARG, "n_seq < 0");
+    if (n_seq > 0 && (!score || !count || !out_log_p)) return fail(PSD_E_ARG, "score / count / out_log_p is NULL");
+    hipError_t e = psd::launch_pvalue(n_seq, score, count, out_log_p, out_anlppt, stream);
+    if (e != hipSuccess) return hip_fail(e, "p-value kernel launch");
+    return PSD_OK;
+}
+
 psd_status psd_philox(int32_t n, const uint32_t* ctr, const uint32_t* key, uint32_t* out, hipStream_t stream) {
     if (n < 0) return fail(PSD_E_ARG, "n < 0");
     if (n > 0 && (!ctr || !key || !out)) return fail(PSD_E_ARG, "NULL argument");

@@ -1,4 +1,5 @@
-// psd_detect.hip -- watermark detection score and parity exports (gfx950).
+// psd_detect.hip -- watermark detection score, its Gamma-tail p-value, and parity
+// exports (gfx950).
 //
 // Detection (eq. S_A; Alg. "Compute Aaronson score ..." in the appendix
 // "Algorithm Implementation"): each scored token w_t recomputes its context key
@@ -152,6 +153,71 @@ __global__ void clock_values_kernel(int layout, int V, int n, const uint32_t* ka
                          : flat_clock_f64((uint32_t)slot[i], (uint32_t)v, k0, k1);
 }
 
+// ln Q(M, S) for M >= 1 and finite S > 0, Q(M, S) = Gamma(M, S) / Gamma(M) the
+// regularised upper incomplete gamma function.  Below S = M + 1 from the power series
+// of the lower function P = 1 - Q, whose terms S^n / ((M+1)...(M+n)) fall
+// geometrically there; above it from Legendre's continued fraction of Q, evaluated
+// with Lentz's method (Abramowitz & Stegun 6.5.29 and 6.5.31).  Both need about
+// sqrt(M) steps where S is near M; `ok` is false if kTailSteps did not suffice.
+constexpr int kTailSteps = 1 << 22;
+
+__device__ double log_gamma_tail(double S, int M, bool& ok) {
+    const double a = (double)M, lx = log(S);
+    ok = true;
+    if (S < a + 1.0) {
+        double term = 1.0, sum = 1.0;
+        int n = 1;
+        for (; n <= kTailSteps; ++n) {
+            term *= S / (a + (double)n);
+            sum += term;
+            if (term < sum * 1e-17) break;
+        }
+        ok = n <= kTailSteps;
+        const double lnP = -S + a * lx - lgamma(a + 1.0) + log(sum);
+        return log1p(-exp(lnP));
+    }
+    const double tiny = 1e-300;
+    double b = S + 1.0 - a, c = 1.0 / tiny, d = 1.0 / b, h = d;
+    int i = 1;
+    for (; i <= kTailSteps; ++i) {
+        const double an = -(double)i * ((double)i - a);
+        b += 2.0;
+        d = an * d + b;
+        if (fabs(d) < tiny) d = tiny;
+        c = b + an / c;
+        if (fabs(c) < tiny) c = tiny;
+        d = 1.0 / d;
+        const double del = d * c;
+        h *= del;
+        if (fabs(del - 1.0) < 4e-16) break;
+    }
+    ok = i <= kTailSteps;
+    return -S + a * lx - lgamma(a) + log(h);
+}
+
+// One thread per sequence: ln p_A and ANLPPT_A of (S_A, M).
+__global__ void pvalue_kernel(int n, const double* score, const int32_t* count, double* out_log_p,
+                              double* out_anlppt) {
+    const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (i >= n) return;
+    const double S = score[i];
+    const int M = count[i];
+    double lp;
+    if (M < 0 || isnan(S)) {
+        lp = NAN;
+    } else if (M == 0 || S <= 0.0) {
+        lp = 0.0;  // nothing scored, or no evidence: p = 1
+    } else if (isinf(S)) {
+        lp = -INFINITY;
+    } else {
+        bool ok;
+        lp = log_gamma_tail(S, M, ok);
+        lp = ok ? fmin(lp, 0.0) : NAN;  // a probability: rounding above ln 1 is clamped
+    }
+    out_log_p[i] = lp;
+    if (out_anlppt) out_anlppt[i] = M > 0 ? -lp / (double)M : NAN;
+}
+
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
     for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
         p[i] = 0u;
@@ -167,6 +233,14 @@ hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream) {
         hipLaunchKernelGGL(detect_kernel<0>, dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
     else
         hipLaunchKernelGGL(detect_kernel<1>, dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_pvalue(int n, const double* score, const int32_t* count, double* out_log_p, double* out_anlppt,
+                         hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(pvalue_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, stream, n, score, count, out_log_p,
+                       out_anlppt);
     return hipGetLastError();
 }
 

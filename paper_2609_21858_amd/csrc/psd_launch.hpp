@@ -19,6 +19,8 @@ struct DetectArgs {
 
 hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
 hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream);
+hipError_t launch_pvalue(int n, const double* score, const int32_t* count, double* out_log_p,
+                         double* out_anlppt, hipStream_t stream);
 hipError_t launch_philox(int n, const uint32_t* ctr, const uint32_t* key, uint32_t* out, hipStream_t stream);
 hipError_t launch_context_keys(uint64_t key, int m, int n, const int64_t* t, const int32_t* windows,
                                uint32_t* out, hipStream_t stream);

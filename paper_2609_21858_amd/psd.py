@@ -68,6 +68,7 @@ def _load():
         "psd_draft": ([P, Bp, i32, i32, vp, vp, vp, vp], i32),
         "psd_verify": ([P, Bp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "psd_detect": ([P, i32, i32, vp, vp, vp, vp, vp, vp], i32),
+        "psd_detect_pvalue": ([i32, vp, vp, vp, vp, vp], i32),
         "psd_philox": ([i32, vp, vp, vp, vp], i32),
         "psd_context_keys": ([P, i32, vp, vp, vp, vp], i32),
         "psd_clock_values": ([P, i32, vp, vp, vp, vp, vp], i32),
@@ -81,8 +82,8 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("psd_abi_version", "psd_last_error", "psd_workspace_bytes", "psd_workspace_clear",
-           "psd_workspace_errors", "psd_draft", "psd_verify", "psd_detect", "psd_philox", "psd_context_keys",
-           "psd_clock_values")
+           "psd_workspace_errors", "psd_draft", "psd_verify", "psd_detect", "psd_detect_pvalue", "psd_philox",
+           "psd_context_keys", "psd_clock_values")
 
 
 def lib():
@@ -186,6 +187,15 @@ def detect(params: Params, tokens, n0, per_token: bool = False, stream=None):
     _check(_lib.psd_detect(ctypes.byref(params), n_seq, seq_len, _ptr(tokens), _ptr(n0), _ptr(score), _ptr(count),
                            _ptr(per), _stream(stream)))
     return score, count, per
+
+
+def detect_pvalue(score, count, stream=None):
+    """psd_detect_pvalue -> (ln p_A f64 [n_seq], ANLPPT_A f64 [n_seq]) of S_A ~ Gamma(M, 1) under the null."""
+    n = int(score.shape[0])
+    log_p = torch.empty((n,), dtype=torch.float64, device=score.device)
+    anl = torch.empty((n,), dtype=torch.float64, device=score.device)
+    _check(_lib.psd_detect_pvalue(n, _ptr(score), _ptr(count), _ptr(log_p), _ptr(anl), _stream(stream)))
+    return log_p, anl
 
 
 def philox(ctr, key, stream=None):

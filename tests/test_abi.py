@@ -96,6 +96,10 @@ def test_draft_and_detect_reject_bad_args(psd):
     assert L.psd_draft(ctypes.byref(p), ctypes.byref(blk), 0, 1, None, FAKE, None, None) == psd.PSD_E_ARG
     assert L.psd_detect(ctypes.byref(p), -1, 4, FAKE, FAKE, FAKE, FAKE, None, None) == psd.PSD_E_ARG
     assert L.psd_detect(ctypes.byref(p), 2, 4, None, FAKE, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_detect_pvalue(-1, FAKE, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_detect_pvalue(2, FAKE, None, FAKE, None, None) == psd.PSD_E_ARG
+    assert L.psd_detect_pvalue(2, FAKE, FAKE, None, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_detect_pvalue(0, None, None, None, None, None) == psd.PSD_OK
     assert L.psd_philox(-1, None, None, None, None) == psd.PSD_E_ARG
     assert L.psd_philox(3, None, FAKE, FAKE, None) == psd.PSD_E_ARG
     assert L.psd_context_keys(None, 1, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG

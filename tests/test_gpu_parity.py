@@ -302,8 +302,10 @@ def test_detect_parity_and_power(psd, layout):
     n0[1] = 200           # nothing scored
     p = psd.make_params(key, w.V, w.K, w.m, dtype=torch.bfloat16, clocks=layout)
     score, count, per = psd.detect(p, toks, n0, per_token=True)
+    log_p, anl = psd.detect_pvalue(score, count)
     _sync()
     score, count, per, tk = _np(score), _np(count), _np(per), _np(toks)
+    _check_pvalues(score, count, _np(log_p), _np(anl))
     for i in range(tk.shape[0]):
         S, M, ref_per = oracle.detect_sequence(key, w.m, w.K, w.V, tk[i], int(_np(n0)[i]), layout)
         assert count[i] == M
@@ -315,6 +317,51 @@ def test_detect_parity_and_power(psd, layout):
     z = (score - count) / np.sqrt(np.maximum(count, 1))
     assert np.all(z[[0, 2, 3, 4, 5]] > 3.0), z
     assert np.all(np.abs(z[6:]) < 4.5), z
+
+
+def _check_pvalues(score, count, log_p, anl):
+    """ln p_A and ANLPPT_A against the oracle's Poisson-sum evaluation of the same (S_A, M).
+    Tolerance: both sides form ln p from terms of size S + M |ln S| + ln M! to a few
+    ulps (their difference cancels down to ln p), so 4e-15 of that size, plus 1e-11
+    relative for the series / continued-fraction truncation at 1e-16."""
+    for S, M, lp, a in zip(score, count, log_p, anl):
+        ref = oracle.gamma_tail_log_p(float(S), int(M))
+        if math.isnan(ref):
+            assert math.isnan(lp), (S, M, lp)
+            continue
+        if M > 0 and S > 0 and math.isfinite(S):
+            tol = 4e-15 * (S + M * abs(math.log(S)) + math.lgamma(M + 1.0)) + 1e-14 + 1e-11 * abs(ref)
+            assert abs(lp - ref) <= tol, (S, M, lp, ref)
+        else:
+            assert lp == ref, (S, M, lp, ref)
+        if M > 0:
+            assert a == pytest.approx(-lp / M, rel=1e-15, abs=0.0) or (math.isinf(lp) and math.isinf(a))
+        else:
+            assert math.isnan(a)
+
+
+def test_detect_pvalue_grid(psd):
+    """psd_detect_pvalue over counts from 1 to 10^6 and scores from far below to far
+    above the null mean (series and continued-fraction sides, both sides of S = M + 1),
+    and the degenerate inputs: M = 0, S = 0, S = inf, NaN S, negative M.  301 sequences:
+    two blocks of 256 threads, the second ragged."""
+    cases = [(0, 5.0), (7, 0.0), (3, math.inf), (3, math.nan), (-1, 2.0), (1, 1e5), (2, 700.0)]
+    for M in (1, 2, 3, 10, 100, 512, 5000, 100000, 10**6):
+        for f, d in ((0.001, 0.0), (0.5, 0.0), (1.0, -1.0), (1.0, 0.0), (1.0, 1.0), (1.0, 1.5), (1.5, 0.0),
+                     (3.0, 0.0), (20.0, 0.0), (1000.0, 0.0)):
+            if f * M + d > 0:
+                cases.append((M, f * M + d))
+    rng = np.random.default_rng(11)
+    while len(cases) < 301:
+        M = int(rng.integers(1, 2000))
+        cases.append((M, float(rng.gamma(M) * rng.uniform(0.5, 2.0))))
+    count = torch.tensor([c[0] for c in cases], dtype=torch.int32, device=DEV)
+    score = torch.tensor([c[1] for c in cases], dtype=torch.float64, device=DEV)
+    log_p, anl = psd.detect_pvalue(score, count)
+    _sync()
+    _check_pvalues(_np(score), _np(count), _np(log_p), _np(anl))
+    # watermark-strength reading: S_A well above M gives a tiny p-value
+    assert _np(log_p)[5] == pytest.approx(-1e5, rel=1e-14)
 
 
 def _cpu_watermarked_text(key, w, n_seq, n_pos, seed, layout):

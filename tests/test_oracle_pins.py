@@ -526,3 +526,13 @@ def test_gamma_tail_null_is_uniform():
     S = rng.exponential(size=(2000, M)).sum(axis=1)
     p = np.exp([oracle.gamma_tail_log_p(s, M) for s in S])
     assert stats.kstest(p, "uniform").pvalue > P_MIN
+
+
+def test_gamma_tail_large_count():
+    """M = 10^6 near the null mean, where the Poisson sum has 10^6 terms."""
+    mpmath = pytest.importorskip("mpmath")
+    mpmath.mp.dps = 40
+    M = 10**6
+    for S in (M - 1.0, float(M), M + 1.0):
+        ref = float(mpmath.log(mpmath.gammainc(M, S, mpmath.inf, regularized=True)))
+        assert oracle.gamma_tail_log_p(S, M) == pytest.approx(ref, rel=1e-11, abs=_tail_tol(S, M))
