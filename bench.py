@@ -125,7 +125,7 @@ def detect_leg(psd, torch, clocks_id, dev, launches=20):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / launches
-    # the Gamma-tail p-value and ANLPPT of the scores (one fp64 thread per sequence)
+    # the Gamma-tail p-value and ANLPPT of the scores (one fp64 wavefront per sequence)
     score, count, _ = psd.detect(p5, toks, n0)
     for _ in range(3):
         psd.detect_pvalue(score, count)

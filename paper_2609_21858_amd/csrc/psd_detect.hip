@@ -153,53 +153,79 @@ __global__ void clock_values_kernel(int layout, int V, int n, const uint32_t* ka
                          : flat_clock_f64((uint32_t)slot[i], (uint32_t)v, k0, k1);
 }
 
-// ln Q(M, S) for M >= 1 and finite S > 0, Q(M, S) = Gamma(M, S) / Gamma(M) the
-// regularised upper incomplete gamma function.  Below S = M + 1 from the power series
-// of the lower function P = 1 - Q, whose terms S^n / ((M+1)...(M+n)) fall
-// geometrically there; above it from Legendre's continued fraction of Q, evaluated
-// with Lentz's method (Abramowitz & Stegun 6.5.29 and 6.5.31).  Both need about
-// sqrt(M) steps where S is near M; `ok` is false if kTailSteps did not suffice.
-constexpr int kTailSteps = 1 << 22;
+// ln Q(M, S), Q(M, S) = Gamma(M, S) / Gamma(M) the regularised upper incomplete gamma
+// function, by one wavefront per sequence.  Both forms used are sums of positive
+// terms that fall monotonically from their first term:
+//  * S < M + 1: the power series of the lower function P = 1 - Q,
+//    P = e^{-S} S^M / Gamma(M + 1) * sum_{n>=0} t_n, t_n = S^n / ((M+1)...(M+n))
+//    (ratio S / (M + n) < 1), and ln Q = ln(1 - P);
+//  * S >= M + 1: the Poisson form Q = sum_{k<M} e^{-S} S^k / k!, summed from
+//    k = M - 1 down (ratio k / S < 1).
+// A round gives each lane kTailChunk consecutive terms: the lane's first term in
+// closed form (lgamma), the rest by the ratio, then a wave log-sum-exp.  Rounds
+// stop once a round's last term is below e^-50 of the sum (the remaining tail is
+// below that term times 1 / (1 - ratio) <~ sqrt(M) of it), or the terms run out.
+constexpr int kTailChunk = 8;
+constexpr int kTailTerms = 1 << 24;  // bound on the terms summed per sequence
 
-__device__ double log_gamma_tail(double S, int M, bool& ok) {
-    const double a = (double)M, lx = log(S);
-    ok = true;
-    if (S < a + 1.0) {
-        double term = 1.0, sum = 1.0;
-        int n = 1;
-        for (; n <= kTailSteps; ++n) {
-            term *= S / (a + (double)n);
-            sum += term;
-            if (term < sum * 1e-17) break;
-        }
-        ok = n <= kTailSteps;
-        const double lnP = -S + a * lx - lgamma(a + 1.0) + log(sum);
-        return log1p(-exp(lnP));
-    }
-    const double tiny = 1e-300;
-    double b = S + 1.0 - a, c = 1.0 / tiny, d = 1.0 / b, h = d;
-    int i = 1;
-    for (; i <= kTailSteps; ++i) {
-        const double an = -(double)i * ((double)i - a);
-        b += 2.0;
-        d = an * d + b;
-        if (fabs(d) < tiny) d = tiny;
-        c = b + an / c;
-        if (fabs(c) < tiny) c = tiny;
-        d = 1.0 / d;
-        const double del = d * c;
-        h *= del;
-        if (fabs(del - 1.0) < 4e-16) break;
-    }
-    ok = i <= kTailSteps;
-    return -S + a * lx - lgamma(a) + log(h);
+__device__ __forceinline__ double wave_max_f64(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
+    return v;
 }
 
-// One thread per sequence: ln p_A and ANLPPT_A of (S_A, M).
-__global__ void pvalue_kernel(int n, const double* score, const int32_t* count, double* out_log_p,
-                              double* out_anlppt) {
-    const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
-    if (i >= n) return;
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// ln of sum_n t_n (series: t_0 = 1; Poisson: the terms themselves).  Called by a
+// whole wavefront with the same (S, M); `ok` is false if kTailTerms did not suffice.
+__device__ double log_tail_sum(double S, int M, bool series, bool& ok) {
+    const int lane = threadIdx.x & 63;
+    const double a = (double)M, lnS = log(S), lg1 = lgamma(a + 1.0);
+    double total = -INFINITY;
+    ok = false;
+    for (int base = 0; base < kTailTerms; base += 64 * kTailChunk) {
+        const int n0 = base + lane * kTailChunk;
+        const int k0 = M - 1 - n0;  // Poisson: the lane's first k
+        double lt;                  // ln of the lane's first term
+        if (series)
+            lt = (double)n0 * lnS - (lgamma(a + (double)n0 + 1.0) - lg1);
+        else
+            lt = k0 >= 0 ? -S + (double)k0 * lnS - lgamma((double)k0 + 1.0) : -INFINITY;
+        double t = 1.0, sum = 0.0;
+        int j = 0;
+        for (; j < kTailChunk; ++j) {
+            const int n = n0 + j;
+            if (!series && n > M - 1) break;
+            if (j > 0) t *= series ? S / (a + (double)n) : (double)(M - n) / S;
+            sum += t;
+        }
+        const double lc = sum > 0.0 ? lt + log(sum) : -INFINITY;
+        const double mx = wave_max_f64(lc);
+        if (mx == -INFINITY) {  // no term left (Poisson form exhausted)
+            ok = true;
+            break;
+        }
+        const double rs = mx + log(wave_sum_f64(lc == -INFINITY ? 0.0 : exp(lc - mx)));
+        total = total == -INFINITY ? rs : fmax(total, rs) + log1p(exp(-fabs(total - rs)));
+        // this round's last term (lane 63; -inf if its chunk ran past the last term)
+        const double last = __shfl(j == kTailChunk ? lt + log(t) : -INFINITY, 63);
+        if (last < total - 50.0) {
+            ok = true;
+            break;
+        }
+    }
+    return total;
+}
+
+// One wavefront per sequence (four per workgroup): ln p_A and ANLPPT_A of (S_A, M).
+__global__ __launch_bounds__(256) void pvalue_kernel(int n, const double* score, const int32_t* count,
+                                                      double* out_log_p, double* out_anlppt) {
+    const int i = (int)(blockIdx.x * 4u + (threadIdx.x >> 6));
+    if (i >= n) return;  // uniform per wavefront
     const double S = score[i];
     const int M = count[i];
     double lp;
@@ -210,12 +236,17 @@ __global__ void pvalue_kernel(int n, const double* score, const int32_t* count, 
     } else if (isinf(S)) {
         lp = -INFINITY;
     } else {
+        const double a = (double)M;
+        const bool series = S < a + 1.0;
         bool ok;
-        lp = log_gamma_tail(S, M, ok);
+        const double ls = log_tail_sum(S, M, series, ok);
+        lp = series ? log1p(-exp(-S + a * log(S) - lgamma(a + 1.0) + ls)) : ls;
         lp = ok ? fmin(lp, 0.0) : NAN;  // a probability: rounding above ln 1 is clamped
     }
-    out_log_p[i] = lp;
-    if (out_anlppt) out_anlppt[i] = M > 0 ? -lp / (double)M : NAN;
+    if ((threadIdx.x & 63) == 0) {
+        out_log_p[i] = lp;
+        if (out_anlppt) out_anlppt[i] = M > 0 ? -lp / (double)M : NAN;
+    }
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -239,7 +270,7 @@ hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream) {
 hipError_t launch_pvalue(int n, const double* score, const int32_t* count, double* out_log_p, double* out_anlppt,
                          hipStream_t stream) {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(pvalue_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, stream, n, score, count, out_log_p,
+    hipLaunchKernelGGL(pvalue_kernel, dim3(blocks_for(n, 4)), dim3(256), 0, stream, n, score, count, out_log_p,
                        out_anlppt);
     return hipGetLastError();
 }
