@@ -323,7 +323,7 @@ def _check_pvalues(score, count, log_p, anl):
     """ln p_A and ANLPPT_A against the oracle's Poisson-sum evaluation of the same (S_A, M).
     Tolerance: both sides form ln p from terms of size S + M |ln S| + ln M! to a few
     ulps (their difference cancels down to ln p), so 4e-15 of that size, plus 1e-11
-    relative for the series / continued-fraction truncation at 1e-16."""
+    relative for the truncation of the term sums."""
     for S, M, lp, a in zip(score, count, log_p, anl):
         ref = oracle.gamma_tail_log_p(float(S), int(M))
         if math.isnan(ref):
@@ -342,7 +342,7 @@ def _check_pvalues(score, count, log_p, anl):
 
 def test_detect_pvalue_grid(psd):
     """psd_detect_pvalue over counts from 1 to 10^6 and scores from far below to far
-    above the null mean (series and continued-fraction sides, both sides of S = M + 1),
+    above the null mean (the series and the Poisson form, both sides of S = M + 1),
     and the degenerate inputs: M = 0, S = 0, S = inf, NaN S, negative M.  301 sequences:
     two blocks of 256 threads, the second ragged."""
     cases = [(0, 5.0), (7, 0.0), (3, math.inf), (3, math.nan), (-1, 2.0), (1, 1e5), (2, 700.0)]
