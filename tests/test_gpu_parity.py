@@ -358,8 +358,13 @@ def test_detect_pvalue_grid(psd):
     count = torch.tensor([c[0] for c in cases], dtype=torch.int32, device=DEV)
     score = torch.tensor([c[1] for c in cases], dtype=torch.float64, device=DEV)
     log_p, anl = psd.detect_pvalue(score, count)
+    # out_anlppt is nullable: the same ln p_A without it
+    log_p2 = torch.empty_like(log_p)
+    assert psd.lib().psd_detect_pvalue(len(cases), score.data_ptr(), count.data_ptr(), log_p2.data_ptr(), None,
+                                       None) == psd.PSD_OK
     _sync()
     _check_pvalues(_np(score), _np(count), _np(log_p), _np(anl))
+    assert np.array_equal(_np(log_p), _np(log_p2), equal_nan=True)
     # watermark-strength reading: S_A well above M gives a tiny p-value
     assert _np(log_p)[5] == pytest.approx(-1e5, rel=1e-14)
 
