@@ -385,6 +385,76 @@ def test_walk_exhaustive_small_grid():
             assert oracle.walk(drafts, chain, K, gamma) == _literal_tree_walk(drafts, list(chain), K, gamma)
 
 
+def _literal_context_walk(drafts, chains, K, gamma):
+    """Formal multi-draft walk with one target sample y(c) per context c: with
+    per-path target rows, context c at depth s takes the row (and so the target
+    winner) of the lowest-index path whose draft prefix is c; D(c) = distinct
+    drafts at c; follow y(c*) while it is in D(c*); bonus after gamma acceptances."""
+    D, Y = {}, {}
+    for k in range(K):
+        for s in range(gamma + 1):
+            c = tuple(drafts[k][:s])
+            Y.setdefault(c, chains[k][s])  # paths in increasing index: the lowest one defines y(c)
+            if s < gamma:
+                D.setdefault(c, set()).add(drafts[k][s])
+    cstar, out = (), []
+    for s in range(gamma):
+        y = Y[cstar]
+        out.append(y)
+        if y < 0 or y not in D.get(cstar, set()):
+            return out
+        cstar = cstar + (y,)
+    out.append(Y[cstar])
+    return out
+
+
+def test_walk_per_path_rows_exhaustive():
+    """Per-path target rows (target_rows = K): every draft grid and every per-path
+    chain grid for V=3 (chains also -1 = empty row), K=2, gamma=2, against the
+    literal per-context walk; and a random sample at K=3, gamma=3."""
+    import itertools
+    K, gamma = 2, 2
+    for d in itertools.product(range(3), repeat=K * gamma):
+        drafts = [list(d[k * gamma:(k + 1) * gamma]) for k in range(K)]
+        for c in itertools.product(range(-1, 3), repeat=K * (gamma + 1)):
+            chains = [list(c[k * (gamma + 1):(k + 1) * (gamma + 1)]) for k in range(K)]
+            assert oracle.walk(drafts, chains, K, gamma, per_path=True) == \
+                _literal_context_walk(drafts, chains, K, gamma), (drafts, chains)
+    rng = np.random.default_rng(12)
+    K, gamma = 3, 3
+    for _ in range(20000):
+        drafts = rng.integers(0, 2, (K, gamma)).tolist()
+        chains = rng.integers(-1, 2, (K, gamma + 1)).tolist()
+        assert oracle.walk(drafts, chains, K, gamma, per_path=True) == _literal_context_walk(drafts, chains, K, gamma)
+
+
+def test_per_path_rows_reduce_to_shared_chain():
+    """When every path's target row at a depth is the shared row of that depth, the
+    lowest active path's context at depth s is prefix || y_{<s}, so per-path
+    verification emits exactly the shared-chain tokens."""
+    w, blk = _tiny_block(3, K=3, gamma=3, V=30, B=3, m=2)
+    tl = blk["target_logits"]
+    per = np.repeat(tl[:, None], w.K, axis=1)
+    args = dict(key=w.key, K=w.K, gamma=w.gamma, m=w.m, T_target=1.0, T_draft=1.0, prefix=blk["prefix_tokens"],
+                start_pos=blk["start_pos"], draft_logits=blk["draft_logits"])
+    for layout in LAYOUTS:
+        a = oracle.verify_block(target_logits=tl, layout=layout, **args)
+        b = oracle.verify_block(target_logits=per, target_rows=w.K, layout=layout, **args)
+        for s in range(w.B):
+            assert a["out_tokens"][s] == b["out_tokens"][s] and a["out_len"][s] == b["out_len"][s]
+            tau = a["out_len"][s]
+            # the lowest active path's chain is the shared chain on the emitted prefix
+            k0 = 0
+            for d in range(tau):
+                assert b["target_tokens"][s][k0][d] == a["target_tokens"][s][d]
+                if d < w.gamma:
+                    act = [k for k in range(w.K) if list(b["draft_tokens"][s][k][:d + 1]) ==
+                           list(a["target_tokens"][s][:d + 1])]
+                    if not act:
+                        break
+                    k0 = min(act)
+
+
 def test_speculative_output_equals_plain_keyed_chain():
     """Several speculative blocks over a position-indexed toy LM emit exactly the
     tokens of plain keyed autoregressive decoding (Thm. "exactness of
