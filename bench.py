@@ -26,6 +26,7 @@ PEAK_HBM_GBPS = 8000.0   # MI355X HBM3E, vendor figure
 MALL_BYTES = 256 << 20
 KERNEL_SOURCES = ["psd_race.hip", "psd_device.hpp", "psd_layout.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "race_kernel_c3_traffic.json")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "race_kernel_c3_counters.json")
 
 
 def kernel_digest() -> str:
@@ -46,6 +47,42 @@ def measured_traffic(clocks: str):
     if rec.get("kernel_digest") != kernel_digest() or rec.get("clocks") != clocks:
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def measured_counters(clocks: str):
+    """VALU-busy and related derived counters of the race kernel from the committed PMC
+    summary, if it was taken on this kernel."""
+    try:
+        with open(COUNTERS_FILE) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_digest") != kernel_digest() or rec.get("clocks") != clocks:
+        return None
+    return rec.get("per_dispatch")
+
+
+def write_counters(csv_path: str, out: str = COUNTERS_FILE) -> dict:
+    """Average per race-kernel dispatch of each counter in a rocprofv3 --pmc run."""
+    import csv
+    import collections
+
+    vals = collections.defaultdict(list)
+    clocks = "tree"
+    for r in csv.DictReader(open(csv_path)):
+        if "race_kernel<" not in r["Kernel_Name"]:
+            continue
+        clocks = "flat" if r["Kernel_Name"].split("race_kernel<")[1].split(">")[0].endswith("1") else "tree"
+        vals[r["Counter_Name"]].append(float(r["Counter_Value"]))
+    if not vals:
+        raise SystemExit(f"{csv_path}: no race_kernel dispatches")
+    rec = {"kernel": "race_kernel", "workload": "V=128256 K=4 gamma=4 B=64 bf16", "clocks": clocks,
+           "kernel_digest": kernel_digest(), "dispatches": max(len(v) for v in vals.values()),
+           "per_dispatch": {k: sum(v) / len(v) for k, v in sorted(vals.items())}}
+    with open(out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    return rec
 
 
 def write_traffic(fetch_csv: str, write_csv: str, out: str = TRAFFIC_FILE) -> dict:
@@ -85,33 +122,45 @@ def write_traffic(fetch_csv: str, write_csv: str, out: str = TRAFFIC_FILE) -> di
     return rec
 
 
-def cpu_baseline(blk, w, clocks_id, n_seq):
+def cpu_baseline(blk, w, clocks_id, n_seq, n_seq_single):
+    """The oracle as it stands, on the host cores of this machine: all n_seq sequences of
+    the block split over one thread per available core (the C oracle runs without the
+    interpreter lock), and the first n_seq_single sequences on one thread."""
     import oracle
     import workloads
 
-    seqs = list(range(n_seq))
     tl = workloads.as_f32_numpy(blk["target_logits"][:n_seq])
     dl = workloads.as_f32_numpy(blk["draft_logits"][:n_seq])
     pre = blk["prefix_tokens"][:n_seq].cpu().numpy()
     sp = blk["start_pos"][:n_seq].cpu().numpy()
+    kw = dict(key=w.key, K=w.K, gamma=w.gamma, m=w.m, T_target=w.T_target, T_draft=w.T_draft, prefix=pre,
+              start_pos=sp, target_logits=tl, draft_logits=dl, layout=clocks_id)
+    affinity = len(os.sched_getaffinity(0))
+    workers = max(1, min(affinity, int(os.environ.get("OMP_NUM_THREADS", affinity))))
     t0 = time.perf_counter()
-    oracle.verify_block(key=w.key, K=w.K, gamma=w.gamma, m=w.m, T_target=w.T_target, T_draft=w.T_draft,
-                        prefix=pre, start_pos=sp, target_logits=tl, draft_logits=dl, layout=clocks_id, seqs=seqs)
+    oracle.verify_block(seqs=list(range(n_seq_single)), **kw)
+    dt1 = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.verify_block_parallel(workers, seqs=list(range(n_seq)), **kw)
     dt = time.perf_counter() - t0
-    return {"value": n_seq * w.gamma / dt, "unit": "positions/s", "cores": 1, "kind": "oracle",
-            "sample": f"sequences 0..{n_seq - 1} of the B=64 block (all {n_seq * (w.K * w.gamma + w.gamma + 1)} "
-                      f"rows of them): exhaustive double-precision clocks, two-pass LSE, race and walk, "
-                      f"single-threaded C; {dt:.1f} s"}
+    rows = w.K * w.gamma + w.gamma + 1
+    return {"value": n_seq * w.gamma / dt, "unit": "positions/s", "cores": workers, "kind": "oracle",
+            "affinity_cpus": affinity, "single_thread_value": n_seq_single * w.gamma / dt1,
+            "sample": f"all-cores leg: sequences 0..{n_seq - 1} of the B={w.B} block ({n_seq * rows} rows), one "
+                      f"thread per sequence on {workers} threads, {dt:.1f} s; single-thread leg: sequences "
+                      f"0..{n_seq_single - 1} ({n_seq_single * rows} rows), {dt1:.1f} s; exhaustive "
+                      f"double-precision clocks, two-pass LSE, race and walk in plain C"}
 
 
-def detect_leg(psd, torch, clocks_id, dev, launches=20):
+def detect_leg(psd, torch, clocks_id, dev, launches=20, replicate=1):
     """Detection throughput on the stress workload's text shape: 256 sequences of
-    512 scored tokens after a 4-token prompt, K=16, V=256000.  The per-token work
-    (context key plus K keyed clocks) does not depend on the token values, so
-    uniform tokens stand in for generated text."""
+    512 scored tokens after a 4-token prompt, K=16, V=256000 (replicate: that many
+    times more sequences).  The per-token work (context key plus K keyed clocks)
+    does not depend on the token values, so uniform tokens stand in for generated
+    text (parity on generated text is a test)."""
     import workloads
     w5 = workloads.WORKLOADS[5]
-    n_seq, n_pos = w5.B, 512
+    n_seq, n_pos = w5.B * replicate, 512
     toks = workloads.uniform_tokens(n_seq, w5.m + n_pos, w5.V, seed=5).to(dev)
     n0 = torch.full((n_seq,), w5.m, dtype=torch.int32, device=dev)
     p5 = psd.make_params(w5.key, w5.V, w5.K, w5.m, dtype=w5.torch_dtype, clocks=clocks_id)
@@ -154,14 +203,21 @@ def main():
     ap.add_argument("--clocks", choices=["tree", "flat"], default="tree")
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seqs", type=int, default=40)
+    ap.add_argument("--cpu-seqs", type=int, default=64, help="sequences of the all-cores oracle leg")
+    ap.add_argument("--cpu-seqs-single", type=int, default=16, help="sequences of the single-thread leg")
+    ap.add_argument("--no-detect-100x", action="store_true")
     ap.add_argument("--pmc-copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for FETCH/WRITE_SIZE scaling)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM traffic record from two rocprofv3 --pmc counter files and exit")
+    ap.add_argument("--counters-from", metavar="CSV",
+                    help="write the race kernel's derived-counter record from a rocprofv3 --pmc file and exit")
     args = ap.parse_args()
     if args.traffic_from:
         print(json.dumps(write_traffic(*args.traffic_from)))
+        return
+    if args.counters_from:
+        print(json.dumps(write_counters(args.counters_from)))
         return
     if args.gpus != 1:
         print(f"bench.py: the race kernel runs on one GPU only (asked for --gpus {args.gpus}); it has no "
@@ -241,15 +297,20 @@ def main():
                    "T": w.T_target, "clocks": args.clocks, "fused_drafting": True, "input_sets": n_sets},
         "hbm_gbps": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic(args.clocks),
+                     "frac": achieved / PEAK_HBM_GBPS,
+                     "traffic": measured_traffic(args.clocks) if args.config == 3 else None,
+                     "counters": measured_counters(args.clocks) if args.config == 3 else None,
                      "algorithmic_bytes_per_launch": bytes_per_launch, "avg_launch_ms": avg_launch_ms,
                      "min_launch_ms": min(per), "max_launch_ms": max(per)},
         "mean_tau": mean_tau,
         "wall_s": wall,
     }
     res["detect"] = detect_leg(psd, torch, clocks_id, dev)
+    if not args.no_detect_100x:
+        res["detect_100x"] = detect_leg(psd, torch, clocks_id, dev, launches=5, replicate=100)
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(sets[0], w, clocks_id, args.cpu_seqs)
+        res["cpu_baseline"] = cpu_baseline(sets[0], w, clocks_id, min(args.cpu_seqs, w.B),
+                                           min(args.cpu_seqs_single, w.B))
     print(json.dumps(res), flush=True)
 
 

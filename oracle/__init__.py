@@ -347,3 +347,26 @@ def verify_block(*, key, K, gamma, m, T_target, T_draft, prefix, start_pos, targ
         out["out_tokens"][b] = emitted
         out["out_len"][b] = len(emitted)
     return out
+
+
+def verify_block_parallel(workers: int, seqs=None, **kw) -> dict:
+    """verify_block over `seqs` (default all), one sequence per task on `workers`
+    threads.  The C oracle runs with the interpreter lock released (ctypes), so the
+    sequences are checked in parallel; results and comparison counts are merged."""
+    import concurrent.futures
+
+    _lib()  # load (or build) the library once, before the threads start
+    B = kw["target_logits"].shape[0]
+    seqs = list(range(B)) if seqs is None else list(seqs)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=max(1, workers)) as ex:
+        parts = list(ex.map(lambda b: verify_block(seqs=[b], **kw), seqs))
+    out = {"draft_tokens": {}, "target_tokens": {}, "out_tokens": {}, "out_len": {}, "draft_lse": {},
+           "target_lse": {}, "stats": {"exact": 0, "near_tie": 0, "mismatch": 0, "mismatches": []}}
+    for part in parts:
+        for k in ("draft_tokens", "target_tokens", "out_tokens", "out_len", "draft_lse", "target_lse"):
+            out[k].update(part[k])
+        for k in ("exact", "near_tie", "mismatch"):
+            out["stats"][k] += part["stats"][k]
+        out["stats"]["mismatches"] += part["stats"]["mismatches"]
+    return out
+

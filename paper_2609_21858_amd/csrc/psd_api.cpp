@@ -7,6 +7,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "../../include/psd.h"
 #include "psd_launch.hpp"
 #include "psd_layout.hpp"
@@ -14,6 +16,10 @@
 namespace {
 
 thread_local char g_err[512] = "";
+
+// Polls of a bounded cross-workgroup wait before it gives up (test hook, psd_set_spin_limit).
+constexpr uint32_t kDefaultSpinLimit = 1u << 22;
+std::atomic<uint32_t> g_spin_limit{kDefaultSpinLimit};
 
 psd_status fail(psd_status st, const char* fmt, ...) {
     va_list ap;
@@ -80,6 +86,8 @@ psd::RaceArgs base_args(const psd_params* p, const psd_block* b) {
     a.T_draft = p->temp_draft;
     a.inv_T_target = 1.0f / p->temp_target;
     a.inv_T_draft = 1.0f / p->temp_draft;
+    a.status = b->status;
+    a.spin_limit = g_spin_limit.load(std::memory_order_relaxed);
     return a;
 }
 
@@ -143,6 +151,8 @@ extern "C" {
 int32_t psd_abi_version(void) { return PSD_ABI_VERSION; }
 
 const char* psd_last_error(void) { return g_err; }
+
+void psd_set_spin_limit(uint32_t polls) { g_spin_limit.store(polls ? polls : kDefaultSpinLimit, std::memory_order_relaxed); }
 
 size_t psd_workspace_bytes(const psd_params* params, int32_t batch, int32_t gamma) {
     if (!params || params->vocab < 1 || params->vocab > PSD_MAX_VOCAB || params->num_drafts < 1 ||

@@ -18,7 +18,9 @@ inline int seg_tokens(int dtype_bf16) { return dtype_bf16 ? kSegTokensBf16 : kSe
 // Control words at the start of every workspace (fixed positions for every call shape).
 constexpr int kCtrlWords = 2048;   // 8 KiB
 constexpr int kCtrlExited = 1;     // workgroups that left the kernel
-constexpr int kCtrlErrors = 2;     // sticky error bits
+constexpr int kCtrlErrors = 2;     // sticky error bits (since the last clear)
+constexpr int kCtrlCallErrors = 3; // error bits of the running call; moved to kCtrlErrors and the
+                                   // caller's status word by the call's last workgroup
 constexpr int kCtrlEpoch = 5;      // epoch of the last completed call
 constexpr int kMaxQueues = 8;      // work queues (one per XCD) of each kind, counters 256 B apart
 // counter of segment queue q (q < kMaxQueues) or of row queue q - kMaxQueues
@@ -110,6 +112,8 @@ struct RaceArgs {
     int phase_nt[kMaxPhases];
     // the row of each sequence that walks its block: (kind, depth, path); kind -1: none
     int walk_kind, walk_s, walk_k;
+    uint32_t* status;     // nullable: this call's error bits, written by its last workgroup
+    uint32_t spin_limit;  // polls of a bounded wait before it gives up (psd_set_spin_limit)
 };
 
 }  // namespace psd

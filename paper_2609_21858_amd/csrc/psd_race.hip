@@ -58,7 +58,6 @@ constexpr int kPassGroups = 16 * kRowEntries;  // group entries of one evaluatio
 constexpr int kBuckets = 32;               // bound buckets of the group list's evaluation order
 constexpr float kMargin = 1e-3f;           // float32 pruning / candidate margin (score units)
 constexpr float kCutSlack = 1e-3f;         // slack of the per-token logit cut (score units)
-constexpr uint32_t kSpinLimit = 1u << 22;  // bounded waits for other workgroups' slots
 constexpr uint32_t kErrSpin = 1u, kErrCand = 2u;
 
 struct Node {
@@ -106,6 +105,7 @@ struct Shared {
     uint32_t next0, next1;  // partial context key of the path's next depth
     int win[32];            // context tokens (own window, next depth's window)
     int key_min, key_max;   // (token, slot) range of the candidates near the best
+    uint32_t err_local;       // error bits this workgroup recorded (it then publishes them with a release)
     uint16_t work[kWorkCap];  // compacted work items (level-3 list index * 16 + group)
     int n_work;
     uint32_t n_ev[2];                 // listed halves, per pass parity
@@ -132,11 +132,26 @@ struct Row {
     int slot0, nslots;
     float invT;
     float T;
+    float shift;  // the row's maximum logit: fp32 scores and bounds use (l - shift) / T
 };
+
+// Scaled logit (l - shift) / T of the race's fp32 scores and bounds.  Near the
+// top of the row the subtraction is exact (Sterbenz), so the scaled value of every
+// token that can still win is O(tens) and rounds to a few 1e-6 score units
+// whatever the magnitude of l / T; tokens far below the maximum have scores far
+// above the threshold, where rounding cannot change a decision.
+__device__ __forceinline__ float scaled(const Row& r, float x) { return (x - r.shift) * r.invT; }
 
 __device__ __forceinline__ uint32_t* ctrl_of(const RaceArgs& a) { return (uint32_t*)(a.ws + a.L.ctrl); }
 
-__device__ __forceinline__ void set_error(const RaceArgs& a, uint32_t bit) { atomicOr(ctrl_of(a) + kCtrlErrors, bit); }
+// Errors of the running call; its last workgroup hands them to the sticky word and
+// to the caller's status word.  The workgroup also notes them in LDS, so that its
+// exit publishes them with a release (see the end of race_kernel).
+__device__ __forceinline__ void set_error(const RaceArgs& a, uint32_t bit) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __hip_atomic_fetch_or(ctrl_of(a) + kCtrlCallErrors, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    atomicOr(&reinterpret_cast<Shared*>(smem_raw)->err_local, bit);
+}
 
 // Cross-workgroup slots are touched only with relaxed device-scope atomics, which
 // are coherent across the XCDs without L2-wide write-back / invalidate; each slot
@@ -155,7 +170,7 @@ __device__ __forceinline__ T ld_dev(const T* p) {
 __device__ __forceinline__ uint64_t wait_slot(const RaceArgs& a, const uint64_t* p, uint32_t epoch) {
     uint64_t v = ld_dev(p);
     for (uint32_t i = 0; (uint32_t)(v >> 32) != epoch; ++i) {
-        if (i >= kSpinLimit) {
+        if (i >= a.spin_limit) {
             set_error(a, kErrSpin);
             break;
         }
@@ -475,11 +490,11 @@ __device__ __forceinline__ void half_scores(const Row& r, uint32_t base4, uint32
         const uint32_t v = base4 + (uint32_t)t;
         if constexpr (LAYOUT == 0) {
             if (v == pc)
-                sc[t] = lnmc - x[t] * r.invT;
-            else if (lnmc - x[t] * r.invT <= thr)
-                sc[t] = ln_f32(mc + exp1_f32(ws[t])) - x[t] * r.invT;
+                sc[t] = lnmc - scaled(r, x[t]);
+            else if (lnmc - scaled(r, x[t]) <= thr)
+                sc[t] = ln_f32(mc + exp1_f32(ws[t])) - scaled(r, x[t]);
         } else {
-            sc[t] = ln_f32(exp1_f32(ws[t])) - x[t] * r.invT;
+            sc[t] = ln_f32(exp1_f32(ws[t])) - scaled(r, x[t]);
         }
     }
 }
@@ -567,14 +582,15 @@ __device__ __forceinline__ void eval_groups(const RaceArgs& a, const Row& r, Sha
         const float lnm = LAYOUT == 0 ? ln_f32(nd[q].m) : kLnClockFloor;
         hm[q][0] = hm[q][1] = 0u;
         cj[q] = false;
-        if (act[q] && lnm - gm[g] * r.invT <= thr0) {
-            // a token can reach thr0 only if lnm - x / T <= thr0, i.e. x >= (lnm -
-            // thr0) T; the cut is lowered by kCutSlack, far more than the rounding of
-            // either form, so the listed tokens include every such token
+        if (act[q] && lnm - scaled(r, gm[g]) <= thr0) {
+            // a token can reach thr0 only if lnm - (x - shift) / T <= thr0, i.e.
+            // x - shift >= (lnm - thr0) T; the cut is lowered by kCutSlack, far more
+            // than the rounding of either form, so the listed tokens include every
+            // such token (compared in the shifted frame: no rounding of shift + cut)
             const float xc = (lnm - thr0 - kCutSlack) * r.T;
             uint32_t m8 = 0u;
 #pragma unroll
-            for (int i = 0; i < 8; ++i) m8 |= (uint32_t)(x[q][i] >= xc) << i;
+            for (int i = 0; i < 8; ++i) m8 |= (uint32_t)(x[q][i] - r.shift >= xc) << i;
             const int nv = (int)V - (int)base;  // tokens of this chunk inside the row
             if (nv < 8) m8 &= nv > 0 ? (1u << nv) - 1u : 0u;
             hm[q][0] = m8 & 15u;
@@ -723,7 +739,7 @@ __device__ __forceinline__ int order_groups(const Row& r, Shared& sm, const floa
         const int e = tid + i * kBlock;
         nd[i] = e < n ? sm.l2[e] : Node{0u, 0.f, 0u};
         const float lnm = LAYOUT == 0 ? ln_f32(nd[i].m) : kLnClockFloor;
-        b[i] = e < n ? lnm - gm[nd[i].id & 0xFFFFFu] * r.invT : INFINITY;
+        b[i] = e < n ? lnm - scaled(r, gm[nd[i].id & 0xFFFFFu]) : INFINITY;
         if (b[i] <= thr) wmin = fminf(wmin, b[i]);
     }
 #pragma unroll
@@ -834,7 +850,7 @@ __device__ __forceinline__ void flush_l3(const RaceArgs& a, const Row& r, Shared
             for (int e = base + tid; e < min(n, base + kWorkCap); e += kBlock) {
                 const Node pa = sm.l3[e >> 4];
                 const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
-                if ((int)g < ng && ln_f32(pa.m) - gm[g] * r.invT <= thr) sm.work[atomicAdd(&sm.n_work, 1)] = e;
+                if ((int)g < ng && ln_f32(pa.m) - scaled(r, gm[g]) <= thr) sm.work[atomicAdd(&sm.n_work, 1)] = e;
             }
             __syncthreads();
             nw = sm.n_work;
@@ -853,12 +869,12 @@ __device__ __forceinline__ void flush_l3(const RaceArgs& a, const Row& r, Shared
             const Node pa = sm.l3[e >> 4];
             const uint32_t g = (pa.id & 0xFFFFFu) * 16u + (uint32_t)(e & 15);
             const float thr = current_threshold(sm);
-            if (ln_f32(pa.m) - gm[g] * r.invT <= thr) {
+            if (ln_f32(pa.m) - scaled(r, gm[g]) <= thr) {
                 const uint32_t slot = pa.id >> 20;
                 float m;
                 uint32_t p;
                 child_min_f32(pa.m, pa.p, 2, g, g << kShift2, node_end(kShift2, g, V), slot, k0, k1, m, p);
-                if (ln_f32(m) - gm[g] * r.invT <= thr) push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | g, m, p);
+                if (ln_f32(m) - scaled(r, gm[g]) <= thr) push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | g, m, p);
             }
         }
         wb += kBlock;
@@ -960,7 +976,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
                 const float v5 = __shfl(val, base + 5);
                 const float E = (av == p) ? m : m + v5;
                 if (l == 0 && g >= 0) {
-                    const float sc = ln_f32(E) - xa * r.invT;
+                    const float sc = ln_f32(E) - scaled(r, xa);
                     if (sc < INFINITY) {
                         atomicMin(&sm.best_key, ordered_key(sc));
                         push_candidate(sm, a, (int)av, (int)slot, sc, xa);
@@ -969,7 +985,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
             } else {
                 if (l == 0 && g >= 0) {
                     const Words wd = philox(av >> 2, slot, 0u, kDomainFlat, k0, k1);
-                    const float sc = ln_f32(exp1_f32(word_at(wd, av & 3u))) - xa * r.invT;
+                    const float sc = ln_f32(exp1_f32(word_at(wd, av & 3u))) - scaled(r, xa);
                     if (sc < INFINITY) {
                         atomicMin(&sm.best_key, ordered_key(sc));
                         push_candidate(sm, a, (int)av, (int)slot, sc, xa);
@@ -1011,12 +1027,12 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
                 const uint32_t i3 = i4 * 16u + (uint32_t)(e & 15);
                 const float thr = current_threshold(sm);
                 const float lnp = ln_f32(pa.m);
-                if ((int)i3 < n3 && lnp - sm.m4[i4] * r.invT <= thr && lnp - sm.m3[i3] * r.invT <= thr) {
+                if ((int)i3 < n3 && lnp - scaled(r, sm.m4[i4]) <= thr && lnp - scaled(r, sm.m3[i3]) <= thr) {
                     const uint32_t slot = pa.id >> 20;
                     float m;
                     uint32_t p;
                     child_min_f32(pa.m, pa.p, 3, i3, i3 << kShift3, node_end(kShift3, i3, V), slot, k0, k1, m, p);
-                    if (ln_f32(m) - sm.m3[i3] * r.invT <= thr) push_node(sm.l3, &sm.n_l3, kL3Cap, (slot << 20) | i3, m, p);
+                    if (ln_f32(m) - scaled(r, sm.m3[i3]) <= thr) push_node(sm.l3, &sm.n_l3, kL3Cap, (slot << 20) | i3, m, p);
                 }
             }
             __syncthreads();
@@ -1034,7 +1050,7 @@ __device__ __forceinline__ void race(const RaceArgs& a, const Row& r, Shared& sm
             if (e < tot) {
                 const int g = e / ns;
                 const uint32_t slot = (uint32_t)(r.slot0 + e % ns);
-                if (kLnClockFloor - gm[g] * r.invT <= current_threshold(sm))
+                if (kLnClockFloor - scaled(r, gm[g]) <= current_threshold(sm))
                     push_node(sm.l2, &sm.n_l2, kL2Cap, (slot << 20) | (uint32_t)g, 0.f, 0u);
             }
             __syncthreads();
@@ -1285,8 +1301,8 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
                         gm[e] = __uint_as_float(w);
                     else if (e < ng + n3)
                         sm.m3[e - ng] = __uint_as_float(w);
-                    else if (e < ng + n3 + a.L.nseg)
-                        sm.stop[e - ng - n3] = (int)w;
+                    else if (e < ng + n3 + a.L.nseg)  // a group index of this row, or -1 (a value
+                        sm.stop[e - ng - n3] = (int)w >= -1 && (int)w < ng ? (int)w : -1;  // left stale by a timed-out wait is dropped)
                     else
                         sm.part[e - ng - n3 - a.L.nseg] = __uint_as_float(w);
                 }
@@ -1430,7 +1446,9 @@ __device__ __forceinline__ void finish_row(const RaceArgs& a, const Row& r, Shar
         }
         __syncthreads();
     } else {
-        race<BF16, VEC, LAYOUT>(a, r, sm, gm, k0, k1);
+        Row rs = r;
+        rs.shift = sm.rowmax;
+        race<BF16, VEC, LAYOUT>(a, rs, sm, gm, k0, k1);
     }
     if (tid == 0) {
         const int y = sm.win_token;
@@ -1478,6 +1496,7 @@ __device__ __forceinline__ void decode_item(const RaceArgs& a, const Shared& sm,
     const int d = __builtin_amdgcn_readfirstlane(sm.ph_depth[ph]);
     const int nd = __builtin_amdgcn_readfirstlane(sm.ph_nd[ph]);
     r.s = d;
+    r.shift = 0.f;
     if (rl < nd) {
         r.kind = 0;
         r.b = rl / a.K;
@@ -1534,6 +1553,7 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
     const int nq = gridDim.x >= 8u * kRolePeriod ? kMaxQueues : 1;
     const int q = (int)(blockIdx.x % (unsigned)nq);
     if (tid == 0) {
+        sm.err_local = 0u;
         const uint32_t last = ld_dev(ctrl + kCtrlEpoch);
         sm.epoch = last == 0xFFFFFFFFu ? 1u : last + 1u;  // 1 .. 2^32-1
         sm.tick[0] = finisher ? take_row(a, q, nq) : take_item(a, q, nq);
@@ -1598,10 +1618,21 @@ __global__ __launch_bounds__(kBlock, 4) void race_kernel(RaceArgs a) {
             publish_segment<BF16>(a, pub_row, pub_seg, sm, parity);
         }
     }
-    // The last workgroup to leave resets the queues and advances the epoch.
+    // The last workgroup to leave resets the queues, hands over the call's error bits
+    // and advances the epoch.  A workgroup that recorded errors fences (release)
+    // before it counts its exit, and the last one fences (acquire) after it: its
+    // read of the call's bits then sees every error of the call.  The exit count
+    // itself stays relaxed (a release per workgroup writes back its L2: ~19 us).
+    __syncthreads();
     if (tid == 0) {
+        if (sm.err_local) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         const uint32_t old = __hip_atomic_fetch_add(ctrl + kCtrlExited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (old == gridDim.x - 1) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            const uint32_t bits =
+                __hip_atomic_exchange(ctrl + kCtrlCallErrors, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (bits) __hip_atomic_fetch_or(ctrl + kCtrlErrors, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (a.status) *a.status = bits;
             for (int i = 0; i < 2 * kMaxQueues; ++i) st_dev(ctrl + ctrl_queue(i), 0u);
             st_dev(ctrl + kCtrlExited, 0u);
             st_dev(ctrl + kCtrlEpoch, sm.epoch);

@@ -49,6 +49,7 @@ class Block(ctypes.Structure):
         ("start_pos", ctypes.c_void_p),
         ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t),
+        ("status", ctypes.c_void_p),
     ]
 
 
@@ -72,6 +73,7 @@ def _load():
         "psd_philox": ([i32, vp, vp, vp, vp], i32),
         "psd_context_keys": ([P, i32, vp, vp, vp, vp], i32),
         "psd_clock_values": ([P, i32, vp, vp, vp, vp, vp], i32),
+        "psd_set_spin_limit": ([ctypes.c_uint32], None),
     }
     for name, (args, res) in sigs.items():
         f = getattr(lib, name)
@@ -83,7 +85,7 @@ def _load():
 _lib = _load()
 EXPORTS = ("psd_abi_version", "psd_last_error", "psd_workspace_bytes", "psd_workspace_clear",
            "psd_workspace_errors", "psd_draft", "psd_verify", "psd_detect", "psd_detect_pvalue", "psd_philox",
-           "psd_context_keys", "psd_clock_values")
+           "psd_context_keys", "psd_clock_values", "psd_set_spin_limit")
 
 
 def lib():
@@ -135,23 +137,31 @@ def workspace_errors(ws: torch.Tensor, stream=None) -> int:
     return int(out.value)
 
 
-def _block(batch, gamma, prefix, start_pos, ws):
+def _block(batch, gamma, prefix, start_pos, ws, status=None):
     return Block(batch, gamma, prefix.data_ptr() if prefix is not None and prefix.numel() else None,
-                 start_pos.data_ptr(), ws.data_ptr(), ws.numel())
+                 start_pos.data_ptr(), ws.data_ptr(), ws.numel(), None if status is None else status.data_ptr())
+
+
+def set_spin_limit(polls: int = 0):
+    """Test hook: polls of a bounded wait before it gives up (0 = default)."""
+    _lib.psd_set_spin_limit(polls)
 
 
 def draft(params: Params, ws, prefix_tokens, start_pos, gamma: int, s_begin: int, draft_logits, draft_tokens,
-          draft_lse=None, stream=None):
-    """psd_draft: draft depths [s_begin, s_begin + draft_logits.shape[2])."""
+          draft_lse=None, stream=None, status=None):
+    """psd_draft: draft depths [s_begin, s_begin + draft_logits.shape[2]).  status: optional
+    int32 [1] device tensor receiving the call's error bits."""
     B = int(start_pos.shape[0])
-    blk = _block(B, gamma, prefix_tokens, start_pos, ws)
+    blk = _block(B, gamma, prefix_tokens, start_pos, ws, status)
     _check(_lib.psd_draft(ctypes.byref(params), ctypes.byref(blk), s_begin, int(draft_logits.shape[2]),
                           _ptr(draft_logits), _ptr(draft_tokens), _ptr(draft_lse), _stream(stream)))
 
 
 def verify(params: Params, ws, prefix_tokens, start_pos, target_logits, draft_logits=None, draft_tokens=None,
-           target_rows: int = 1, want_lse: bool = False, want_targets: bool = False, out=None, stream=None):
-    """psd_verify; allocates the outputs it is not given.  Returns a dict of tensors."""
+           target_rows: int = 1, want_lse: bool = False, want_targets: bool = False, out=None, stream=None,
+           status=None):
+    """psd_verify; allocates the outputs it is not given.  Returns a dict of tensors.  status:
+    optional int32 [1] device tensor receiving the call's error bits."""
     B = int(start_pos.shape[0])
     K = params.num_drafts
     gamma = int(target_logits.shape[-2]) - 1
@@ -169,7 +179,7 @@ def verify(params: Params, ws, prefix_tokens, start_pos, target_logits, draft_lo
             o.setdefault("draft_lse", torch.empty((B, K, gamma), dtype=torch.float32, device=dev))
     if want_targets:
         o.setdefault("target_tokens", torch.empty(tshape, dtype=torch.int32, device=dev))
-    blk = _block(B, gamma, prefix_tokens, start_pos, ws)
+    blk = _block(B, gamma, prefix_tokens, start_pos, ws, status)
     _check(_lib.psd_verify(ctypes.byref(params), ctypes.byref(blk), target_rows, _ptr(target_logits),
                            _ptr(draft_logits), _ptr(draft_tokens), _ptr(o["out_tokens"]), _ptr(o["out_len"]),
                            _ptr(o.get("target_lse")), _ptr(o.get("draft_lse")), _ptr(o.get("target_tokens")),

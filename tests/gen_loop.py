@@ -22,27 +22,36 @@ def block_starts(length: torch.Tensor, m: int, n_pos: int) -> torch.Tensor:
 
 
 def generate(verify, rows, prompt, n_pos, gamma, K, noise, gen, dtype):
-    """rows: float32 [B][table_positions][V]; prompt: int32 [B][m].
+    """rows: float32 [B][table_positions][V], or a function of the absolute positions
+    idx int64 [B][gamma+1] (each in [0, table_positions)) returning the target rows
+    float32 [B][gamma+1][V] of those positions; prompt: int32 [B][m].
     verify(prefix, start_pos, target_logits, draft_logits) -> (out_tokens, out_len) host arrays."""
-    B, P, V = rows.shape
-    m = prompt.shape[1]
-    assert P == table_positions(m, n_pos, gamma), (P, m, n_pos, gamma)
-    dev = rows.device
-    length = torch.full((B,), m, dtype=torch.int64, device=dev)
-    buf = torch.full((B, m + n_pos + gamma + 1), -1, dtype=torch.int32, device=dev)
-    buf[:, :m] = prompt
+    B, m = prompt.shape
+    P = table_positions(m, n_pos, gamma)
+    if callable(rows):
+        rows_at = rows
+    else:
+        assert rows.shape[0] == B and rows.shape[1] == P, (rows.shape, P)
+        V = rows.shape[2]
+        rows_at = lambda idx: torch.gather(rows, 1, idx.view(B, gamma + 1, 1).expand(B, gamma + 1, V))
+    dev = prompt.device
+    # the text and the lengths live on the host: every index is checked there
+    length = np.full(B, m, dtype=np.int64)
+    buf = np.full((B, m + n_pos + gamma + 1), -1, dtype=np.int32)
+    buf[:, :m] = prompt.cpu().numpy()
     blocks = 0
     while int(length.min()) < m + n_pos:
-        start = block_starts(length, m, n_pos)
-        idx = start.view(B, 1) + torch.arange(gamma + 1, device=dev).view(1, gamma + 1)
+        start = np.minimum(length, m + n_pos - 1)  # block_starts: finished sequences clamped
+        idx = start[:, None] + np.arange(gamma + 1)[None, :]
         assert int(idx.min()) >= 0 and int(idx.max()) < P, (int(idx.max()), P)
-        pidx = start.view(B, 1) - m + torch.arange(m, device=dev).view(1, m)
+        pidx = start[:, None] - m + np.arange(m)[None, :]
         assert m == 0 or (int(pidx.min()) >= 0 and int(pidx.max()) < buf.shape[1])
-        tl = torch.gather(rows, 1, idx.view(B, gamma + 1, 1).expand(B, gamma + 1, V)).to(dtype).contiguous()
+        tl = rows_at(torch.from_numpy(idx).to(dev)).to(dtype).contiguous()
+        V = tl.shape[-1]
         dl = (tl[:, None, :gamma].float() + noise * torch.randn((B, K, gamma, V), generator=gen, device=dev)).to(dtype)
-        prefix = torch.gather(buf, 1, pidx).contiguous() if m else buf[:, :0].contiguous()
-        out_tokens, out_len = verify(prefix, start, tl, dl)
-        out_len = np.asarray(out_len)
+        prefix = torch.from_numpy(np.ascontiguousarray(np.take_along_axis(buf, pidx, 1) if m else buf[:, :0])).to(dev)
+        out_tokens, out_len = verify(prefix, torch.from_numpy(start).to(dev), tl, dl)
+        out_tokens, out_len = np.asarray(out_tokens), np.asarray(out_len)
         assert np.all((out_len >= 1) & (out_len <= gamma + 1)), out_len
         for b in range(B):
             L0 = int(length[b])
@@ -50,7 +59,7 @@ def generate(verify, rows, prompt, n_pos, gamma, K, noise, gen, dtype):
                 continue
             n = int(out_len[b])
             assert L0 + n <= buf.shape[1]
-            buf[b, L0:L0 + n] = torch.as_tensor(np.asarray(out_tokens[b][:n]), dtype=torch.int32, device=dev)
+            buf[b, L0:L0 + n] = out_tokens[b][:n]
             length[b] = L0 + n
         blocks += 1
-    return buf[:, :m + n_pos].contiguous(), blocks
+    return torch.from_numpy(np.ascontiguousarray(buf[:, :m + n_pos])).to(dev), blocks

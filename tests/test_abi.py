@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol(psd):
     for n in names:
         assert hasattr(psd.lib(), n), n
         assert n in psd.EXPORTS
-    assert psd.lib().psd_abi_version() == 1
+    assert psd.lib().psd_abi_version() == 2
 
 
 def test_workspace_bytes(psd):
