@@ -202,12 +202,15 @@ psd_status psd_draft(const psd_params* params, const psd_block* block, int32_t s
     return run_race(params, a, stream);
 }
 
-psd_status psd_verify(const psd_params* params, const psd_block* block, int32_t target_rows,
-                      const void* target_logits, const void* draft_logits, int32_t* draft_tokens,
-                      int32_t* out_tokens, int32_t* out_len, float* target_lse, float* draft_lse,
-                      int32_t* target_tokens, hipStream_t stream) {
-    psd_status st = check_params(params);
-    if (st != PSD_OK) return st;
+}  // extern "C"
+
+namespace {
+
+psd_status verify_impl(const psd_params* params, const psd_block* block, int32_t target_rows,
+                       const void* target_logits, const void* draft_logits, int32_t* draft_tokens,
+                       int32_t* out_tokens, int32_t* out_len, float* target_lse, float* draft_lse,
+                       int32_t* target_tokens, hipStream_t stream) {
+    psd_status st;
     if ((st = check_block(params, block)) != PSD_OK) return st;
     if (target_rows != 1 && target_rows != params->num_drafts)
         return fail(PSD_E_ARG, "target_rows must be 1 or num_drafts (%d), got %d", params->num_drafts, target_rows);
@@ -229,6 +232,46 @@ psd_status psd_verify(const psd_params* params, const psd_block* block, int32_t 
     a.target_rows = target_rows;
     build_depths(a, block->gamma + 1);
     return run_race(params, a, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+psd_status psd_verify(const psd_params* params, const psd_block* block, int32_t target_rows,
+                      const void* target_logits, const void* draft_logits, int32_t* draft_tokens,
+                      int32_t* out_tokens, int32_t* out_len, float* target_lse, float* draft_lse,
+                      int32_t* target_tokens, hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    return verify_impl(params, block, target_rows, target_logits, draft_logits, draft_tokens, out_tokens, out_len,
+                       target_lse, draft_lse, target_tokens, stream);
+}
+
+psd_status psd_verify_static(const psd_params* params, const psd_block* block, int32_t target_rows,
+                             const void* target_logits, const void* draft_logits, int32_t* draft_tokens,
+                             int32_t* out_tokens, int32_t* out_len, float* target_lse, float* draft_lse,
+                             int32_t* target_tokens, hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    if (!block) return fail(PSD_E_ARG, "block is NULL");
+    if (block->workspace || block->workspace_bytes)
+        return fail(PSD_E_ARG, "psd_verify_static uses the library's fixed scratch: pass workspace NULL, 0 bytes");
+    if (block->batch < 1 || block->gamma < 1 || block->gamma > PSD_MAX_GAMMA)
+        return fail(PSD_E_ARG, "batch %d / gamma %d out of range", block->batch, block->gamma);
+    const size_t need =
+        psd::ws_layout(block->batch, params->num_drafts, block->gamma, params->vocab, params->dtype == PSD_BF16).total;
+    if (need > psd::kStaticScratchBytes)
+        return fail(PSD_E_WORKSPACE, "the shape needs %zu bytes of scratch; the fixed scratch holds %zu "
+                    "(use psd_verify with a workspace)", need, psd::kStaticScratchBytes);
+    void* ws = nullptr;
+    hipError_t e = psd::static_scratch(&ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "fixed scratch");
+    psd_block b = *block;
+    b.workspace = ws;
+    b.workspace_bytes = psd::kStaticScratchBytes;
+    return verify_impl(params, &b, target_rows, target_logits, draft_logits, draft_tokens, out_tokens, out_len,
+                       target_lse, draft_lse, target_tokens, stream);
 }
 
 psd_status psd_detect(const psd_params* params, int32_t n_seq, int32_t seq_len, const int32_t* tokens,

@@ -28,4 +28,10 @@ hipError_t launch_clock_values(int layout, int V, int n, const uint32_t* kappa, 
                                const int32_t* token, double* out, hipStream_t stream);
 hipError_t launch_fill_zero(uint32_t* p, size_t n_words, hipStream_t stream);
 
+// Bytes of the fixed per-device scratch behind psd_verify_static.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+// Device address of this device's fixed scratch (looked up and zeroed on the first
+// call on the device, the clear enqueued on `stream`).
+hipError_t static_scratch(void** out, hipStream_t stream);
+
 }  // namespace psd

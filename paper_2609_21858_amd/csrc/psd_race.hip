@@ -37,6 +37,8 @@
 
 #include <math.h>
 
+#include <mutex>
+
 #include "psd_device.hpp"
 #include "psd_launch.hpp"
 #include "psd_layout.hpp"
@@ -1677,5 +1679,38 @@ hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipSt
     return layout == 0 ? launch_one<false, false, 0>(a, stream) : launch_one<false, false, 1>(a, stream);
 }
 
+
+// ---------------------------------------------------------------- static scratch
+
+// The allocation-free entry point's workspace: one fixed array per device, held
+// until the process ends.  In host code `scratch` is only a handle for the
+// runtime; its device address is looked up once per device (with that device
+// current) and kept, and only that address is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_scratch(void** out, hipStream_t stream) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+        if (!p || ((uintptr_t)p & 255u) != 0) return hipErrorInvalidSymbol;
+        // zero once (control words, epoch, queues) with a fill kernel ahead of the
+        // first call on the caller's stream
+        if ((e = launch_fill_zero((uint32_t*)p, kStaticScratchBytes / 4, stream)) != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 }  // namespace psd

@@ -68,6 +68,7 @@ def _load():
         "psd_workspace_errors": ([vp, vp, ctypes.POINTER(ctypes.c_uint32)], i32),
         "psd_draft": ([P, Bp, i32, i32, vp, vp, vp, vp], i32),
         "psd_verify": ([P, Bp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
+        "psd_verify_static": ([P, Bp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "psd_detect": ([P, i32, i32, vp, vp, vp, vp, vp, vp], i32),
         "psd_detect_pvalue": ([i32, vp, vp, vp, vp, vp], i32),
         "psd_philox": ([i32, vp, vp, vp, vp], i32),
@@ -84,7 +85,7 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("psd_abi_version", "psd_last_error", "psd_workspace_bytes", "psd_workspace_clear",
-           "psd_workspace_errors", "psd_draft", "psd_verify", "psd_detect", "psd_detect_pvalue", "psd_philox",
+           "psd_workspace_errors", "psd_draft", "psd_verify", "psd_verify_static", "psd_detect", "psd_detect_pvalue", "psd_philox",
            "psd_context_keys", "psd_clock_values", "psd_set_spin_limit")
 
 
@@ -184,6 +185,32 @@ def verify(params: Params, ws, prefix_tokens, start_pos, target_logits, draft_lo
                            _ptr(draft_logits), _ptr(draft_tokens), _ptr(o["out_tokens"]), _ptr(o["out_len"]),
                            _ptr(o.get("target_lse")), _ptr(o.get("draft_lse")), _ptr(o.get("target_tokens")),
                            _stream(stream)))
+    return o
+
+
+def verify_static(params: Params, prefix_tokens, start_pos, target_logits, draft_logits=None, draft_tokens=None,
+                  target_rows: int = 1, out=None, status=None, stream=None):
+    """psd_verify_static (the library's fixed scratch, no workspace).  Outputs come
+    from `out` (a dict of tensors: draft_tokens, out_tokens, out_len and optionally
+    target_lse, draft_lse, target_tokens) or are allocated here by torch when missing."""
+    B = int(start_pos.shape[0])
+    K = params.num_drafts
+    gamma = int(target_logits.shape[-2]) - 1
+    dev = target_logits.device
+    o = {} if out is None else dict(out)
+    if draft_tokens is None:
+        draft_tokens = o.get("draft_tokens")
+    if draft_tokens is None:
+        draft_tokens = torch.empty((B, K, gamma), dtype=torch.int32, device=dev)
+    o["draft_tokens"] = draft_tokens
+    o.setdefault("out_tokens", torch.empty((B, gamma + 1), dtype=torch.int32, device=dev))
+    o.setdefault("out_len", torch.empty((B,), dtype=torch.int32, device=dev))
+    blk = Block(B, gamma, prefix_tokens.data_ptr() if prefix_tokens is not None and prefix_tokens.numel() else None,
+                start_pos.data_ptr(), None, 0, None if status is None else status.data_ptr())
+    _check(_lib.psd_verify_static(ctypes.byref(params), ctypes.byref(blk), target_rows, _ptr(target_logits),
+                                  _ptr(draft_logits), _ptr(draft_tokens), _ptr(o["out_tokens"]), _ptr(o["out_len"]),
+                                  _ptr(o.get("target_lse")), _ptr(o.get("draft_lse")), _ptr(o.get("target_tokens")),
+                                  _stream(stream)))
     return o
 
 

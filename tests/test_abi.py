@@ -105,3 +105,23 @@ def test_draft_and_detect_reject_bad_args(psd):
     assert L.psd_context_keys(None, 1, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
     assert L.psd_clock_values(ctypes.byref(p), 2, None, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
     assert L.psd_workspace_clear(None, 16, None) == psd.PSD_E_ARG
+
+
+def test_verify_static_rejects_before_launch(psd):
+    """The allocation-free entry point takes no workspace and refuses shapes beyond its
+    fixed 32 MiB scratch, before touching the device."""
+    L = psd.lib()
+    p = psd.make_params(1, 128256, 4, 4, 0.7, 0.7)
+    ok_blk = psd.Block(64, 4, FAKE, FAKE, None, 0, None)
+    with_ws = psd.Block(64, 4, FAKE, FAKE, FAKE, 1 << 20, None)
+    args = (1, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None)
+    assert L.psd_verify_static(ctypes.byref(p), ctypes.byref(with_ws), *args) == psd.PSD_E_ARG
+    assert L.psd_verify_static(ctypes.byref(p), None, *args) == psd.PSD_E_ARG
+    big = psd.make_params(1, 256000, 16, 4)
+    big_blk = psd.Block(256, 4, FAKE, FAKE, None, 0, None)
+    assert psd.workspace_bytes(big, 256, 4) > 32 << 20
+    assert L.psd_verify_static(ctypes.byref(big), ctypes.byref(big_blk), *args) == psd.PSD_E_WORKSPACE
+    assert b"fixed scratch" in L.psd_last_error()
+    assert psd.workspace_bytes(p, 64, 4) <= 32 << 20  # the headline block fits
+    bad = psd.make_params(1, 0, 4, 4)
+    assert L.psd_verify_static(ctypes.byref(bad), ctypes.byref(ok_blk), *args) == psd.PSD_E_ARG
