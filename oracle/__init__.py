@@ -84,6 +84,9 @@ def _lib():
     lib.oracle_race.argtypes = [f32p, ctypes.c_int, ctypes.c_float, u32p, ctypes.c_int, ctypes.c_int,
                                 ctypes.c_int, ctypes.POINTER(_RaceResult)]
     lib.oracle_race.restype = ctypes.c_int
+    lib.oracle_mpfr.argtypes = [f32p, ctypes.c_int, ctypes.c_float, u32p, ctypes.c_int, ctypes.c_int,
+                                ctypes.c_int, i32p, i32p, f64p]
+    lib.oracle_mpfr.restype = ctypes.c_int
     lib.oracle_detect_term.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.c_int, i32p, ctypes.c_int64]
     lib.oracle_detect_term.restype = ctypes.c_double
@@ -169,6 +172,25 @@ def race(logits, T: float, kappa, slot0: int, nslots: int, layout: int = LAYOUT_
     if rc != 0:
         raise ValueError("oracle_race failed (%d)" % rc)
     return {"token": res.token, "slot": res.slot, "best": res.best, "second": res.second, "lse": res.lse}
+
+
+def mpfr(logits, T: float, kappa, nu: int, layout: int = LAYOUT_TREE, n_out: int = None) -> dict:
+    """The nu MPFR samples of one row under the keyed source kappa (exhaustive, double):
+    the labels of the smallest ln G_{v,j} - l_v/T over (v, j < nu), G_{v,j} the sum of
+    the clocks of slots 0..j of token v.  Returns the first n_out (default nu + 4)
+    sorted (token, arrival, score) entries; the samples are the first nu tokens."""
+    n_out = nu + 4 if n_out is None else n_out
+    x, xp = _f32(logits)
+    k, kp = _u32(kappa)
+    tok, tp = _i32(np.zeros(n_out, np.int32))
+    arr, ap = _i32(np.zeros(n_out, np.int32))
+    sc = np.zeros(n_out, np.float64)
+    rc = _lib().oracle_mpfr(xp, x.size, T, kp, nu, layout, n_out, tp, ap,
+                            sc.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise ValueError("oracle_mpfr failed (%d)" % rc)
+    return {"tokens": [int(t) for t in tok], "arrivals": [int(a) for a in arr], "scores": [float(v) for v in sc],
+            "samples": [int(t) for t in tok[:nu]]}
 
 
 def token_score(logits, T: float, kappa, slot0: int, nslots: int, v: int, layout: int = LAYOUT_TREE) -> float:
@@ -349,7 +371,7 @@ def verify_block(*, key, K, gamma, m, T_target, T_draft, prefix, start_pos, targ
     return out
 
 
-def verify_block_parallel(workers: int, seqs=None, **kw) -> dict:
+def verify_block_parallel(workers: int, seqs=None, mpfr_mode: bool = False, **kw) -> dict:
     """verify_block over `seqs` (default all), one sequence per task on `workers`
     threads.  The C oracle runs with the interpreter lock released (ctypes), so the
     sequences are checked in parallel; results and comparison counts are merged."""
@@ -359,7 +381,8 @@ def verify_block_parallel(workers: int, seqs=None, **kw) -> dict:
     B = kw["target_logits"].shape[0]
     seqs = list(range(B)) if seqs is None else list(seqs)
     with concurrent.futures.ThreadPoolExecutor(max_workers=max(1, workers)) as ex:
-        parts = list(ex.map(lambda b: verify_block(seqs=[b], **kw), seqs))
+        fn = verify_block_mpfr if mpfr_mode else verify_block
+        parts = list(ex.map(lambda b: fn(seqs=[b], **kw), seqs))
     out = {"draft_tokens": {}, "target_tokens": {}, "out_tokens": {}, "out_len": {}, "draft_lse": {},
            "target_lse": {}, "stats": {"exact": 0, "near_tie": 0, "mismatch": 0, "mismatches": []}}
     for part in parts:
@@ -368,5 +391,111 @@ def verify_block_parallel(workers: int, seqs=None, **kw) -> dict:
         for k in ("exact", "near_tie", "mismatch"):
             out["stats"][k] += part["stats"][k]
         out["stats"]["mismatches"] += part["stats"]["mismatches"]
+    return out
+
+
+# ---------------------------------------------------------------- identical drafters (MPFR)
+
+def context_groups(paths):
+    """Paths with equal draft prefixes share a context (Alg. "Multi-Draft ... (Formal)":
+    the context tree with multiplicities).  Returns the groups as lists of path
+    indices in increasing order, ordered by their lowest index."""
+    groups = {}
+    for k, pre in enumerate(paths):
+        groups.setdefault(tuple(int(t) for t in pre), []).append(k)
+    return sorted(groups.values(), key=lambda g: g[0])
+
+
+def _check_mpfr(tag, got, res, stats):
+    """GPU samples of one context (member order) against the oracle's sorted list:
+    exact, or each differing sample inside a run of oracle scores closer than
+    NEAR_TIE to the one at its rank (either order of near-tied arrivals is valid)."""
+    want = res["tokens"][:len(got)]
+    if list(got) == want:
+        stats["exact"] += 1
+        return
+    sc = res["scores"]
+    for i, g in enumerate(got):
+        if g == want[i]:
+            continue
+        lo = hi = i
+        while lo > 0 and sc[lo] - sc[lo - 1] < NEAR_TIE:
+            lo -= 1
+        while hi + 1 < len(sc) and sc[hi + 1] - sc[hi] < NEAR_TIE:
+            hi += 1
+        if g not in res["tokens"][lo:hi + 1]:
+            stats["mismatch"] += 1
+            stats["mismatches"].append((tag, list(got), want, sc))
+            return
+    stats["near_tie"] += 1
+
+
+def verify_block_mpfr(*, key, K, gamma, m, T_target, T_draft, prefix, start_pos, target_logits,
+                      draft_logits=None, draft_tokens=None, target_rows=1, layout=LAYOUT_TREE, gpu=None, seqs=None):
+    """Oracle of one speculative block with K identical drafters (MPFR mode).
+
+    Paths stand for the K drafts of Alg. "Multi-Draft ... (Formal)": at depth s the
+    paths whose drafts so far are equal form one context c with multiplicity nu(c)
+    = the group's size; the context's proposal row is the draft row of its lowest
+    path, its keyed source Pi(c) = the context key of (key, t, last m tokens), and
+    its nu(c) drafts are MPFR(Q(.|c), Pi(c), nu(c)) -- the i-th smallest score goes
+    to the group's i-th path, so equal draft tokens move to one child context with
+    their count as its multiplicity.  The target at a context is MPFR(P(.|c), Pi(c), 1),
+    the race of slot 0 alone; the walk is the HET walk (emit y(c*), stop unless it is
+    among the drafts D(c*) of the active paths).  Arguments as verify_block."""
+    B = target_logits.shape[0]
+    seqs = list(range(B)) if seqs is None else list(seqs)
+    stats = {"exact": 0, "near_tie": 0, "mismatch": 0, "mismatches": []}
+    out = {"draft_tokens": {}, "target_tokens": {}, "out_tokens": {}, "out_len": {},
+           "draft_lse": {}, "target_lse": {}, "stats": stats}
+    per_path = target_rows != 1
+    for b in seqs:
+        pre = [int(a) for a in prefix[b]]
+        t0 = int(start_pos[b])
+        drafts = np.zeros((K, gamma), np.int64)
+        for s in range(gamma):
+            if draft_logits is None:
+                drafts[:, s] = [int(draft_tokens[b][k][s]) for k in range(K)]
+                continue
+            for k in range(K):
+                out["draft_lse"][(b, k, s)] = lse(draft_logits[b][k][s], T_draft)
+            for members in context_groups([drafts[k, :s] for k in range(K)]):
+                rep = members[0]
+                kappa = context_key(key, t0 + s, window_of(pre, drafts[rep, :s], m))
+                res = mpfr(draft_logits[b][rep][s], T_draft, kappa, len(members), layout)
+                if gpu is not None:
+                    got = [int(gpu["draft_tokens"][b][k][s]) for k in members]
+                    _check_mpfr(("draft", b, s, tuple(members)), got, res, stats)
+                    for k, g in zip(members, got):
+                        drafts[k, s] = g
+                else:
+                    for k, v in zip(members, res["samples"]):
+                        drafts[k, s] = v
+        out["draft_tokens"][b] = drafts
+        chains = []
+        for k in (range(K) if per_path else [None]):
+            chain = np.zeros(gamma + 1, np.int64)
+            for s in range(gamma + 1):
+                if per_path:
+                    ctx_path, row = drafts[k, :s], target_logits[b][k][s]
+                    gtok = None if gpu is None else int(gpu["target_tokens"][b][k][s])
+                else:
+                    ctx_path = gpu["target_tokens"][b][:s] if gpu is not None else chain[:s]
+                    row = target_logits[b][s]
+                    gtok = None if gpu is None else int(gpu["target_tokens"][b][s])
+                kappa = context_key(key, t0 + s, window_of(pre, ctx_path, m))
+                res = race(row, T_target, kappa, 0, 1, layout)
+                out["target_lse"][(b, k, s) if per_path else (b, s)] = res["lse"]
+                if gtok is not None:
+                    _check(("target", b, k, s), gtok, res, row, T_target, kappa, 0, 1, layout, stats)
+                    chain[s] = gtok
+                else:
+                    chain[s] = res["token"]
+            chains.append(chain)
+        chain_arr = np.stack(chains) if per_path else chains[0]
+        out["target_tokens"][b] = chain_arr
+        emitted = walk(drafts, chain_arr, K, gamma, per_path)
+        out["out_tokens"][b] = emitted
+        out["out_len"][b] = len(emitted)
     return out
 

@@ -287,6 +287,67 @@ int oracle_race(const float *logits, int V, float T, const uint32_t kappa[2], in
     return 0;
 }
 
+/* ---------------- multi-sample PFR (identical drafters) ------------------ */
+
+/* MPFR samples of one row (Sec. 5 eq. MPFR; App. "A better finite-support MPFR
+ * implementation", Alg. "Direct finite-support implementation of B-sample MPFR"):
+ * token v's arrivals are G_{v,j} = E_0[v] + ... + E_j[v] (slot i of the keyed
+ * source is the (i+1)-th exponential of v's unit-rate clock), its mapped score is
+ * G_{v,j} / P(v), and the samples are the labels of the smallest scores over
+ * (v, j < nu) -- no token can hold more than nu of the nu smallest, so nu arrivals
+ * per token suffice.  Scores in log form: ln G_{v,j} - l_v / T (the LSE is common
+ * to all).  Exact ties: lowest v, then lowest j.
+ * Writes the n_out smallest (score, token, arrival) in increasing order (n_out >= nu:
+ * the first nu are the samples, the rest classify near-ties); entries past the
+ * number of finite-score pairs get token -1 and score +inf.  Returns 0, or < 0 on
+ * bad arguments / allocation failure. */
+int oracle_mpfr(const float *logits, int V, float T, const uint32_t kappa[2], int nu, int layout, int n_out,
+                int32_t *tokens, int32_t *arrivals, double *scores) {
+    if (V < 1 || V > (1 << 19) || nu < 1 || n_out < nu) return -1;
+    double *E = (double *)malloc(sizeof(double) * (size_t)V);
+    double *G = (double *)malloc(sizeof(double) * (size_t)V * (size_t)nu);
+    if (!E || !G) {
+        free(E); free(G);
+        return -2;
+    }
+    for (int j = 0; j < nu; j++) {
+        oracle_clocks(kappa, j, V, layout, E);
+        for (int v = 0; v < V; v++) G[(size_t)v * nu + j] = (j == 0 ? 0.0 : G[(size_t)v * nu + j - 1]) + E[v];
+    }
+    for (int i = 0; i < n_out; i++) {
+        tokens[i] = -1;
+        arrivals[i] = -1;
+        scores[i] = INFINITY;
+    }
+    /* plain insertion into the sorted list of the n_out smallest */
+    for (int v = 0; v < V; v++) {
+        double x = (double)logits[v] / (double)T;
+        if (x == -INFINITY) continue;
+        for (int j = 0; j < nu; j++) {
+            double sc = log(G[(size_t)v * nu + j]) - x;
+            int pos = n_out;
+            while (pos > 0) {
+                int q = pos - 1;
+                /* (sc, v, j) before entry q?  entries hold lower (v, j) on equal scores */
+                if (sc < scores[q]) pos = q;
+                else break;
+            }
+            if (pos >= n_out) continue;
+            for (int q = n_out - 1; q > pos; q--) {
+                scores[q] = scores[q - 1];
+                tokens[q] = tokens[q - 1];
+                arrivals[q] = arrivals[q - 1];
+            }
+            scores[pos] = sc;
+            tokens[pos] = v;
+            arrivals[pos] = j;
+        }
+    }
+    free(E);
+    free(G);
+    return 0;
+}
+
 /* ---------------- detection --------------------------------------------- */
 
 /* A_t = -log(1 - r_t(w_t)) with r = exp(-K * min_{j<K} E_j[w]): the target's
