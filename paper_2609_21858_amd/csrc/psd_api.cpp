@@ -46,8 +46,7 @@ psd_status check_params(const psd_params* p) {
     if (p->dtype != PSD_F32 && p->dtype != PSD_BF16) return fail(PSD_E_ARG, "unknown dtype %d", p->dtype);
     if (p->clocks != PSD_CLOCKS_TREE && p->clocks != PSD_CLOCKS_FLAT)
         return fail(PSD_E_ARG, "unknown clock layout %d", p->clocks);
-    if (p->mode == PSD_MODE_MPFR) return fail(PSD_E_UNSUPPORTED, "mode MPFR (identical drafters) is not implemented");
-    if (p->mode != PSD_MODE_HET) return fail(PSD_E_ARG, "unknown mode %d", p->mode);
+    if (p->mode != PSD_MODE_HET && p->mode != PSD_MODE_MPFR) return fail(PSD_E_ARG, "unknown mode %d", p->mode);
     return PSD_OK;
 }
 
@@ -88,6 +87,7 @@ psd::RaceArgs base_args(const psd_params* p, const psd_block* b) {
     a.inv_T_draft = 1.0f / p->temp_draft;
     a.status = b->status;
     a.spin_limit = g_spin_limit.load(std::memory_order_relaxed);
+    a.target_slots = p->mode == PSD_MODE_MPFR ? 1 : p->num_drafts;
     return a;
 }
 
@@ -132,6 +132,39 @@ void build_depths(psd::RaceArgs& a, int n_depth) {
     a.n_phase = n;
     a.n_items = first;
     a.n_rows = first / a.L.nseg;
+}
+
+// Identical drafters: depths [s_begin, s_begin + s_count) drafted one launch per depth
+// (each depth's contexts depend on the previous depth's drafts).
+psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_begin, int32_t s_count,
+                           const void* draft_logits, int32_t* draft_tokens, float* draft_lse, hipStream_t stream) {
+    const size_t es = p->dtype == PSD_BF16 ? 2 : 4;
+    const bool vec = ((size_t)p->vocab * es) % 16 == 0 && aligned16(draft_logits);
+    psd::MpfrArgs m;
+    memset(&m, 0, sizeof m);
+    m.logits = draft_logits;
+    m.draft_tokens = draft_tokens;
+    m.draft_lse = draft_lse;
+    m.prefix = b->prefix_tokens;
+    m.start_pos = b->start_pos;
+    m.ctrl = (uint32_t*)((unsigned char*)b->workspace +
+                         psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16).ctrl);
+    m.key = p->key;
+    m.V = p->vocab;
+    m.K = p->num_drafts;
+    m.m = p->ctx_window;
+    m.B = b->batch;
+    m.gamma = b->gamma;
+    m.s_begin = s_begin;
+    m.s_count = s_count;
+    m.T = p->temp_draft;
+    m.invT = 1.0f / p->temp_draft;
+    for (int s = s_begin; s < s_begin + s_count; ++s) {
+        m.s = s;
+        hipError_t e = psd::launch_mpfr_draft(m, p->dtype == PSD_BF16, vec, p->clocks, stream);
+        if (e != hipSuccess) return hip_fail(e, "MPFR draft kernel launch");
+    }
+    return PSD_OK;
 }
 
 psd_status run_race(const psd_params* p, psd::RaceArgs& a, hipStream_t stream) {
@@ -191,6 +224,15 @@ psd_status psd_draft(const psd_params* params, const psd_block* block, int32_t s
         return fail(PSD_E_ARG, "draft depths [%d, %d) outside [0, gamma=%d)", s_begin, s_begin + s_count, block->gamma);
     if (!draft_logits) return fail(PSD_E_ARG, "draft_logits is NULL");
     if (!draft_tokens) return fail(PSD_E_ARG, "draft_tokens is NULL");
+    if (params->mode == PSD_MODE_MPFR) {
+        if ((st = run_mpfr_drafts(params, block, s_begin, s_count, draft_logits, draft_tokens, draft_lse, stream)) != PSD_OK)
+            return st;
+        const psd::WsLayout L = psd::ws_layout(block->batch, params->num_drafts, block->gamma, params->vocab,
+                                               params->dtype == PSD_BF16);
+        hipError_t e = psd::launch_finish_status((uint32_t*)((unsigned char*)block->workspace + L.ctrl), block->status, stream);
+        if (e != hipSuccess) return hip_fail(e, "status kernel launch");
+        return PSD_OK;
+    }
     psd::RaceArgs a = base_args(params, block);
     a.draft_logits = draft_logits;
     a.draft_tokens = draft_tokens;
@@ -218,6 +260,14 @@ psd_status verify_impl(const psd_params* params, const psd_block* block, int32_t
     if (!draft_tokens) return fail(PSD_E_ARG, "draft_tokens is NULL");
     if (!out_tokens || !out_len) return fail(PSD_E_ARG, "out_tokens / out_len is NULL");
     if (!draft_logits && draft_lse) return fail(PSD_E_ARG, "draft_lse requires draft_logits");
+    if (params->mode == PSD_MODE_MPFR && draft_logits) {
+        // identical drafters: the context tree is drafted depth by depth first, then the
+        // target rows race slot 0 in the fused kernel with the drafts as input
+        if ((st = run_mpfr_drafts(params, block, 0, block->gamma, draft_logits, draft_tokens, draft_lse, stream)) != PSD_OK)
+            return st;
+        draft_logits = nullptr;
+        draft_lse = nullptr;
+    }
     psd::RaceArgs a = base_args(params, block);
     a.target_logits = target_logits;
     a.draft_logits = draft_logits;
@@ -292,7 +342,8 @@ psd_status psd_detect(const psd_params* params, int32_t n_seq, int32_t seq_len, 
     a.n_seq = n_seq;
     a.seq_len = seq_len;
     a.V = params->vocab;
-    a.K = params->num_drafts;
+    // identical drafters: the target races slot 0 alone, whose clock is the pivot (K = 1)
+    a.K = params->mode == PSD_MODE_MPFR ? 1 : params->num_drafts;
     a.m = params->ctx_window;
     hipError_t e = psd::launch_detect(a, params->clocks, stream);
     if (e != hipSuccess) return hip_fail(e, "detect kernel launch");

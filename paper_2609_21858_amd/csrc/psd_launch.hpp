@@ -17,7 +17,24 @@ struct DetectArgs {
     int n_seq, seq_len, V, K, m;
 };
 
+// One depth of drafting with identical drafters (multi-sample PFR), one workgroup
+// per draft row (b, k) of depth s.
+struct MpfrArgs {
+    const void* logits;         // [B][K][s_count][V] draft rows of depths s_begin .. s_begin + s_count - 1
+    int32_t* draft_tokens;      // [B][K][gamma]: depths < s read, depth s written
+    float* draft_lse;           // nullable [B][K][gamma]
+    const int32_t* prefix;      // [B][m]
+    const int64_t* start_pos;   // [B]
+    uint32_t* ctrl;             // workspace control words (error bits of the call)
+    uint64_t key;
+    int V, K, m, B, gamma;
+    int s_begin, s_count, s;    // depth of this launch: s_begin <= s < s_begin + s_count
+    float T, invT;
+};
+
 hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
+hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
+hipError_t launch_finish_status(uint32_t* ctrl, uint32_t* status, hipStream_t stream);
 hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream);
 hipError_t launch_pvalue(int n, const double* score, const int32_t* count, double* out_log_p,
                          double* out_anlppt, hipStream_t stream);

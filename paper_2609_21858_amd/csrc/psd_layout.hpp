@@ -101,6 +101,7 @@ struct RaceArgs {
     float inv_T_target, inv_T_draft;
     int s_begin, s_count;       // draft depths computed in this call (s_count = 0: none)
     int target_rows;            // 0: no target rows, 1: shared, K: per path
+    int target_slots;           // slots a target row races: K (distinct drafters), 1 (identical: MPFR)
     int n_items;                // rows * nseg
     int n_rows;                 // rows of this call
     // Work order: phases of rows, each at one depth: phase_nd draft rows, then

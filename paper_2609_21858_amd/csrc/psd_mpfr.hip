@@ -1,0 +1,604 @@
+// psd_mpfr.hip -- drafting with identical drafters: multi-sample PFR (gfx950).
+//
+// Sec. 5 (eq. MPFR) with the direct finite-support sampler of the appendix "A
+// better finite-support MPFR implementation": token v's unit-rate clock has
+// arrivals G_{v,j} = E_0[v] + ... + E_j[v] (slot i of the keyed source is v's
+// (i+1)-th exponential), and the nu samples of a context are the labels of the nu
+// smallest ln G_{v,j} - l_v / T over (v, j < nu).  In Alg. "Multi-Draft ...
+// (Formal)" the K drafts of a block form a context tree with multiplicities; here
+// the tree is held as K paths: at depth s the paths with equal drafts so far share
+// one context, whose proposal row is its lowest path's row, and the context's i-th
+// sample goes to its i-th path.
+//
+// One launch per depth, one workgroup per draft row (b, k).  Every workgroup
+// streams its row once (log-sum-exp, maxima of 128-token groups).  The workgroup
+// of a context's lowest path then samples the context:
+//  1. seeds: the largest token of the top group of each eighth of the row; their
+//     first nu arrivals, exact in fp64, give theta = the nu-th smallest of those
+//     scores, an upper bound on the context's nu-th smallest score;
+//  2. since G_{v,j} >= E_0[v], every token of a sample has a slot-0 score at most
+//     theta: a descent of slot 0's tree (root, 32768-, 2048- and 128-token nodes,
+//     8-token chunks) lists every token whose slot-0 score, in fp32 with a margin,
+//     is at most theta (flat clocks: every group whose clock-floor bound passes);
+//  3. the listed tokens' arrivals are rebuilt exactly in fp64 one at a time, and nu
+//     rounds of a workgroup-wide lexicographic minimum over (score, token, arrival)
+//     emit the samples in order (exact ties: lowest token, then lowest arrival).
+// The fp32 scores use (l - row maximum) / T, like the race kernel.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include "psd_device.hpp"
+#include "psd_launch.hpp"
+#include "psd_layout.hpp"
+
+namespace psd {
+
+namespace {
+
+constexpr int kMBlock = 256;
+constexpr int kMaxGroups = 4096;  // 128-token groups of V <= 2^19
+constexpr int kMCand = 1024;      // listed candidate tokens of a context
+constexpr int kSeeds = 8;
+constexpr float kMMargin = 1e-3f;  // fp32 pruning margin (score units)
+constexpr uint32_t kMErrCand = 2u;
+
+struct MNode {
+    uint32_t i;  // node index at its level
+    float m;     // slot-0 minimum clock of the node
+    uint32_t p;  // token holding it
+};
+
+struct MShared {
+    float gm[kMaxGroups];      // group maxima of the row
+    float m3[256];             // 2048-token block maxima
+    float m4[16];              // 32768-token node maxima
+    int path_tok[32 * 32];     // draft tokens of the K paths at depths < s ([path][depth])
+    int seed_g[kSeeds];
+    int seed_tok[kSeeds];
+    double pair[kSeeds * 32];  // seed arrival scores (shifted frame)
+    MNode l4[16];
+    MNode l3[256];
+    MNode lg[256];             // surviving groups of one batch of level-3 nodes
+    int cand_v[kMCand];
+    float cand_x[kMCand];
+    int cand_j[kMCand];
+    double cand_g[kMCand];
+    double cand_s[kMCand];
+    float red_m[kMBlock / 64], red_s[kMBlock / 64], red_x[kMBlock / 64];
+    double red_d[kMBlock / 64];
+    int red_v[kMBlock / 64], red_j[kMBlock / 64], red_i[kMBlock / 64];
+    uint32_t mask;
+    int n_l4, n_l3, n_lg, n_cand;
+    float rowmax, theta;
+    uint32_t kappa0, kappa1;
+    int samples[32];
+};
+
+__device__ __forceinline__ float mload(const unsigned char* row, bool bf16, int v) {
+    return bf16 ? __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16) : ((const float*)row)[v];
+}
+
+// 8 logits from `base` (-inf past V).
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void mload8(const unsigned char* row, int V, int base, float (&x)[8]) {
+    if constexpr (VEC) {
+        if constexpr (BF16) {
+            uint4 u = make_uint4(0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u);
+            if (base < V) u = *(const uint4*)((const uint16_t*)row + base);
+            x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
+            x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
+        } else {
+            float4 f0 = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY), f1 = f0;
+            if (base < V) f0 = *(const float4*)((const float*)row + base);
+            if (base + 4 < V) f1 = *(const float4*)((const float*)row + base + 4);
+            x[0] = f0.x; x[1] = f0.y; x[2] = f0.z; x[3] = f0.w;
+            x[4] = f1.x; x[5] = f1.y; x[6] = f1.z; x[7] = f1.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = base + i < V ? mload(row, BF16, base + i) : -INFINITY;
+    }
+}
+
+template <int LAYOUT>
+__device__ __forceinline__ double clock_f64(uint32_t V, uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
+    return LAYOUT == 0 ? tree_clock_f64(V, slot, v, k0, k1) : flat_clock_f64(slot, v, k0, k1);
+}
+
+__device__ __forceinline__ bool lexless(double s, int v, int j, double s2, int v2, int j2) {
+    return s < s2 || (s == s2 && (v < v2 || (v == v2 && j < j2)));
+}
+
+// (a list longer than kMCand is counted, not stored: the caller tightens theta and
+// lists again)
+__device__ __forceinline__ void push_cand(MShared& sm, int v, float x) {
+    const int i = atomicAdd(&sm.n_cand, 1);
+    if (i < kMCand) {
+        sm.cand_v[i] = v;
+        sm.cand_x[i] = x;
+    }
+}
+
+// The candidates of one 8-token chunk (lane's part of a surviving group): chunk
+// minimum (mc, pc), slot-0 token clocks, scores against theta.
+template <int LAYOUT>
+__device__ __forceinline__ void eval_chunk(MShared& sm, const MpfrArgs& a, const float (&x)[8], uint32_t chunk,
+                                           float mg, uint32_t pg, float shift, uint32_t k0, uint32_t k1) {
+    const uint32_t V = (uint32_t)a.V;
+    const uint32_t cs = chunk * 8u, ce = node_end(kShift1, chunk, V);
+    if (cs >= V) return;
+    float cmax = -INFINITY;
+    for (uint32_t t = 0; t < ce - cs; ++t) cmax = fmaxf(cmax, x[t]);
+    if (cmax == -INFINITY) return;
+    const float theta = sm.theta;
+    float mc = 0.f;
+    uint32_t pc = 0u;
+    if constexpr (LAYOUT == 0) {
+        child_min_f32(mg, pg, 1, chunk, cs, ce, 0u, k0, k1, mc, pc);
+        if (ln_f32(mc) - (cmax - shift) * a.invT > theta) return;
+    } else {
+        if (kLnClockFloor - (cmax - shift) * a.invT > theta) return;
+    }
+#pragma unroll
+    for (uint32_t h = 0; h < 2; ++h) {
+        const Words w = LAYOUT == 0 ? philox(chunk, 0u, 8u + h, kDomainTree, k0, k1)
+                                    : philox((cs >> 2) + h, 0u, 0u, kDomainFlat, k0, k1);
+        const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
+#pragma unroll
+        for (uint32_t t = 0; t < 4; ++t) {
+            const uint32_t v = cs + 4u * h + t;
+            const float xv = x[4 * h + t];
+            if (v >= ce || xv == -INFINITY) continue;
+            float E;
+            if constexpr (LAYOUT == 0)
+                E = v == pc ? mc : mc + exp1_f32(ws[t]);
+            else
+                E = exp1_f32(ws[t]);
+            if (ln_f32(E) - (xv - shift) * a.invT <= theta) push_cand(sm, (int)v, xv);
+        }
+    }
+}
+
+template <bool BF16, bool VEC, int LAYOUT>
+__global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
+    __shared__ MShared sm;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = (int)blockIdx.x / a.K, k = (int)blockIdx.x % a.K, s = a.s;
+    const uint32_t V = (uint32_t)a.V;
+    const int ng = (a.V + 127) / 128, n3 = (ng + 15) / 16, n4 = (n3 + 15) / 16;
+    const size_t esize = BF16 ? 2 : 4;
+    const unsigned char* row = (const unsigned char*)a.logits +
+                               (((size_t)b * a.K + k) * a.s_count + (size_t)(s - a.s_begin)) * (size_t)a.V * esize;
+
+    // ---- the context of path k: the paths whose drafts at depths < s equal its own
+    for (int e = tid; e < a.K * s; e += kMBlock)
+        sm.path_tok[e] = a.draft_tokens[((size_t)b * a.K + e / s) * a.gamma + e % s];
+    if (tid == 0) sm.n_l4 = sm.n_l3 = sm.n_cand = 0;
+    __syncthreads();
+    if (wave == 0) {
+        bool same = lane < a.K;
+        for (int d = 0; d < s && same; ++d) same = sm.path_tok[lane * s + d] == sm.path_tok[k * s + d];
+        const uint64_t bal = __ballot(same);
+        if (lane == 0) sm.mask = (uint32_t)bal;
+    }
+
+    // ---- stream the row: log-sum-exp, group maxima, row maximum
+    const float c2 = a.invT * 1.4426950408889634f;
+    float mrun = -INFINITY, srun = 0.f, xmax = -INFINITY;
+    const int nstep = (a.V + 2047) / 2048;
+    for (int st0 = 0; st0 < nstep; st0 += 4) {
+        float x[4][8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mload8<BF16, VEC>(row, a.V, (st0 + q) * 2048 + 8 * tid, x[q]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (st0 + q >= nstep) break;
+            float um = x[q][0];
+#pragma unroll
+            for (int i = 1; i < 8; ++i) um = fmaxf(um, x[q][i]);
+            const float g = row16_max(um);
+            const int gi = (st0 + q) * 16 + (tid >> 4);
+            if ((lane & 15) == 0 && gi < ng) sm.gm[gi] = g;
+            xmax = fmaxf(xmax, um);
+            if (um > -INFINITY) {
+                const float mn = fmaxf(mrun, um * c2);
+                float acc = mrun == -INFINITY ? 0.f : srun * __builtin_amdgcn_exp2f(mrun - mn);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) acc += __builtin_amdgcn_exp2f(fmaf(x[q][i], c2, -mn));
+                srun = acc;
+                mrun = mn;
+            }
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const float om = __shfl_xor(mrun, off), os = __shfl_xor(srun, off);
+        xmax = fmaxf(xmax, __shfl_xor(xmax, off));
+        const float mn = fmaxf(mrun, om);
+        if (mn > -INFINITY) {
+            srun = (mrun == -INFINITY ? 0.f : srun * __builtin_amdgcn_exp2f(mrun - mn)) +
+                   (om == -INFINITY ? 0.f : os * __builtin_amdgcn_exp2f(om - mn));
+            mrun = mn;
+        }
+    }
+    if (lane == 0) {
+        sm.red_m[wave] = mrun;
+        sm.red_s[wave] = srun;
+        sm.red_x[wave] = xmax;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        float m = sm.red_m[0], sacc = sm.red_s[0], xm = sm.red_x[0];
+        for (int w = 1; w < kMBlock / 64; ++w) {
+            xm = fmaxf(xm, sm.red_x[w]);
+            const float om = sm.red_m[w], os = sm.red_s[w], mn = fmaxf(m, om);
+            if (mn > -INFINITY) {
+                sacc = (m == -INFINITY ? 0.f : sacc * __builtin_amdgcn_exp2f(m - mn)) +
+                       (om == -INFINITY ? 0.f : os * __builtin_amdgcn_exp2f(om - mn));
+                m = mn;
+            }
+        }
+        sm.rowmax = xm;
+        if (a.draft_lse)
+            a.draft_lse[((size_t)b * a.K + k) * a.gamma + s] =
+                m == -INFINITY ? -INFINITY : (m + __builtin_amdgcn_logf(sacc)) * 0.69314718055994531f;
+    }
+    __syncthreads();
+    const uint32_t mask = sm.mask;
+    if (k != __ffs((int)mask) - 1) return;  // the context's lowest path samples it (uniform)
+    const int nu = __popc(mask);
+    const float shift = sm.rowmax;
+    if (shift == -INFINITY) {  // no finite logit: every draft of the context is -1
+        if (tid < nu) sm.samples[tid] = -1;
+    } else {
+        // ---- context key (key, t, last m tokens of prefix || path), level maxima, seeds
+        if (tid == 0) {
+            uint32_t k0 = (uint32_t)a.key, k1 = (uint32_t)(a.key >> 32);
+            const uint64_t t = (uint64_t)(a.start_pos[b] + s);
+            fold(k0, k1, (uint32_t)t, (uint32_t)(t >> 32), 0u);
+            for (int i = 0; i < a.m; ++i) {
+                const int g = s + i;  // index in prefix (m tokens) || path (s tokens)
+                const int w = g < a.m ? a.prefix[(size_t)b * a.m + g] : sm.path_tok[k * s + (g - a.m)];
+                fold(k0, k1, (uint32_t)w, (uint32_t)i, 1u);
+            }
+            sm.kappa0 = k0;
+            sm.kappa1 = k1;
+        }
+        for (int t = tid; t < n3; t += kMBlock) {
+            float mx = -INFINITY;
+            for (int g = 16 * t; g < min(ng, 16 * t + 16); ++g) mx = fmaxf(mx, sm.gm[g]);
+            sm.m3[t] = mx;
+        }
+        {
+            // seed groups: the largest group of each eighth of the row (lowest index on ties)
+            const int r = 2 * wave + (lane >> 5), l32 = lane & 31;
+            const int g0 = r * ng / kSeeds, g1 = (r + 1) * ng / kSeeds;
+            float bv = -INFINITY;
+            int bg = 0x7FFFFFFF;
+            for (int g = g0 + l32; g < g1; g += 32)
+                if (sm.gm[g] > bv) {
+                    bv = sm.gm[g];
+                    bg = g;
+                }
+#pragma unroll
+            for (int off = 16; off > 0; off >>= 1) {
+                const float ov = __shfl_xor(bv, off);
+                const int og = __shfl_xor(bg, off);
+                if (ov > bv || (ov == bv && og < bg)) {
+                    bv = ov;
+                    bg = og;
+                }
+            }
+            if (l32 == 0) sm.seed_g[r] = bv == -INFINITY ? -1 : bg;
+        }
+        __syncthreads();
+        for (int t = tid; t < n4; t += kMBlock) {
+            float mx = -INFINITY;
+            for (int i = 16 * t; i < min(n3, 16 * t + 16); ++i) mx = fmaxf(mx, sm.m3[i]);
+            sm.m4[t] = mx;
+        }
+        if (tid < kSeeds * 16) {
+            // the seed group's largest token (its lowest index holding the maximum)
+            const int i = tid >> 4, sub = tid & 15, g = sm.seed_g[i];
+            int tk = 0x7FFFFFFF;
+            if (g >= 0) {
+                float x[8];
+                const int base = g * 128 + sub * 8;
+                mload8<BF16, VEC>(row, a.V, base, x);
+#pragma unroll
+                for (int t = 7; t >= 0; --t)
+                    if (base + t < a.V && x[t] == sm.gm[g]) tk = base + t;
+            }
+#pragma unroll
+            for (int off = 8; off > 0; off >>= 1) tk = min(tk, __shfl_xor(tk, off));
+            if (sub == 0) sm.seed_tok[i] = g >= 0 && tk != 0x7FFFFFFF ? tk : -1;
+        }
+        __syncthreads();
+        const uint32_t k0 = sm.kappa0, k1 = sm.kappa1;
+        // seed arrivals, exact: E_j for every (seed, j < nu), then cumulative sums
+        for (int e = tid; e < kSeeds * nu; e += kMBlock) {
+            const int i = e / nu, j = e % nu, v = sm.seed_tok[i];
+            sm.pair[i * 32 + j] = v >= 0 ? clock_f64<LAYOUT>(V, (uint32_t)j, (uint32_t)v, k0, k1) : 0.0;
+        }
+        __syncthreads();
+        if (tid < kSeeds) {
+            const int v = sm.seed_tok[tid];
+            const double xs = v >= 0 ? ((double)mload(row, BF16, v) - (double)shift) / (double)a.T : 0.0;
+            double G = 0.0;
+            for (int j = 0; j < nu; ++j) {
+                G += sm.pair[tid * 32 + j];
+                sm.pair[tid * 32 + j] = v >= 0 ? log(G) - xs : INFINITY;
+            }
+            for (int j = nu; j < 32; ++j) sm.pair[tid * 32 + j] = INFINITY;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            // theta = the nu-th smallest seed score (nu rounds of a wave minimum)
+            double v4[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v4[q] = sm.pair[lane + 64 * q];
+            double th = INFINITY;
+            for (int r = 0; r < nu; ++r) {
+                double mv = v4[0];
+                int mi = lane;
+#pragma unroll
+                for (int q = 1; q < 4; ++q)
+                    if (v4[q] < mv) {
+                        mv = v4[q];
+                        mi = lane + 64 * q;
+                    }
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    const double ov = __shfl_xor(mv, off);
+                    const int oi = __shfl_xor(mi, off);
+                    if (ov < mv || (ov == mv && oi < mi)) {
+                        mv = ov;
+                        mi = oi;
+                    }
+                }
+                th = mv;
+                if ((mi & 63) == lane) v4[mi >> 6] = INFINITY;
+            }
+            if (lane == 0) sm.theta = th == INFINITY ? INFINITY : (float)th + kMMargin;
+        }
+        __syncthreads();
+
+        // ---- list every token whose slot-0 score can reach theta.  A list longer than
+        // kMCand tightens theta to the nu-th smallest exact slot-0 score among its first
+        // kMCand tokens (nu real arrivals, so still an upper bound) and lists again.
+        float rm = 0.f;
+        uint32_t rp = 0u;
+        if constexpr (LAYOUT == 0) root_min_f32(V, 0u, k0, k1, rm, rp);
+        for (int attempt = 0;; ++attempt) {
+            if (tid == 0) sm.n_l4 = sm.n_l3 = sm.n_cand = 0;
+            __syncthreads();
+            if constexpr (LAYOUT == 0) {
+                if (tid < n4) {
+                    float m;
+                    uint32_t p;
+                    const uint32_t cs = (uint32_t)tid << kShift4;
+                    child_min_f32(rm, rp, 4, (uint32_t)tid, cs, node_end(kShift4, (uint32_t)tid, V), 0u, k0, k1, m, p);
+                    if (ln_f32(m) - (sm.m4[tid] - shift) * a.invT <= sm.theta)
+                        sm.l4[atomicAdd(&sm.n_l4, 1)] = MNode{(uint32_t)tid, m, p};
+                }
+                __syncthreads();
+                if (tid < sm.n_l4 * 16) {
+                    const MNode pa = sm.l4[tid >> 4];
+                    const uint32_t i3 = pa.i * 16u + (uint32_t)(tid & 15);
+                    if ((int)i3 < n3) {
+                        float m;
+                        uint32_t p;
+                        child_min_f32(pa.m, pa.p, 3, i3, i3 << kShift3, node_end(kShift3, i3, V), 0u, k0, k1, m, p);
+                        if (ln_f32(m) - (sm.m3[i3] - shift) * a.invT <= sm.theta)
+                            sm.l3[atomicAdd(&sm.n_l3, 1)] = MNode{i3, m, p};
+                    }
+                }
+                __syncthreads();
+                const int nl3 = sm.n_l3;
+                for (int n0 = 0; n0 < nl3; n0 += 16) {  // 16 level-3 nodes (256 groups) per batch
+                    if (tid == 0) sm.n_lg = 0;
+                    __syncthreads();
+                    const int e = n0 * 16 + tid;
+                    if (e < nl3 * 16) {
+                        const MNode pa = sm.l3[e >> 4];
+                        const uint32_t g = pa.i * 16u + (uint32_t)(e & 15);
+                        if ((int)g < ng && ln_f32(pa.m) - (sm.gm[g] - shift) * a.invT <= sm.theta) {
+                            float m;
+                            uint32_t p;
+                            child_min_f32(pa.m, pa.p, 2, g, g << kShift2, node_end(kShift2, g, V), 0u, k0, k1, m, p);
+                            if (ln_f32(m) - (sm.gm[g] - shift) * a.invT <= sm.theta)
+                                sm.lg[atomicAdd(&sm.n_lg, 1)] = MNode{g, m, p};
+                        }
+                    }
+                    __syncthreads();
+                    const int nlg = sm.n_lg;
+                    for (int g0 = 0; g0 < nlg; g0 += 16) {  // 16 lanes per group, one chunk each
+                        const int gi = g0 + (tid >> 4);
+                        if (gi < nlg) {
+                            const MNode gn = sm.lg[gi];
+                            const uint32_t chunk = gn.i * 16u + (uint32_t)(tid & 15);
+                            float x[8];
+                            mload8<BF16, VEC>(row, a.V, (int)(chunk * 8u), x);
+                            eval_chunk<0>(sm, a, x, chunk, gn.m, gn.p, shift, k0, k1);
+                        }
+                    }
+                    __syncthreads();
+                }
+            } else {
+                for (int g0 = 0; g0 < ng; g0 += 16) {
+                    const int g = g0 + (tid >> 4);
+                    if (g < ng && kLnClockFloor - (sm.gm[g] - shift) * a.invT <= sm.theta) {
+                        const uint32_t chunk = (uint32_t)g * 16u + (uint32_t)(tid & 15);
+                        float x[8];
+                        mload8<BF16, VEC>(row, a.V, (int)(chunk * 8u), x);
+                        eval_chunk<1>(sm, a, x, chunk, 0.f, 0u, shift, k0, k1);
+                    }
+                }
+            }
+            __syncthreads();
+            if (sm.n_cand <= kMCand) break;
+            if (attempt == 3) {  // still too many: the samples may be wrong, and the call says so
+                if (tid == 0)
+                    __hip_atomic_fetch_or(a.ctrl + kCtrlCallErrors, kMErrCand, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            // tighter theta: exact slot-0 scores of the stored tokens, nu-th smallest
+            for (int c = tid; c < kMCand; c += kMBlock)
+                sm.cand_s[c] = log(clock_f64<LAYOUT>(V, 0u, (uint32_t)sm.cand_v[c], k0, k1)) -
+                               ((double)sm.cand_x[c] - (double)shift) / (double)a.T;
+            __syncthreads();
+            double th = INFINITY;
+            for (int r = 0; r < nu; ++r) {
+                double bs = INFINITY;
+                int bi = 0x7FFFFFFF;
+                for (int c = tid; c < kMCand; c += kMBlock)
+                    if (sm.cand_s[c] < bs) {
+                        bs = sm.cand_s[c];
+                        bi = c;
+                    }
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    const double os = __shfl_xor(bs, off);
+                    const int oi = __shfl_xor(bi, off);
+                    if (os < bs || (os == bs && oi < bi)) {
+                        bs = os;
+                        bi = oi;
+                    }
+                }
+                if (lane == 0) {
+                    sm.red_d[wave] = bs;
+                    sm.red_i[wave] = bi;
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    for (int w = 1; w < kMBlock / 64; ++w)
+                        if (sm.red_d[w] < bs || (sm.red_d[w] == bs && sm.red_i[w] < bi)) {
+                            bs = sm.red_d[w];
+                            bi = sm.red_i[w];
+                        }
+                    if (bi >= 0 && bi < kMCand) sm.cand_s[bi] = INFINITY;
+                    sm.red_d[0] = bs;
+                }
+                __syncthreads();
+                th = sm.red_d[0];
+                __syncthreads();
+            }
+            if (tid == 0) sm.theta = fminf(sm.theta, (float)th + kMMargin);
+            __syncthreads();
+        }
+
+        // ---- exact arrivals of the listed tokens; nu rounds of the lexicographic minimum
+        const int nc = min(sm.n_cand, kMCand);
+        for (int c = tid; c < nc; c += kMBlock) {
+            const int v = sm.cand_v[c];
+            const double G = clock_f64<LAYOUT>(V, 0u, (uint32_t)v, k0, k1);
+            sm.cand_g[c] = G;
+            sm.cand_j[c] = 0;
+            sm.cand_s[c] = log(G) - ((double)sm.cand_x[c] - (double)shift) / (double)a.T;
+        }
+        __syncthreads();
+        for (int r = 0; r < nu; ++r) {
+            double bs = INFINITY;
+            int bv = 0x7FFFFFFF, bj = 0x7FFFFFFF, bi = -1;
+            for (int c = tid; c < nc; c += kMBlock)
+                if (lexless(sm.cand_s[c], sm.cand_v[c], sm.cand_j[c], bs, bv, bj)) {
+                    bs = sm.cand_s[c];
+                    bv = sm.cand_v[c];
+                    bj = sm.cand_j[c];
+                    bi = c;
+                }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) {
+                const double os = __shfl_xor(bs, off);
+                const int ov = __shfl_xor(bv, off), oj = __shfl_xor(bj, off), oi = __shfl_xor(bi, off);
+                if (lexless(os, ov, oj, bs, bv, bj)) {
+                    bs = os;
+                    bv = ov;
+                    bj = oj;
+                    bi = oi;
+                }
+            }
+            if (lane == 0) {
+                sm.red_d[wave] = bs;
+                sm.red_v[wave] = bv;
+                sm.red_j[wave] = bj;
+                sm.red_i[wave] = bi;
+            }
+            __syncthreads();
+            if (tid == 0) {
+                for (int w = 1; w < kMBlock / 64; ++w)
+                    if (lexless(sm.red_d[w], sm.red_v[w], sm.red_j[w], bs, bv, bj)) {
+                        bs = sm.red_d[w];
+                        bv = sm.red_v[w];
+                        bj = sm.red_j[w];
+                        bi = sm.red_i[w];
+                    }
+                sm.samples[r] = bs < INFINITY ? bv : -1;
+                if (bi >= 0 && bs < INFINITY) {
+                    // the winner's next arrival (or none past nu)
+                    const int j = sm.cand_j[bi] + 1;
+                    if (j < nu) {
+                        const double G = sm.cand_g[bi] + clock_f64<LAYOUT>(V, (uint32_t)j, (uint32_t)bv, k0, k1);
+                        sm.cand_g[bi] = G;
+                        sm.cand_j[bi] = j;
+                        sm.cand_s[bi] = log(G) - ((double)sm.cand_x[bi] - (double)shift) / (double)a.T;
+                    } else {
+                        sm.cand_s[bi] = INFINITY;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        // the context's r-th sample goes to its r-th path
+        uint32_t mm = mask;
+        for (int r = 0; r < nu; ++r) {
+            const int kk = __ffs((int)mm) - 1;
+            mm &= mm - 1u;
+            a.draft_tokens[((size_t)b * a.K + kk) * a.gamma + s] = sm.samples[r];
+        }
+    }
+}
+
+// The call's error bits to the sticky word and the caller's status word (for calls
+// that end without a fused race kernel, whose last workgroup does this).
+__global__ void finish_status_kernel(uint32_t* ctrl, uint32_t* status) {
+    const uint32_t bits = __hip_atomic_exchange(ctrl + kCtrlCallErrors, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (bits) __hip_atomic_fetch_or(ctrl + kCtrlErrors, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (status) *status = bits;
+}
+
+}  // namespace
+
+hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout, hipStream_t stream) {
+    const dim3 grid((unsigned)(a.B * a.K)), block(kMBlock);
+    if (bf16) {
+        if (vec) {
+            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<true, true, 0>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((mpfr_draft_kernel<true, true, 1>), grid, block, 0, stream, a);
+        } else {
+            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<true, false, 0>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((mpfr_draft_kernel<true, false, 1>), grid, block, 0, stream, a);
+        }
+    } else {
+        if (vec) {
+            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<false, true, 0>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((mpfr_draft_kernel<false, true, 1>), grid, block, 0, stream, a);
+        } else {
+            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<false, false, 0>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((mpfr_draft_kernel<false, false, 1>), grid, block, 0, stream, a);
+        }
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_finish_status(uint32_t* ctrl, uint32_t* status, hipStream_t stream) {
+    hipLaunchKernelGGL(finish_status_kernel, dim3(1), dim3(1), 0, stream, ctrl, status);
+    return hipGetLastError();
+}
+
+}  // namespace psd

@@ -1527,7 +1527,7 @@ __device__ __forceinline__ void decode_item(const RaceArgs& a, const Shared& sm,
         }
         r.ptr = (const unsigned char*)a.target_logits + off * (size_t)a.V * esize;
         r.slot0 = 0;
-        r.nslots = a.K;
+        r.nslots = a.target_slots;
         r.invT = a.inv_T_target;
         r.T = a.T_target;
     }

@@ -81,9 +81,17 @@ def test_verify_rejects_bad_block(psd):
     assert "workspace" in psd.lib().psd_last_error().decode()
 
 
-def test_mode_mpfr_unsupported(psd):
+def test_mode_mpfr_validated_like_het(psd):
+    """Identical-drafter mode takes the same arguments and is checked the same way."""
     p = psd.make_params(1, 1000, 2, 4, mode=psd.PSD_MODE_MPFR)
-    assert _verify(psd, p) == psd.PSD_E_UNSUPPORTED
+    assert _verify(psd, p, B=0) == psd.PSD_E_ARG
+    assert _verify(psd, p, tl=None) == psd.PSD_E_ARG
+    assert _verify(psd, p, target_rows=3) == psd.PSD_E_ARG
+    assert _verify(psd, p, ws=None) == psd.PSD_E_WORKSPACE
+    blk = psd.Block(2, 3, FAKE, FAKE, FAKE, psd.workspace_bytes(p, 2, 3), None)
+    assert psd.lib().psd_draft(ctypes.byref(p), ctypes.byref(blk), 0, 4, FAKE, FAKE, None, None) == psd.PSD_E_ARG
+    p.mode = 2
+    assert _verify(psd, p) == psd.PSD_E_ARG
 
 
 def test_draft_and_detect_reject_bad_args(psd):

@@ -1,0 +1,157 @@
+"""GPU parity of identical-drafter (MPFR) mode against the CPU oracle.
+
+psd_verify / psd_draft with mode MPFR draw each context's nu(c) drafts as the
+labels of its nu(c) smallest mapped-Poisson scores (cumulative clocks) and race
+the target rows on slot 0; detection scores the slot-0 clock.  Per context the
+GPU's samples must equal the oracle's in order, except inside runs of oracle
+scores closer than 1e-6 (either order of near-tied arrivals is valid); target
+tokens, accepted lengths and emitted tokens exactly as in the distinct-drafter
+tests; LSE within 1e-5 relative (floor 1e-5 below |LSE| = 1).
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import oracle  # noqa: E402
+import workloads  # noqa: E402
+
+DEV = "cuda"
+LSE_TOL = 1e-5
+LAYOUTS = [0, 1]
+WORKERS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+@pytest.fixture(scope="module")
+def psd():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_21858_amd import psd as m
+    return m
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def run_mpfr(psd, w, seed, layout, target_rows=1, mode="fused", gen_device="cpu", seqs=None, blk=None):
+    print(f"[mpfr] {w.name} V={w.V} K={w.K} g={w.gamma} B={w.B} {w.dtype} T_Q={w.T_draft} layout={layout} "
+          f"rows={target_rows} mode={mode} seed={seed}", flush=True)
+    if blk is None:
+        blk = workloads.make_block(w, seed, device=gen_device, target_rows=target_rows)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in blk.items()}
+    params = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype, clocks=layout,
+                             mode=psd.PSD_MODE_MPFR)
+    ws = psd.new_workspace(params, w.B, w.gamma, DEV)
+    status = torch.full((1,), -1, dtype=torch.int32, device=DEV)
+    dl = torch.full((w.B, w.K, w.gamma), 7.0, dtype=torch.float32, device=DEV)
+    if mode == "fused":
+        out = psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], g["draft_logits"],
+                         target_rows=target_rows, want_lse=True, want_targets=True, status=status,
+                         out={"draft_lse": dl})
+    else:
+        dt = torch.full((w.B, w.K, w.gamma), -7, dtype=torch.int32, device=DEV)
+        st_d = torch.full((1,), -1, dtype=torch.int32, device=DEV)
+        for s in range(w.gamma):
+            psd.draft(params, ws, g["prefix_tokens"], g["start_pos"], w.gamma, s,
+                      g["draft_logits"][:, :, s:s + 1].contiguous(), dt, dl, status=st_d)
+            torch.cuda.synchronize()
+            assert int(st_d[0]) == 0
+        out = psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], None, dt,
+                         target_rows=target_rows, want_lse=True, want_targets=True, status=status)
+        out["draft_lse"] = dl
+    torch.cuda.synchronize()
+    assert int(status[0]) == 0 and psd.workspace_errors(ws) == 0
+    seqs = list(range(w.B)) if seqs is None else list(seqs)
+    gpu = {k: _np(v)[seqs] for k, v in out.items()}
+    ref = oracle.verify_block_parallel(WORKERS, mpfr_mode=True, key=w.key, K=w.K, gamma=w.gamma, m=w.m,
+                                       T_target=w.T_target, T_draft=w.T_draft,
+                                       prefix=_np(blk["prefix_tokens"])[seqs], start_pos=_np(blk["start_pos"])[seqs],
+                                       target_logits=workloads.as_f32_numpy(blk["target_logits"][seqs]),
+                                       draft_logits=workloads.as_f32_numpy(blk["draft_logits"][seqs]),
+                                       target_rows=target_rows, layout=layout, gpu=gpu)
+    st = ref["stats"]
+    assert st["mismatch"] == 0, st["mismatches"][:3]
+    merged = 0
+    for i in range(len(seqs)):
+        n = int(gpu["out_len"][i])
+        assert n == ref["out_len"][i], (i, n, ref["out_len"][i])
+        assert list(gpu["out_tokens"][i][:n]) == ref["out_tokens"][i]
+        assert all(x == -1 for x in gpu["out_tokens"][i][n:])
+        d = gpu["draft_tokens"][i]
+        merged += sum(len(oracle.context_groups([d[k, :s] for k in range(w.K)])) < w.K for s in range(1, w.gamma))
+    for key, v in ref["target_lse"].items():
+        got = gpu["target_lse"][key] if target_rows == 1 else gpu["target_lse"][key[0]][key[1]][key[2]]
+        assert (got == v == -np.inf) or abs(got - v) <= LSE_TOL * max(1.0, abs(v)), (key, got, v)
+    for (b, k, s), v in ref["draft_lse"].items():
+        got = gpu["draft_lse"][b][k][s]
+        assert (got == v == -np.inf) or abs(got - v) <= LSE_TOL * max(1.0, abs(v)), ((b, k, s), got, v)
+    print(f"[mpfr]   exact={st['exact']} near_tie={st['near_tie']} depths with shared contexts={merged} "
+          f"mean_tau={np.mean([ref['out_len'][i] for i in range(len(seqs))]):.3f}", flush=True)
+    out["merged_depths"] = merged
+    return out, ref
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_config1(psd, layout):
+    for seed in range(4):
+        run_mpfr(psd, workloads.WORKLOADS[1], seed, layout)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("case", [
+    dict(V=1000, K=4, gamma=4, B=4, dtype="fp32", m=4, T_draft=0.3),   # peaked drafts: contexts merge deeper
+    dict(V=777, K=3, gamma=3, B=3, dtype="bf16", m=0, T_draft=1.0),    # ragged, no window
+    dict(V=3, K=5, gamma=3, B=3, dtype="fp32", m=2, T_draft=1.0),      # more drafts than tokens
+    dict(V=1, K=2, gamma=2, B=1, dtype="fp32", m=1, T_draft=1.0),      # one token
+    dict(V=40000, K=8, gamma=3, B=2, dtype="bf16", m=3, T_draft=0.5),  # several level-4 nodes, nu up to 8
+    dict(V=20000, K=16, gamma=2, B=2, dtype="fp32", m=16, T_draft=2.0),  # nu = 16, long window
+])
+def test_mpfr_ragged_and_edge_shapes(psd, layout, case):
+    w = workloads.custom(case["V"], case["K"], case["gamma"], case["B"], dtype=case["dtype"], m=case["m"],
+                         tau=0.7, sigma=2.0, alpha=1.0, T_draft=case["T_draft"])
+    out, _ = run_mpfr(psd, w, 12, layout)
+    if case["T_draft"] < 0.5:  # peaked drafts: paths share contexts past depth 0 (multiplicities > 1)
+        assert out["merged_depths"] > 0
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_two_call_and_per_path(psd, layout):
+    w = workloads.custom(5000, 4, 4, 4, dtype="bf16", m=3, tau=0.5, sigma=2.0, alpha=1.0, T_draft=0.6)
+    blk = workloads.make_block(w, 3)
+    a, _ = run_mpfr(psd, w, 3, layout, blk=blk)
+    b, _ = run_mpfr(psd, w, 3, layout, mode="two_call", blk=blk)
+    for k in ("draft_tokens", "out_tokens", "out_len", "target_tokens"):
+        assert torch.equal(a[k], b[k]), k
+    run_mpfr(psd, w, 4, layout, target_rows=w.K)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_config2_full(psd, layout):
+    run_mpfr(psd, workloads.WORKLOADS[2], 2, layout)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_config3_all_sequences(psd, layout):
+    run_mpfr(psd, workloads.WORKLOADS[3], 3, layout, gen_device=DEV)
+
+
+def test_mpfr_detection_pivot_is_slot0(psd):
+    """Detection in MPFR mode scores the slot-0 clock: it equals the oracle's K = 1 score."""
+    w = workloads.WORKLOADS[3]
+    toks = workloads.uniform_tokens(8, 200, w.V, seed=4)
+    n0 = torch.full((8,), w.m, dtype=torch.int32)
+    for layout in LAYOUTS:
+        p = psd.make_params(w.key, w.V, w.K, w.m, dtype=w.torch_dtype, clocks=layout, mode=psd.PSD_MODE_MPFR)
+        score, count, per = psd.detect(p, toks.to(DEV), n0.to(DEV), per_token=True)
+        torch.cuda.synchronize()
+        for i in range(8):
+            S, M, _ = oracle.detect_sequence(w.key, w.m, 1, w.V, _np(toks)[i], w.m, layout)
+            assert int(count[i]) == M and abs(float(score[i]) - S) <= 1e-9 * abs(S)
