@@ -69,9 +69,7 @@ def write_counters(csv_path: str, out: str = COUNTERS_FILE) -> dict:
 
     vals = collections.defaultdict(list)
     clocks = "tree"
-    for r in csv.DictReader(open(csv_path)):
-        if "race_kernel<" not in r["Kernel_Name"]:
-            continue
+    for r in headline_race_rows(list(csv.DictReader(open(csv_path)))):
         clocks = "flat" if r["Kernel_Name"].split("race_kernel<")[1].split(">")[0].endswith("1") else "tree"
         vals[r["Counter_Name"]].append(float(r["Counter_Value"]))
     if not vals:
@@ -85,6 +83,15 @@ def write_counters(csv_path: str, out: str = COUNTERS_FILE) -> dict:
     return rec
 
 
+def headline_race_rows(rows):
+    """Race-kernel rows of the headline (distinct-drafter) step: those dispatched before
+    the first identical-drafter draft kernel (the bench's MPFR leg runs afterwards)."""
+    rows = sorted(rows, key=lambda r: int(r["Dispatch_Id"]))
+    first_mpfr = min((int(r["Dispatch_Id"]) for r in rows if "mpfr_draft_kernel" in r["Kernel_Name"]),
+                     default=1 << 62)
+    return [r for r in rows if "race_kernel<" in r["Kernel_Name"] and int(r["Dispatch_Id"]) < first_mpfr]
+
+
 def write_traffic(fetch_csv: str, write_csv: str, out: str = TRAFFIC_FILE) -> dict:
     """HBM bytes per launch of the race kernel from two rocprofv3 --pmc runs of
     `bench.py --pmc-copy-calibration` (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch).
@@ -95,7 +102,7 @@ def write_traffic(fetch_csv: str, write_csv: str, out: str = TRAFFIC_FILE) -> di
 
     def per_dispatch(path):
         rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
-        race = [r for r in rows if "race_kernel<" in r["Kernel_Name"]]
+        race = headline_race_rows(rows)
         last = int(race[-1]["Dispatch_Id"])
         copy = [r for r in rows if int(r["Dispatch_Id"]) > last and "copyBuffer" in r["Kernel_Name"]
                 and int(r["Grid_Size"]) >= 65536]
