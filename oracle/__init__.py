@@ -90,6 +90,9 @@ def _lib():
     lib.oracle_detect_term.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.c_int, i32p, ctypes.c_int64]
     lib.oracle_detect_term.restype = ctypes.c_double
+    lib.oracle_detect_clock.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                        ctypes.c_int, i32p, ctypes.c_int64]
+    lib.oracle_detect_clock.restype = ctypes.c_double
     lib.oracle_detect_sequence.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                            ctypes.c_int, i32p, ctypes.c_int, ctypes.c_int, i32p, f64p]
     lib.oracle_detect_sequence.restype = ctypes.c_double
@@ -498,4 +501,92 @@ def verify_block_mpfr(*, key, K, gamma, m, T_target, T_draft, prefix, start_pos,
         out["out_tokens"][b] = emitted
         out["out_len"][b] = len(emitted)
     return out
+
+
+# ---------------------------------------------------------------- further detection scores
+
+def detect_clocks(key: int, m: int, K: int, V: int, tokens, n0: int, layout: int = LAYOUT_TREE) -> np.ndarray:
+    """c_t = K min_j E_j[w_t] for every position (NaN before n0 and for tokens outside
+    [0, V)): the pivot is r_t = exp(-c_t), uniform under the null."""
+    tk, tp = _i32(tokens)
+    out = np.full(tk.size, np.nan)
+    for t in range(n0, tk.size):
+        out[t] = _lib().oracle_detect_clock(ctypes.c_uint64(key), m, K, V, layout, tp, t)
+    return out
+
+
+def li_params(delta: float):
+    """k_Delta = floor(1/(1-Delta)), q_Delta = 1 - k_Delta (1-Delta) (App. on Li et al.'s score).
+    1/(1-Delta) within 1e-12 (relative) of an integer counts as that integer, and then q = 0:
+    binary rounding (1/(1 - 0.9) = 10.000000000000002) must not leave a spurious q ~ 1e-16."""
+    x = 1.0 / (1.0 - delta)
+    k = math.floor(x + 1e-12 * x)
+    q = 1.0 - k * (1.0 - delta)
+    if q < 1e-12:
+        q = 0.0
+    return k, q
+
+
+def score_terms(c, delta: float, eps: float) -> dict:
+    """Per-token scores of the pivot r = exp(-c) (App. "Gumbel Watermark" and the two
+    following appendices): Aaronson's A = -log(1 - r), the U-score U = r, Li et al.'s
+    h*_{gum,Delta}(r) = log(k r^{Delta/(1-Delta)} + [q > 0] r^{(1-q)/q}) and Lattimore's
+    h_{PL,eps}(r) = min(eps^{-1/2}, (1 - r)^{-1/2}) - (2 - sqrt(eps))."""
+    c = np.asarray(c, np.float64)
+    r = np.exp(-c)
+    one_minus_r = -np.expm1(-c)
+    k, q = li_params(delta)
+    li = np.log(k * r ** (delta / (1.0 - delta)) + (r ** ((1.0 - q) / q) if q > 0 else 0.0))
+    pl = np.minimum(eps ** -0.5, one_minus_r ** -0.5) - (2.0 - math.sqrt(eps))
+    return {"A": -np.log(one_minus_r), "U": r, "Li": li, "PL": pl}
+
+
+def _null_log_mgf(kind: str, lam: float, delta: float, eps: float):
+    """(ln E[e^{lam h(U)}], E_lam[h]) under U ~ Unif(0, 1), by adaptive quadrature (the
+    tilted mean is the derivative of the log-MGF)."""
+    from scipy import integrate
+    if kind == "U":
+        if lam == 0.0:
+            return 0.0, 0.5
+        return math.log(math.expm1(lam) / lam), 1.0 / (-math.expm1(-lam)) - 1.0 / lam
+    if kind == "Li":
+        k, q = li_params(delta)
+        h = lambda u: math.log(k * u ** (delta / (1.0 - delta)) + (u ** ((1.0 - q) / q) if q > 0 else 0.0))
+        hmax = math.log(k + (1 if q > 0 else 0))
+        pts = None
+    else:
+        c0 = 2.0 - math.sqrt(eps)
+        h = lambda u: min(eps ** -0.5, (1.0 - u) ** -0.5) - c0
+        hmax = eps ** -0.5 - c0
+        pts = [1.0 - eps]
+    import warnings
+    kw = dict(epsabs=1e-15, epsrel=1e-12, limit=400)
+    if pts is not None and 0.0 < pts[0] < 1.0:
+        kw["points"] = pts
+    with warnings.catch_warnings():
+        warnings.simplefilter("ignore", integrate.IntegrationWarning)
+        z = integrate.quad(lambda u: math.exp(lam * (h(u) - hmax)), 0.0, 1.0, **kw)[0]
+        zh = integrate.quad(lambda u: h(u) * math.exp(lam * (h(u) - hmax)), 0.0, 1.0, **kw)[0]
+    return lam * hmax + math.log(z), zh / z
+
+
+def chernoff_log_p(kind: str, S: float, M: int, delta: float = 0.5, eps: float = 0.01) -> float:
+    """Chernoff bound on the null tail of a sum of M iid per-token scores:
+    ln p <= min_{lam >= 0} M ln E[e^{lam h(U)}] - lam S (App. "Gumbel Watermark" for the
+    U-score; the same construction for Li et al.'s and Lattimore's scores, whose null
+    p-values the paper leaves unstated).  0 when S is at most the null mean."""
+    from scipy import optimize
+    M = int(M)
+    if M <= 0 or not math.isfinite(S):
+        return float("nan") if (M < 0 or math.isnan(S)) else 0.0
+    mean0 = _null_log_mgf(kind, 0.0, delta, eps)[1]
+    if S <= M * mean0:
+        return 0.0
+    dphi = lambda lam: M * _null_log_mgf(kind, lam, delta, eps)[1] - S
+    hi = 1.0
+    while dphi(hi) < 0.0 and hi < 1e4:
+        hi *= 2.0
+    lam = optimize.brentq(dphi, 0.0, min(hi, 1e4), xtol=1e-14, rtol=1e-14, maxiter=400) if dphi(min(hi, 1e4)) > 0 \
+        else min(hi, 1e4)
+    return min(0.0, M * _null_log_mgf(kind, lam, delta, eps)[0] - lam * S)
 

@@ -375,6 +375,28 @@ double oracle_detect_term(uint64_t key, int m, int K, int V, int layout, const i
     return -log(-expm1(-c));
 }
 
+/* The target's clock of the observed token, c_t = K * min_{j<K} E_j[w_t] (Exp(1)
+ * under the null), whose pivot is r_t = exp(-c_t): every detection score below is
+ * a function of it.  NaN for a token outside [0, V). */
+double oracle_detect_clock(uint64_t key, int m, int K, int V, int layout, const int32_t *tokens, int64_t t) {
+    int32_t win[64];
+    if (m > 64) return NAN;
+    for (int i = 0; i < m; i++) {
+        int64_t idx = t - m + i;
+        win[i] = idx >= 0 ? tokens[idx] : -1;
+    }
+    int32_t w = tokens[t];
+    if (w < 0 || w >= V) return NAN;
+    uint32_t kappa[2];
+    oracle_context_key(key, t, win, m, kappa);
+    double cmin = INFINITY;
+    for (int j = 0; j < K; j++) {
+        double e = oracle_clock(kappa, j, V, layout, w);
+        if (e < cmin) cmin = e;
+    }
+    return (double)K * cmin;
+}
+
 /* Score one sequence: S = sum over t in [n0, n) of A_t (in t order), count of
  * scored tokens; per_token (nullable) receives every A_t (NaN when skipped). */
 double oracle_detect_sequence(uint64_t key, int m, int K, int V, int layout, const int32_t *tokens,
