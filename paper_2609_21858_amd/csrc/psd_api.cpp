@@ -333,6 +333,8 @@ psd_status psd_detect(const psd_params* params, int32_t n_seq, int32_t seq_len, 
     if (n_seq > 0 && (!tokens || !n0 || !out_score || !out_count))
         return fail(PSD_E_ARG, "tokens / n0 / out_score / out_count is NULL");
     psd::DetectArgs a;
+    memset(&a, 0, sizeof a);
+    a.row_stride = seq_len;
     a.tokens = tokens;
     a.n0 = n0;
     a.out_score = out_score;
@@ -347,6 +349,91 @@ psd_status psd_detect(const psd_params* params, int32_t n_seq, int32_t seq_len, 
     a.m = params->ctx_window;
     hipError_t e = psd::launch_detect(a, params->clocks, stream);
     if (e != hipSuccess) return hip_fail(e, "detect kernel launch");
+    return PSD_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Li et al.'s k_Delta, q_Delta: 1/(1 - Delta) within 1e-12 (relative) of an integer counts
+// as that integer, and then q = 0 (binary rounding must not leave q ~ 1e-16).
+psd_status score_params(const psd_score_params* sp, double& lnk, double& a, double& b, int& qpos, double& cap,
+                        double& c0) {
+    if (!sp) return fail(PSD_E_ARG, "score params is NULL");
+    if (!(sp->li_delta > 0.0 && sp->li_delta < 1.0)) return fail(PSD_E_ARG, "li_delta must be in (0, 1)");
+    if (!(sp->pl_eps > 0.0 && sp->pl_eps <= 1.0)) return fail(PSD_E_ARG, "pl_eps must be in (0, 1]");
+    const double d = sp->li_delta, x = 1.0 / (1.0 - d);
+    const double k = floor(x + 1e-12 * x);
+    double q = 1.0 - k * (1.0 - d);
+    if (q < 1e-12) q = 0.0;
+    lnk = log(k);
+    a = d / (1.0 - d);
+    b = q > 0.0 ? (1.0 - q) / q : 0.0;
+    qpos = q > 0.0;
+    cap = 1.0 / sqrt(sp->pl_eps);
+    c0 = 2.0 - sqrt(sp->pl_eps);
+    return PSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+psd_status psd_detect_scores(const psd_params* params, const psd_score_params* sp, int32_t n_seq, int32_t seq_len,
+                             int32_t row_stride, const int32_t* tokens, const int32_t* n0, double* out_scores,
+                             int32_t* out_count, hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    if (n_seq < 0 || seq_len < 0) return fail(PSD_E_ARG, "negative n_seq / seq_len");
+    if (row_stride < seq_len) return fail(PSD_E_ARG, "row_stride %d < seq_len %d", row_stride, seq_len);
+    if (n_seq > 0 && (!tokens || !n0 || !out_scores || !out_count))
+        return fail(PSD_E_ARG, "tokens / n0 / out_scores / out_count is NULL");
+    psd::DetectArgs a;
+    memset(&a, 0, sizeof a);
+    if ((st = score_params(sp, a.li_lnk, a.li_a, a.li_b, a.li_q, a.pl_cap, a.pl_c0)) != PSD_OK) return st;
+    a.tokens = tokens;
+    a.n0 = n0;
+    a.out_score = out_scores;
+    a.out_count = out_count;
+    a.key = params->key;
+    a.n_seq = n_seq;
+    a.seq_len = seq_len;
+    a.row_stride = row_stride;
+    a.V = params->vocab;
+    a.K = params->mode == PSD_MODE_MPFR ? 1 : params->num_drafts;
+    a.m = params->ctx_window;
+    a.multi = 1;
+    hipError_t e = psd::launch_detect(a, params->clocks, stream);
+    if (e != hipSuccess) return hip_fail(e, "detect kernel launch");
+    return PSD_OK;
+}
+
+psd_status psd_detect_scores_pvalue(const psd_score_params* sp, int32_t n_seq, const double* scores,
+                                    const int32_t* count, double* out_log_p, hipStream_t stream) {
+    psd::ScorePvalueArgs a;
+    memset(&a, 0, sizeof a);
+    psd_status st = score_params(sp, a.li_lnk, a.li_a, a.li_b, a.li_q, a.pl_cap, a.pl_c0);
+    if (st != PSD_OK) return st;
+    if (n_seq < 0) return fail(PSD_E_ARG, "n_seq < 0");
+    if (n_seq > 0 && (!scores || !count || !out_log_p)) return fail(PSD_E_ARG, "scores / count / out_log_p is NULL");
+    a.scores = scores;
+    a.count = count;
+    a.out_log_p = out_log_p;
+    a.n = n_seq;
+    a.pl_eps = sp->pl_eps;
+    hipError_t e = psd::launch_score_pvalues(a, stream);
+    if (e != hipSuccess) return hip_fail(e, "score p-value kernel launch");
+    return PSD_OK;
+}
+
+psd_status psd_detection_rate(int32_t n, const double* log_p, int32_t stride, double alpha, int32_t* out_count,
+                              hipStream_t stream) {
+    if (n < 0 || stride < 1) return fail(PSD_E_ARG, "n < 0 or stride < 1");
+    if (!(alpha > 0.0 && alpha <= 1.0)) return fail(PSD_E_ARG, "alpha must be in (0, 1]");
+    if (!out_count || (n > 0 && !log_p)) return fail(PSD_E_ARG, "log_p / out_count is NULL");
+    hipError_t e = psd::launch_detection_rate(n, log_p, stride, log(alpha), out_count, stream);
+    if (e != hipSuccess) return hip_fail(e, "detection rate kernel launch");
     return PSD_OK;
 }
 

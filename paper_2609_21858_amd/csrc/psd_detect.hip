@@ -27,15 +27,31 @@ namespace {
 constexpr int kDetBlock = 1024;  // threads per detection workgroup
 constexpr int kDetParts = 2;     // lanes per scored token (adjacent), each taking every other slot
 
-template <int LAYOUT>
+// The further per-token scores of a pivot r = e^{-c}: the U-score r, Li et al.'s
+// h*_{gum,Delta}(r) = log(k r^{Delta/(1-Delta)} + [q > 0] r^{(1-q)/q}) in log-sum-exp
+// form, and Lattimore's min(eps^{-1/2}, (1 - r)^{-1/2}) - (2 - sqrt(eps)).
+__device__ __forceinline__ double li_term(const DetectArgs& a, double c) {
+    const double t1 = a.li_lnk - a.li_a * c;
+    if (!a.li_q) return t1;
+    const double t2 = -a.li_b * c;
+    return fmax(t1, t2) + log1p(exp(-fabs(t1 - t2)));
+}
+__device__ __forceinline__ double pl_term(const DetectArgs& a, double c) {
+    return fmin(a.pl_cap, 1.0 / sqrt(-expm1(-c))) - a.pl_c0;
+}
+
+template <int LAYOUT, bool MULTI>
 __global__ __launch_bounds__(kDetBlock) void detect_kernel(DetectArgs a) {
-    __shared__ double part[kDetBlock / 64];
+    constexpr int NS = MULTI ? 4 : 1;
+    __shared__ double part[NS][kDetBlock / 64];
     __shared__ int cnt[kDetBlock / 64];
     const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
     const int sub = tid % kDetParts;
-    const int32_t* toks = a.tokens + (size_t)i * a.seq_len;
+    const int32_t* toks = a.tokens + (size_t)i * a.row_stride;
     const int n0 = max(0, a.n0[i]);
-    double acc = 0.0;
+    double acc[NS];
+#pragma unroll
+    for (int q = 0; q < NS; ++q) acc[q] = 0.0;
     int c = 0;
     for (int t0 = 0; t0 < a.seq_len; t0 += kDetBlock / kDetParts) {
         // uniform trip count: both lanes of a token reach the shuffle
@@ -87,8 +103,14 @@ __global__ __launch_bounds__(kDetBlock) void detect_kernel(DetectArgs a) {
         cmin = fmin(cmin, __shfl_xor(cmin, 1));
         if (sub == 0 && t < a.seq_len) {
             if (scored) {
-                const double A = -log(-expm1(-(double)a.K * cmin));
-                acc += A;
+                const double cc = (double)a.K * cmin;  // the target's clock of w_t; pivot e^{-cc}
+                const double A = -log(-expm1(-cc));
+                acc[0] += A;
+                if constexpr (MULTI) {
+                    acc[1] += exp(-cc);
+                    acc[2] += li_term(a, cc);
+                    acc[3] += pl_term(a, cc);
+                }
                 ++c;
                 if (a.out_per_token) a.out_per_token[(size_t)i * a.seq_len + t] = (float)A;
             } else if (a.out_per_token) {
@@ -99,22 +121,24 @@ __global__ __launch_bounds__(kDetBlock) void detect_kernel(DetectArgs a) {
     // fixed-order reduction: within each wave, then over the waves
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
-        acc += __shfl_xor(acc, off);
+#pragma unroll
+        for (int q = 0; q < NS; ++q) acc[q] += __shfl_xor(acc[q], off);
         c += __shfl_xor(c, off);
     }
     if (lane == 0) {
-        part[tid >> 6] = acc;
+#pragma unroll
+        for (int q = 0; q < NS; ++q) part[q][tid >> 6] = acc[q];
         cnt[tid >> 6] = c;
     }
     __syncthreads();
-    if (tid == 0) {
+    if (tid < NS) {
         double s = 0.0;
+        for (int w = 0; w < kDetBlock / 64; ++w) s += part[tid][w];
+        a.out_score[(size_t)i * NS + tid] = s;
+    }
+    if (tid == 0) {
         int n = 0;
-        for (int w = 0; w < kDetBlock / 64; ++w) {
-            s += part[w];
-            n += cnt[w];
-        }
-        a.out_score[i] = s;
+        for (int w = 0; w < kDetBlock / 64; ++w) n += cnt[w];
         a.out_count[i] = n;
     }
 }
@@ -209,7 +233,9 @@ __device__ double log_tail_sum(double S, int M, bool series, bool& ok) {
             ok = true;
             break;
         }
-        const double rs = mx + log(wave_sum_f64(lc == -INFINITY ? 0.0 : exp(lc - mx)));
+        // (lane 0's sum for every lane: the butterfly's rounding may differ per lane, and
+        // the stopping test below must be uniform)
+        const double rs = mx + log(__shfl(wave_sum_f64(lc == -INFINITY ? 0.0 : exp(lc - mx)), 0));
         total = total == -INFINITY ? rs : fmax(total, rs) + log1p(exp(-fabs(total - rs)));
         // this round's last term (lane 63; -inf if its chunk ran past the last term)
         const double last = __shfl(j == kTailChunk ? lt + log(t) : -INFINITY, 63);
@@ -221,13 +247,8 @@ __device__ double log_tail_sum(double S, int M, bool series, bool& ok) {
     return total;
 }
 
-// One wavefront per sequence (four per workgroup): ln p_A and ANLPPT_A of (S_A, M).
-__global__ __launch_bounds__(256) void pvalue_kernel(int n, const double* score, const int32_t* count,
-                                                      double* out_log_p, double* out_anlppt) {
-    const int i = (int)(blockIdx.x * 4u + (threadIdx.x >> 6));
-    if (i >= n) return;  // uniform per wavefront
-    const double S = score[i];
-    const int M = count[i];
+// ln p_A = ln Q(M, S) of one (S_A, M), by a whole wavefront.
+__device__ double gamma_tail_log_p(double S, int M) {
     double lp;
     if (M < 0 || isnan(S)) {
         lp = NAN;
@@ -243,9 +264,193 @@ __global__ __launch_bounds__(256) void pvalue_kernel(int n, const double* score,
         lp = series ? log1p(-exp(-S + a * log(S) - lgamma(a + 1.0) + ls)) : ls;
         lp = ok ? fmin(lp, 0.0) : NAN;  // a probability: rounding above ln 1 is clamped
     }
+    return lp;
+}
+
+// One wavefront per sequence (four per workgroup): ln p_A and ANLPPT_A of (S_A, M).
+__global__ __launch_bounds__(256) void pvalue_kernel(int n, const double* score, const int32_t* count,
+                                                      double* out_log_p, double* out_anlppt) {
+    const int i = (int)(blockIdx.x * 4u + (threadIdx.x >> 6));
+    if (i >= n) return;  // uniform per wavefront
+    const double S = score[i];
+    const int M = count[i];
+    const double lp = gamma_tail_log_p(S, M);
     if ((threadIdx.x & 63) == 0) {
         out_log_p[i] = lp;
         if (out_anlppt) out_anlppt[i] = M > 0 ? -lp / (double)M : NAN;
+    }
+}
+
+// ---- Chernoff bounds of the U-score and of Li et al.'s and Lattimore's scores:
+// ln p <= min_{lam >= 0} M ln Phi(lam) - lam S, Phi(lam) = E[e^{lam h(U)}], U ~ Unif(0, 1)
+// (App. "Gumbel Watermark" gives it for the U-score, Phi = (e^lam - 1) / lam).  The
+// objective is convex with derivative M E_lam[h] - S (E_lam the tilted mean), so lam is
+// found by bisection on that derivative.  Li and PL: Phi by composite 8-point
+// Gauss-Legendre in the log domain, enough panels that each spans at most about one
+// unit of the integrand's exponential rate:
+//  * Li, with u = e^{-s}: Phi = int_0^inf e^{-s + lam L(s)} ds, L(s) = h(e^{-s}) =
+//    logsumexp(ln k - a s, [q > 0] (-b s)); cut at s = 60 (the rest is below e^-59
+//    of Phi), split where the faster of the two exponentials has died out;
+//  * PL, with w = (1 - u)^{-1/2} on [1, eps^{-1/2}]: Phi = int 2 w^-3 e^{lam (w - c0)}
+//    dw + eps e^{lam (eps^{-1/2} - c0)} (the truncated mass).
+// 8-point Gauss-Legendre rule on [-1, 1] (Abramowitz & Stegun, Table 25.4).
+__constant__ double kGLx[4] = {0.1834346424956498049394761, 0.5255324099163289858177390,
+                               0.7966664774136267395915539, 0.9602898564975362316835609};
+__constant__ double kGLw[4] = {0.3626837833783619829651504, 0.3137066458778872873379622,
+                               0.2223810344533744705443560, 0.1012285362903762591525314};
+
+// Online log-sum-exp of terms e^tau and of h e^tau.
+struct LseAcc {
+    double m, s, sh;
+};
+__device__ __forceinline__ void lse_add(LseAcc& A, double tau, double h) {
+    if (tau == -INFINITY) return;
+    if (tau > A.m) {
+        const double f = exp(A.m - tau);
+        A.s = A.s * f + 1.0;
+        A.sh = A.sh * f + h;
+        A.m = tau;
+    } else {
+        const double e = exp(tau - A.m);
+        A.s += e;
+        A.sh += h * e;
+    }
+}
+__device__ __forceinline__ LseAcc lse_merge(LseAcc A, LseAcc B) {
+    if (B.m == -INFINITY) return A;
+    if (A.m == -INFINITY) return B;
+    const double m = fmax(A.m, B.m), fa = exp(A.m - m), fb = exp(B.m - m);
+    return LseAcc{m, A.s * fa + B.s * fb, A.sh * fa + B.sh * fb};
+}
+__device__ __forceinline__ LseAcc wave_lse(LseAcc A) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const LseAcc B{__shfl_xor(A.m, o), __shfl_xor(A.s, o), __shfl_xor(A.sh, o)};
+        A = lse_merge(A, B);
+    }
+    return A;
+}
+
+__device__ __forceinline__ double li_L(const ScorePvalueArgs& a, double s) {
+    const double t1 = a.li_lnk - a.li_a * s;
+    if (!a.li_q) return t1;
+    const double t2 = -a.li_b * s;
+    return fmax(t1, t2) + log1p(exp(-fabs(t1 - t2)));
+}
+
+// Composite Gauss-Legendre over [x0, x1] in n panels of the terms
+// e^{ln(weight * jacobian) + exponent} (kind 2: Li in s, kind 3: PL in w), into A.
+__device__ void gl_panels(const ScorePvalueArgs& a, int kind, double lam, double x0, double x1, int n, LseAcc& A) {
+    const int lane = threadIdx.x & 63;
+    const double w = (x1 - x0) / (double)n;
+    for (int p = lane; p < n; p += 64) {
+        const double mid = x0 + ((double)p + 0.5) * w, half = 0.5 * w;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const double x = mid + (j < 4 ? -kGLx[j] : kGLx[j - 4]) * half;
+            const double lw = log(kGLw[j & 3] * half);
+            double tau, h;
+            if (kind == 2) {
+                h = li_L(a, x);
+                tau = lw - x + lam * h;
+            } else {
+                h = x - a.pl_c0;
+                tau = lw + 0.69314718055994531 - 3.0 * log(x) + lam * h;
+            }
+            lse_add(A, tau, h);
+        }
+    }
+}
+
+// ln Phi(lam) and the tilted mean E_lam[h] of score kind 1 (U), 2 (Li), 3 (PL); whole wave.
+__device__ void tilt(const ScorePvalueArgs& a, int kind, double lam, double& ln_phi, double& mean) {
+    if (kind == 1) {
+        if (lam < 1e-8) {
+            ln_phi = 0.5 * lam;
+            mean = 0.5 + lam / 12.0;
+        } else {
+            ln_phi = lam + log(-expm1(-lam)) - log(lam);
+            mean = 1.0 / (-expm1(-lam)) - 1.0 / lam;
+        }
+        return;
+    }
+    LseAcc A{-INFINITY, 0.0, 0.0};
+    constexpr int kMaxPanels = 16384;
+    if (kind == 2) {
+        const double cf = a.li_q ? fmax(a.li_a, a.li_b) : a.li_a;
+        const double cs = a.li_q ? fmin(a.li_a, a.li_b) : a.li_a;
+        const double s1 = cf > cs ? fmin(60.0, (fabs(a.li_lnk) + 40.0) / (cf - cs)) : 0.0;
+        const int n1 = (int)fmin((double)kMaxPanels, ceil(s1 * (1.0 + lam * cf)) + 4.0);
+        const int n2 = (int)fmin((double)kMaxPanels, ceil((60.0 - s1) * (1.0 + lam * cs)) + 4.0);
+        if (s1 > 0.0) gl_panels(a, 2, lam, 0.0, s1, n1, A);
+        gl_panels(a, 2, lam, s1, 60.0, n2, A);
+    } else {
+        const double W = a.pl_cap;
+        if (W > 1.0) {
+            const int n = (int)fmin((double)kMaxPanels, ceil((W - 1.0) * (lam + 3.0)) + 4.0);
+            gl_panels(a, 3, lam, 1.0, W, n, A);
+        }
+        if ((threadIdx.x & 63) == 0) lse_add(A, log(a.pl_eps) + lam * (W - a.pl_c0), W - a.pl_c0);
+    }
+    A = wave_lse(A);
+    // the butterfly combines the lanes' terms in a different order on each lane, so
+    // results can differ in the last bit: every lane takes lane 0's, which keeps the
+    // caller's bisection decisions (and with them every later shuffle) uniform
+    ln_phi = __shfl(A.m + log(A.s), 0);
+    mean = __shfl(A.sh / A.s, 0);
+}
+
+__device__ double chernoff_log_p(const ScorePvalueArgs& a, int kind, double S, int M) {
+    if (M < 0 || isnan(S)) return NAN;
+    if (M == 0) return 0.0;
+    double lp0, mean0;
+    tilt(a, kind, 0.0, lp0, mean0);
+    if (S <= (double)M * mean0) return 0.0;
+    double lo = 0.0, hi = 1.0, lnphi, mean;
+    for (;;) {  // bracket the root of the derivative (doubling, at most 14 steps)
+        tilt(a, kind, hi, lnphi, mean);
+        if ((double)M * mean - S > 0.0 || hi >= 1e4) break;
+        lo = hi;
+        hi *= 2.0;
+    }
+    for (int it = 0; it < 100 && hi - lo > 1e-13 * hi; ++it) {
+        const double mid = 0.5 * (lo + hi);
+        tilt(a, kind, mid, lnphi, mean);
+        if ((double)M * mean - S < 0.0)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    const double lam = 0.5 * (lo + hi);
+    tilt(a, kind, lam, lnphi, mean);
+    return fmin(0.0, (double)M * lnphi - lam * S);
+}
+
+// One wavefront per (sequence, score): ln p_A (exact Gamma tail) or a Chernoff bound.
+__global__ __launch_bounds__(256) void score_pvalue_kernel(ScorePvalueArgs a) {
+    const int item = (int)(blockIdx.x * 4u + (threadIdx.x >> 6));
+    if (item >= 4 * a.n) return;  // uniform per wavefront
+    const int i = item >> 2, kind = item & 3;
+    const double S = a.scores[(size_t)i * 4 + kind];
+    const int M = a.count[i];
+    const double lp = kind == 0 ? gamma_tail_log_p(S, M) : chernoff_log_p(a, kind, S, M);
+    if ((threadIdx.x & 63) == 0) a.out_log_p[(size_t)i * 4 + kind] = lp;
+}
+
+// Number of log p-values (stride apart) at or below ln alpha (NaN: not detected).
+__global__ __launch_bounds__(1024) void detection_rate_kernel(int n, const double* log_p, int stride,
+                                                               double log_alpha, int32_t* out) {
+    __shared__ int part[16];
+    int c = 0;
+    for (int i = threadIdx.x; i < n; i += 1024) c += log_p[(size_t)i * stride] <= log_alpha ? 1 : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int t = 0;
+        for (int w = 0; w < 16; ++w) t += part[w];
+        *out = t;
     }
 }
 
@@ -260,10 +465,29 @@ inline unsigned blocks_for(long n, int per) { return (unsigned)((n + per - 1) / 
 
 hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream) {
     if (a.n_seq <= 0) return hipSuccess;
-    if (layout == 0)
-        hipLaunchKernelGGL(detect_kernel<0>, dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
-    else
-        hipLaunchKernelGGL(detect_kernel<1>, dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
+    if (a.multi) {
+        if (layout == 0)
+            hipLaunchKernelGGL((detect_kernel<0, true>), dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
+        else
+            hipLaunchKernelGGL((detect_kernel<1, true>), dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
+    } else {
+        if (layout == 0)
+            hipLaunchKernelGGL((detect_kernel<0, false>), dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
+        else
+            hipLaunchKernelGGL((detect_kernel<1, false>), dim3(a.n_seq), dim3(kDetBlock), 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_score_pvalues(const ScorePvalueArgs& a, hipStream_t stream) {
+    if (a.n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(score_pvalue_kernel, dim3(blocks_for((long)a.n * 4, 4)), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_detection_rate(int n, const double* log_p, int stride, double log_alpha, int32_t* out_count,
+                                 hipStream_t stream) {
+    hipLaunchKernelGGL(detection_rate_kernel, dim3(1), dim3(1024), 0, stream, n, log_p, stride, log_alpha, out_count);
     return hipGetLastError();
 }
 

@@ -8,14 +8,34 @@
 namespace psd {
 
 struct DetectArgs {
-    const int32_t* tokens;  // [n_seq][seq_len]
+    const int32_t* tokens;  // [n_seq][row_stride], positions [0, seq_len) of each row scored
     const int32_t* n0;      // [n_seq]
-    double* out_score;      // [n_seq]
+    double* out_score;      // [n_seq] (Aaronson's S_A only) or [n_seq][4] (every score)
     int32_t* out_count;     // [n_seq]
     float* out_per_token;   // nullable [n_seq][seq_len]
     uint64_t key;
     int n_seq, seq_len, V, K, m;
+    int row_stride;
+    // further scores (App. on Li et al.'s and Lattimore's scores), with multi = 1
+    int multi;
+    double li_lnk, li_a, li_b;  // ln k_Delta, Delta / (1 - Delta), (1 - q) / q
+    int li_q;                   // q_Delta > 0
+    double pl_cap, pl_c0;       // eps^{-1/2}, 2 - sqrt(eps)
 };
+
+// Null-tail p-values of the four detection scores of each sequence.
+struct ScorePvalueArgs {
+    const double* scores;   // [n][4]: S_A, S_U, S_Li, S_PL
+    const int32_t* count;   // [n]
+    double* out_log_p;      // [n][4]
+    int n;
+    double li_lnk, li_a, li_b;
+    int li_q;
+    double pl_cap, pl_c0, pl_eps;
+};
+hipError_t launch_score_pvalues(const ScorePvalueArgs& a, hipStream_t stream);
+hipError_t launch_detection_rate(int n, const double* log_p, int stride, double log_alpha, int32_t* out_count,
+                                 hipStream_t stream);
 
 // One depth of drafting with identical drafters (multi-sample PFR), one workgroup
 // per draft row (b, k) of depth s.

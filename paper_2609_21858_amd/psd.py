@@ -75,6 +75,9 @@ def _load():
         "psd_context_keys": ([P, i32, vp, vp, vp, vp], i32),
         "psd_clock_values": ([P, i32, vp, vp, vp, vp, vp], i32),
         "psd_set_spin_limit": ([ctypes.c_uint32], None),
+        "psd_detect_scores": ([P, vp, i32, i32, i32, vp, vp, vp, vp, vp], i32),
+        "psd_detect_scores_pvalue": ([vp, i32, vp, vp, vp, vp], i32),
+        "psd_detection_rate": ([i32, vp, i32, ctypes.c_double, vp, vp], i32),
     }
     for name, (args, res) in sigs.items():
         f = getattr(lib, name)
@@ -86,7 +89,8 @@ def _load():
 _lib = _load()
 EXPORTS = ("psd_abi_version", "psd_last_error", "psd_workspace_bytes", "psd_workspace_clear",
            "psd_workspace_errors", "psd_draft", "psd_verify", "psd_verify_static", "psd_detect", "psd_detect_pvalue", "psd_philox",
-           "psd_context_keys", "psd_clock_values", "psd_set_spin_limit")
+           "psd_context_keys", "psd_clock_values", "psd_set_spin_limit", "psd_detect_scores",
+           "psd_detect_scores_pvalue", "psd_detection_rate")
 
 
 def lib():
@@ -224,6 +228,43 @@ def detect(params: Params, tokens, n0, per_token: bool = False, stream=None):
     _check(_lib.psd_detect(ctypes.byref(params), n_seq, seq_len, _ptr(tokens), _ptr(n0), _ptr(score), _ptr(count),
                            _ptr(per), _stream(stream)))
     return score, count, per
+
+
+class ScoreParams(ctypes.Structure):
+    _fields_ = [("li_delta", ctypes.c_double), ("pl_eps", ctypes.c_double)]
+
+
+def detect_scores(params: Params, tokens, n0, li_delta: float, pl_eps: float, seq_len: int = None, stream=None):
+    """psd_detect_scores -> (scores f64 [n_seq][4] = S_A, S_U, S_Li, S_PL; count i32 [n_seq]).
+    seq_len < tokens.shape[1] scores that prefix of every row."""
+    n_seq, stride = int(tokens.shape[0]), int(tokens.shape[1])
+    seq_len = stride if seq_len is None else int(seq_len)
+    sp = ScoreParams(li_delta, pl_eps)
+    scores = torch.empty((n_seq, 4), dtype=torch.float64, device=tokens.device)
+    count = torch.empty((n_seq,), dtype=torch.int32, device=tokens.device)
+    _check(_lib.psd_detect_scores(ctypes.byref(params), ctypes.byref(sp), n_seq, seq_len, stride, _ptr(tokens),
+                                  _ptr(n0), _ptr(scores), _ptr(count), _stream(stream)))
+    return scores, count
+
+
+def detect_scores_pvalue(scores, count, li_delta: float, pl_eps: float, stream=None):
+    """psd_detect_scores_pvalue -> ln p f64 [n_seq][4] (A exact; U, Li, PL Chernoff bounds)."""
+    n = int(scores.shape[0])
+    sp = ScoreParams(li_delta, pl_eps)
+    out = torch.empty((n, 4), dtype=torch.float64, device=scores.device)
+    _check(_lib.psd_detect_scores_pvalue(ctypes.byref(sp), n, _ptr(scores), _ptr(count), _ptr(out),
+                                         _stream(stream)))
+    return out
+
+
+def detection_rate(log_p, alpha: float, stream=None):
+    """psd_detection_rate over a column of log p-values ([n] or [n][c] with one column
+    selected by the caller's view) -> int32 [1] count with ln p <= ln alpha."""
+    n = int(log_p.shape[0])
+    stride = int(log_p.stride(0))
+    out = torch.empty((1,), dtype=torch.int32, device=log_p.device)
+    _check(_lib.psd_detection_rate(n, _ptr(log_p), stride, alpha, _ptr(out), _stream(stream)))
+    return out
 
 
 def detect_pvalue(score, count, stream=None):

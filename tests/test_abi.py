@@ -133,3 +133,22 @@ def test_verify_static_rejects_before_launch(psd):
     assert psd.workspace_bytes(p, 64, 4) <= 32 << 20  # the headline block fits
     bad = psd.make_params(1, 0, 4, 4)
     assert L.psd_verify_static(ctypes.byref(bad), ctypes.byref(ok_blk), *args) == psd.PSD_E_ARG
+
+
+def test_detect_scores_reject_bad_args(psd):
+    p = psd.make_params(1, 1000, 2, 4)
+    L = psd.lib()
+    good = psd.ScoreParams(0.3, 0.05)
+    for bad in (psd.ScoreParams(0.0, 0.05), psd.ScoreParams(1.0, 0.05), psd.ScoreParams(0.3, 0.0),
+                psd.ScoreParams(0.3, 1.5), psd.ScoreParams(float("nan"), 0.05)):
+        assert L.psd_detect_scores(ctypes.byref(p), ctypes.byref(bad), 2, 4, 4, FAKE, FAKE, FAKE, FAKE,
+                                   None) == psd.PSD_E_ARG
+        assert L.psd_detect_scores_pvalue(ctypes.byref(bad), 2, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_detect_scores(ctypes.byref(p), ctypes.byref(good), 2, 8, 4, FAKE, FAKE, FAKE, FAKE,
+                               None) == psd.PSD_E_ARG  # row stride shorter than the scored length
+    assert L.psd_detect_scores(ctypes.byref(p), None, 2, 4, 4, FAKE, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_detect_scores(ctypes.byref(p), ctypes.byref(good), 2, 4, 4, None, FAKE, FAKE, FAKE,
+                               None) == psd.PSD_E_ARG
+    assert L.psd_detection_rate(3, FAKE, 0, 0.01, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_detection_rate(3, FAKE, 1, 0.0, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_detection_rate(3, None, 1, 0.01, FAKE, None) == psd.PSD_E_ARG

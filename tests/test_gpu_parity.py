@@ -477,6 +477,27 @@ def test_config5_generate_then_detect(psd, layout):
     assert np.all(z[:half] > 5.0), z[:half].min()
     assert np.all(np.abs(z[half:]) < 4.5), np.abs(z[half:]).max()
     assert np.all(_np(log_p)[:half] < math.log(1e-6)) and np.median(_np(log_p)[half:]) > math.log(0.05)
+    # every score (Aaronson, U, Li Delta = 0.3, PL eps = 0.05), TPR@1%FPR on the keyed half
+    # and the empirical FPR on the wrong-key half (App. "Drafter-substitution ablation")
+    delta, eps = 0.3, 0.05
+    sc4, ct4 = psd.detect_scores(p, toks, n0, delta, eps)
+    lp4 = psd.detect_scores_pvalue(sc4, ct4, delta, eps)
+    tpr = [int(psd.detection_rate(lp4[:half, q], 0.01)[0]) / half for q in range(4)]
+    fpr = [int(psd.detection_rate(lp4[half:, q], 0.01)[0]) / half for q in range(4)]
+    _sync()
+    sc4, lp4 = _np(sc4), _np(lp4)
+    assert np.allclose(sc4[:, 0], score, rtol=1e-12, atol=0.0)
+    for i in list(range(0, w.B, 37)):
+        c = oracle.detect_clocks(key, w.m, w.K, w.V, tk[i], w.m, layout)
+        terms = oracle.score_terms(c[~np.isnan(c)], delta, eps)
+        for q, kind in enumerate(("A", "U", "Li", "PL")):
+            assert abs(sc4[i, q] - terms[kind].sum()) <= SCORE_TOL * abs(terms[kind].sum()) + 1e-12, (i, kind)
+        for q, kind in enumerate(("U", "Li", "PL"), start=1):
+            ref = oracle.chernoff_log_p(kind, float(sc4[i, q]), n_pos, delta, eps)
+            assert abs(lp4[i, q] - ref) <= 1e-7 * abs(ref) + 1e-9, (i, kind, lp4[i, q], ref)
+    print(f"[detect] TPR@1%FPR A/U/Li/PL {tpr}  empirical FPR {fpr}", flush=True)
+    assert tpr[0] == 1.0 and all(t >= 0.9 for t in tpr)
+    assert all(f <= 0.06 for f in fpr)
 
 
 def _check_pvalues(score, count, log_p, anl):
