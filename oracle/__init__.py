@@ -590,3 +590,45 @@ def chernoff_log_p(kind: str, S: float, M: int, delta: float = 0.5, eps: float =
         else min(hi, 1e4)
     return min(0.0, M * _null_log_mgf(kind, lam, delta, eps)[0] - lam * S)
 
+
+# ---------------------------------------------------------------- logit processing before the race
+
+def truncation_mask(logits, T: float, top_k: int = 0, top_p: float = 1.0) -> np.ndarray:
+    """Tokens kept by top-k, then top-p, truncation (the paper's experiments race the
+    processed distribution P_k: temperature, top-k = 50, top-p; Alg. "Batched-target
+    direct-top-k MPFR speculative sampling").  Order: logit descending, ties to the
+    lowest index; top-k keeps the first min(k, #finite) (k = 0: all finite); top-p then
+    keeps the shortest prefix of those whose softmax mass (at T, over the top-k set)
+    reaches top_p.  Returns a boolean mask over the vocabulary."""
+    x = np.asarray(logits, np.float32)
+    finite = np.flatnonzero(x != -np.inf)
+    order = finite[np.lexsort((finite, -x[finite].astype(np.float64)))]  # by -x, then index
+    if top_k > 0:
+        order = order[:top_k]
+    if top_p < 1.0 and order.size:
+        z = x[order].astype(np.float64) / np.float64(np.float32(T))
+        p = np.exp(z - z.max())
+        p /= p.sum()
+        cum = np.cumsum(p)
+        n = int(np.searchsorted(cum, top_p, side="left")) + 1
+        order = order[:min(n, order.size)]
+    mask = np.zeros(x.size, bool)
+    mask[order] = True
+    return mask
+
+
+def truncate(logits, T: float, top_k: int = 0, top_p: float = 1.0) -> np.ndarray:
+    """The row with every token outside the kept set at -inf (probability 0)."""
+    x = np.array(logits, np.float32, copy=True)
+    if top_k > 0 or top_p < 1.0:
+        x[~truncation_mask(x, T, top_k, top_p)] = -np.inf
+    return x
+
+
+def truncate_block(arr, T: float, top_k: int, top_p: float):
+    """truncate() on every row (last axis) of a logits array."""
+    if top_k <= 0 and top_p >= 1.0:
+        return arr
+    flat = np.asarray(arr, np.float32).reshape(-1, arr.shape[-1])
+    return np.stack([truncate(r, T, top_k, top_p) for r in flat]).reshape(arr.shape)
+
