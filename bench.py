@@ -238,6 +238,44 @@ def mpfr_leg(psd, torch, w, sets, clocks_id, dev, launches=20):
             "mean_tau": float(outs[(launches - 1) % len(sets)]["out_len"].float().mean())}
 
 
+def topk_leg(psd, torch, w, sets, clocks_id, dev, mpfr=False, top_k=50, top_p=1.0, launches=20):
+    """The same block with every row truncated to its top_k logits (the paper's
+    experiments use top-k = 50): one selection launch over the draft rows and one over
+    the target rows, then the list races and the walk.  Algorithmic bytes: every row
+    read once, as in the untruncated step."""
+    params = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype, clocks=clocks_id,
+                             mode=psd.PSD_MODE_MPFR if mpfr else psd.PSD_MODE_HET, top_k=top_k, top_p=top_p)
+    ws = psd.new_workspace(params, w.B, w.gamma, dev)
+    status = torch.zeros((1,), dtype=torch.int32, device=dev)
+    outs = [dict(out_tokens=torch.empty((w.B, w.gamma + 1), dtype=torch.int32, device=dev),
+                 out_len=torch.empty((w.B,), dtype=torch.int32, device=dev)) for _ in sets]
+    dts = [torch.empty((w.B, w.K, w.gamma), dtype=torch.int32, device=dev) for _ in sets]
+
+    def step(i):
+        s = sets[i % len(sets)]
+        psd.verify(params, ws, s["prefix_tokens"], s["start_pos"], s["target_logits"], s["draft_logits"],
+                   dts[i % len(sets)], out=outs[i % len(sets)], status=status)
+
+    for i in range(3):
+        step(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(launches):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    if int(status[0]) or psd.workspace_errors(ws):
+        raise RuntimeError("top-k step reported errors")
+    ms = e0.elapsed_time(e1) / launches
+    nbytes = w.algorithmic_bytes()
+    return {"workload": w.name + (", identical drafters (MPFR)" if mpfr else "") + f", top-k {top_k}"
+            + (f", top-p {top_p}" if top_p < 1.0 else ""), "ms_per_step": ms,
+            "positions_per_s": w.B * w.gamma / (ms / 1e3), "achieved_gbps": nbytes / (ms / 1e3) / 1e9,
+            "frac_of_hbm_peak": nbytes / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS, "launches": launches,
+            "mean_tau": float(outs[(launches - 1) % len(sets)]["out_len"].float().mean())}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -349,6 +387,9 @@ def main():
         "wall_s": wall,
     }
     res["mpfr"] = mpfr_leg(psd, torch, w, sets, clocks_id, dev)
+    res["topk"] = [topk_leg(psd, torch, w, sets, clocks_id, dev),
+                   topk_leg(psd, torch, w, sets, clocks_id, dev, mpfr=True),
+                   topk_leg(psd, torch, w, sets, clocks_id, dev, top_p=0.9)]
     res["detect"] = detect_leg(psd, torch, clocks_id, dev)
     if not args.no_detect_100x:
         res["detect_100x"] = detect_leg(psd, torch, clocks_id, dev, launches=5, replicate=100)

@@ -47,7 +47,17 @@ psd_status check_params(const psd_params* p) {
     if (p->clocks != PSD_CLOCKS_TREE && p->clocks != PSD_CLOCKS_FLAT)
         return fail(PSD_E_ARG, "unknown clock layout %d", p->clocks);
     if (p->mode != PSD_MODE_HET && p->mode != PSD_MODE_MPFR) return fail(PSD_E_ARG, "unknown mode %d", p->mode);
+    if (p->top_k < 0 || p->top_k > PSD_MAX_TOP_K) return fail(PSD_E_ARG, "top_k %d outside [0, %d]", p->top_k, PSD_MAX_TOP_K);
+    if (!(p->top_p > 0.f && p->top_p <= 1.f)) return fail(PSD_E_ARG, "top_p must be in (0, 1]");
+    if (p->top_p < 1.f && p->top_k == 0) return fail(PSD_E_ARG, "top_p < 1 needs top_k in [1, %d]", PSD_MAX_TOP_K);
     return PSD_OK;
+}
+
+// Bytes a block of these parameters needs: the race kernel's workspace, plus the kept
+// lists of every row when logits are truncated.
+size_t workspace_need(const psd_params* p, int B, int gamma) {
+    const psd::WsLayout L = psd::ws_layout(B, p->num_drafts, gamma, p->vocab, p->dtype == PSD_BF16);
+    return p->top_k > 0 ? psd::topk_layout(L, p->top_k).total : L.total;
 }
 
 psd_status check_block(const psd_params* p, const psd_block* b) {
@@ -60,8 +70,9 @@ psd_status check_block(const psd_params* p, const psd_block* b) {
     const long items = (long)L.n_rows * L.nseg;
     if (items > 0x7FFFFFFFL) return fail(PSD_E_ARG, "block too large (%ld work items)", items);
     if (!b->workspace) return fail(PSD_E_WORKSPACE, "workspace is NULL");
-    if (b->workspace_bytes < L.total)
-        return fail(PSD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", b->workspace_bytes, L.total);
+    const size_t need = workspace_need(p, b->batch, b->gamma);
+    if (b->workspace_bytes < need)
+        return fail(PSD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", b->workspace_bytes, need);
     if (((uintptr_t)b->workspace & 255u) != 0) return fail(PSD_E_WORKSPACE, "workspace must be 256-byte aligned");
     return PSD_OK;
 }
@@ -167,6 +178,81 @@ psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_be
     return PSD_OK;
 }
 
+// Truncated logits: the kept list of every row of the call, then one workgroup per
+// sequence racing the lists (drafts of depths [s_begin, s_begin + s_count), then the
+// target rows when target_rows > 0, then the walk).
+psd_status run_topk(const psd_params* p, const psd_block* b, int32_t s_begin, int32_t s_count, int32_t target_rows,
+                    const void* target_logits, const void* draft_logits, int32_t* draft_tokens, int32_t* out_tokens,
+                    int32_t* out_len, float* target_lse, float* draft_lse, int32_t* target_tokens, hipStream_t stream) {
+    const bool bf16 = p->dtype == PSD_BF16;
+    const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, bf16);
+    const psd::TopkLayout T = psd::topk_layout(L, p->top_k);
+    unsigned char* ws = (unsigned char*)b->workspace;
+    const int K = p->num_drafts, G = b->gamma, B = b->batch;
+    psd::TopkSelectArgs s;
+    memset(&s, 0, sizeof s);
+    s.V = p->vocab;
+    s.top_k = p->top_k;
+    s.top_p = p->top_p;
+    s.cap = p->top_k;
+    s.list_tok = (int32_t*)(ws + T.tok);
+    s.list_val = (float*)(ws + T.val);
+    s.list_len = (int32_t*)(ws + T.len);
+    s.list_lse = (float*)(ws + T.lse);
+    s.radix_rows = (uint32_t*)(ws + L.ctrl) + psd::kCtrlTopkRadix;
+    int ns = 0;
+    if (draft_logits && s_count > 0) {
+        psd::TopkSegment& g = s.seg[ns++];
+        g.logits = draft_logits;
+        g.n_rows = B * K * s_count;
+        g.T = p->temp_draft;
+        g.row_id_base = s_begin;
+        g.group = s_count;
+        g.group_stride = G;
+        g.lse_out = draft_lse;
+        g.lse_index_base = s_begin;
+        g.lse_group_stride = G;
+    }
+    if (target_rows > 0) {
+        psd::TopkSegment& g = s.seg[ns++];
+        g.logits = target_logits;
+        g.n_rows = B * target_rows * (G + 1);
+        g.T = p->temp_target;
+        g.row_id_base = B * K * G;
+        g.lse_out = target_lse;
+    }
+    hipError_t e;
+    if ((e = psd::launch_topk_select(s, bf16, stream)) != hipSuccess) return hip_fail(e, "top-k select launch");
+    psd::TopkRaceArgs r;
+    memset(&r, 0, sizeof r);
+    r.prefix = b->prefix_tokens;
+    r.start_pos = b->start_pos;
+    r.draft_tokens = draft_tokens;
+    r.out_tokens = out_tokens;
+    r.out_len = out_len;
+    r.target_tokens = target_tokens;
+    r.list_tok = s.list_tok;
+    r.list_val = s.list_val;
+    r.list_len = s.list_len;
+    r.cap = p->top_k;
+    r.key = p->key;
+    r.V = p->vocab;
+    r.K = K;
+    r.m = p->ctx_window;
+    r.B = B;
+    r.gamma = G;
+    r.s_begin = s_begin;
+    r.s_count = draft_logits ? s_count : 0;
+    r.target_rows = target_rows;
+    r.mpfr = p->mode == PSD_MODE_MPFR;
+    r.T_target = p->temp_target;
+    r.T_draft = p->temp_draft;
+    if ((e = psd::launch_topk_race(r, p->clocks, stream)) != hipSuccess) return hip_fail(e, "top-k race launch");
+    if ((e = psd::launch_finish_status((uint32_t*)(ws + L.ctrl), b->status, stream)) != hipSuccess)
+        return hip_fail(e, "status kernel launch");
+    return PSD_OK;
+}
+
 psd_status run_race(const psd_params* p, psd::RaceArgs& a, hipStream_t stream) {
     const size_t es = p->dtype == PSD_BF16 ? 2 : 4;
     bool vec = ((size_t)p->vocab * es) % 16 == 0;
@@ -192,7 +278,8 @@ size_t psd_workspace_bytes(const psd_params* params, int32_t batch, int32_t gamm
         params->num_drafts > PSD_MAX_DRAFTS || batch < 1 || gamma < 1 || gamma > PSD_MAX_GAMMA ||
         (params->dtype != PSD_F32 && params->dtype != PSD_BF16))
         return 0;
-    return psd::ws_layout(batch, params->num_drafts, gamma, params->vocab, params->dtype == PSD_BF16).total;
+    if (params->top_k < 0 || params->top_k > PSD_MAX_TOP_K) return 0;
+    return workspace_need(params, batch, gamma);
 }
 
 psd_status psd_workspace_clear(void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -224,6 +311,9 @@ psd_status psd_draft(const psd_params* params, const psd_block* block, int32_t s
         return fail(PSD_E_ARG, "draft depths [%d, %d) outside [0, gamma=%d)", s_begin, s_begin + s_count, block->gamma);
     if (!draft_logits) return fail(PSD_E_ARG, "draft_logits is NULL");
     if (!draft_tokens) return fail(PSD_E_ARG, "draft_tokens is NULL");
+    if (params->top_k > 0)
+        return run_topk(params, block, s_begin, s_count, 0, nullptr, draft_logits, draft_tokens, nullptr, nullptr,
+                        nullptr, draft_lse, nullptr, stream);
     if (params->mode == PSD_MODE_MPFR) {
         if ((st = run_mpfr_drafts(params, block, s_begin, s_count, draft_logits, draft_tokens, draft_lse, stream)) != PSD_OK)
             return st;
@@ -260,6 +350,9 @@ psd_status verify_impl(const psd_params* params, const psd_block* block, int32_t
     if (!draft_tokens) return fail(PSD_E_ARG, "draft_tokens is NULL");
     if (!out_tokens || !out_len) return fail(PSD_E_ARG, "out_tokens / out_len is NULL");
     if (!draft_logits && draft_lse) return fail(PSD_E_ARG, "draft_lse requires draft_logits");
+    if (params->top_k > 0)
+        return run_topk(params, block, 0, block->gamma, target_rows, target_logits, draft_logits, draft_tokens,
+                        out_tokens, out_len, target_lse, draft_lse, target_tokens, stream);
     if (params->mode == PSD_MODE_MPFR && draft_logits) {
         // identical drafters: the context tree is drafted depth by depth first, then the
         // target rows race slot 0 in the fused kernel with the drafts as input
@@ -309,8 +402,7 @@ psd_status psd_verify_static(const psd_params* params, const psd_block* block, i
         return fail(PSD_E_ARG, "psd_verify_static uses the library's fixed scratch: pass workspace NULL, 0 bytes");
     if (block->batch < 1 || block->gamma < 1 || block->gamma > PSD_MAX_GAMMA)
         return fail(PSD_E_ARG, "batch %d / gamma %d out of range", block->batch, block->gamma);
-    const size_t need =
-        psd::ws_layout(block->batch, params->num_drafts, block->gamma, params->vocab, params->dtype == PSD_BF16).total;
+    const size_t need = workspace_need(params, block->batch, block->gamma);
     if (need > psd::kStaticScratchBytes)
         return fail(PSD_E_WORKSPACE, "the shape needs %zu bytes of scratch; the fixed scratch holds %zu "
                     "(use psd_verify with a workspace)", need, psd::kStaticScratchBytes);

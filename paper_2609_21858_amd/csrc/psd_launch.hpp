@@ -52,6 +52,77 @@ struct MpfrArgs {
     float T, invT;
 };
 
+// Truncation before the race (top-k, then top-p): per row a kept list of at most
+// top_k (token, logit) pairs, sorted, its length and LSE, after the race kernel's
+// workspace (same row identifiers).
+constexpr int kMaxTopK = 256;
+struct TopkLayout {
+    size_t tok, val, len, lse, total;  // offsets from the workspace base; total = end
+};
+inline TopkLayout topk_layout(const WsLayout& L, int top_k) {
+    TopkLayout T;
+    size_t o = L.total;
+    T.tok = o;
+    o = align256(o + (size_t)L.n_rows * top_k * 4);
+    T.val = o;
+    o = align256(o + (size_t)L.n_rows * top_k * 4);
+    T.len = o;
+    o = align256(o + (size_t)L.n_rows * 4);
+    T.lse = o;
+    o = align256(o + (size_t)L.n_rows * 4);
+    T.total = o;
+    return T;
+}
+
+// One launch selects the kept lists of up to two row segments (the draft rows and the
+// target rows of a call): blocks [0, seg[0].n_rows) take segment 0, the next
+// seg[1].n_rows blocks segment 1.  Row r of a segment is row id
+// row_id_base + (group > 0 ? (r / group) * group_stride + r % group : r), and its LSE
+// goes to lse_out[lse_index_base + (same map with lse_group_stride)] when non-null.
+struct TopkSegment {
+    const void* logits;  // [n_rows][V]
+    int n_rows;
+    float T;
+    int row_id_base, group, group_stride;
+    float* lse_out;
+    int lse_index_base, lse_group_stride;
+};
+struct TopkSelectArgs {
+    TopkSegment seg[2];
+    int V;
+    int top_k;
+    float top_p;
+    int cap;
+    int32_t* list_tok;
+    float* list_val;
+    int32_t* list_len;
+    float* list_lse;
+    uint32_t* radix_rows;  // nullable: counts rows whose one-pass selection could not be
+                           // proven exact and were selected again by radix passes
+};
+
+struct TopkRaceArgs {
+    const int32_t* prefix;
+    const int64_t* start_pos;
+    int32_t* draft_tokens;   // [B][K][gamma]
+    int32_t* out_tokens;     // [B][gamma+1] (target_rows > 0)
+    int32_t* out_len;        // [B]
+    int32_t* target_tokens;  // nullable
+    const int32_t* list_tok;
+    const float* list_val;
+    const int32_t* list_len;
+    int cap;
+    uint64_t key;
+    int V, K, m, B, gamma;
+    int s_begin, s_count;    // draft depths of this call
+    int target_rows;         // 0 (drafting only), 1, K
+    int mpfr;
+    float T_target, T_draft;
+};
+
+hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t stream);
+hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t stream);
+
 hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
 hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
 hipError_t launch_finish_status(uint32_t* ctrl, uint32_t* status, hipStream_t stream);

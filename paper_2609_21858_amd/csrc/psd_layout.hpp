@@ -22,6 +22,7 @@ constexpr int kCtrlErrors = 2;     // sticky error bits (since the last clear)
 constexpr int kCtrlCallErrors = 3; // error bits of the running call; moved to kCtrlErrors and the
                                    // caller's status word by the call's last workgroup
 constexpr int kCtrlEpoch = 5;      // epoch of the last completed call
+constexpr int kCtrlTopkRadix = 6;  // rows of truncated calls selected by radix passes (cumulative)
 constexpr int kMaxQueues = 8;      // work queues (one per XCD) of each kind, counters 256 B apart
 // counter of segment queue q (q < kMaxQueues) or of row queue q - kMaxQueues
 inline constexpr int ctrl_queue(int q) { return 64 * (q + 1); }

@@ -1,0 +1,692 @@
+// psd_topk.hip -- logit processing before the race: top-k, then top-p (gfx950).
+//
+// The paper's experiments race the processed distributions (temperature, top-k,
+// top-p; Alg. "Batched-target direct-top-k MPFR speculative sampling"): every
+// token outside a row's kept set has probability 0.  With at most 256 kept tokens
+// per row the race needs no pruning, so this path has two kernels:
+//  * topk_select_kernel, one workgroup per row, one pass over the row in HBM: every
+//    thread keeps the 8 best (key, index) pairs of its elements (order-preserving
+//    keys; ties to the lowest index) through a branch-free max/min network and
+//    remembers the best pair it dropped; bisections over the kept pairs' keys and
+//    then their indices give the k-th best pair of the 2048 kept ones, which is the
+//    row's k-th best unless some thread dropped a pair at least as good -- such rows
+//    (rare: it needs 9 of the row's k best in one thread, or many ties at the cut)
+//    are selected again by exact radix passes.  Then the kept list is sorted by
+//    (logit descending, index ascending), its top-p prefix and the log-sum-exp of the
+//    kept set at the row's temperature are formed in fp64;
+//  * topk_race_kernel, one workgroup per sequence with one wave per independent
+//    chain (each draft path, the target chain): the block's races in dependency
+//    order over the lists, with exact fp64 clocks of every (token, slot) -- distinct
+//    drafters race slot k / all K slots, identical drafters draw each context's nu
+//    samples from the cumulative clocks and race the targets on slot 0 -- then the
+//    walk.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "psd_device.hpp"
+#include "psd_launch.hpp"
+#include "psd_layout.hpp"
+
+namespace psd {
+
+namespace {
+
+constexpr int kTBlock = 256;
+constexpr int kKeep = 8;    // pairs each thread keeps while streaming its elements
+constexpr int kUnroll = 4;  // 16-byte loads in flight per thread
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- keys
+
+// Order-preserving keys (larger value, larger key); -0 takes the key of +0, as the two
+// compare equal.
+__device__ __forceinline__ uint32_t key_f32(uint32_t u) {
+    if (u == 0x80000000u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float val_f32(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+__device__ __forceinline__ uint32_t key_bf16(uint32_t b) {
+    if (b == 0x8000u) b = 0u;
+    return (b & 0x8000u) ? (~b & 0xFFFFu) : (b | 0x8000u);
+}
+__device__ __forceinline__ float val_bf16(uint32_t k) {
+    const uint32_t b = (k & 0x8000u) ? (k & 0x7FFFu) : (~k & 0xFFFFu);
+    return __uint_as_float(b << 16);
+}
+
+// A kept pair packs (key, kIdx - local element number): a larger pair is a larger
+// logit, or the same logit at a lower index.  bf16 keys are 16 bits, so a pair fits
+// 32 bits (at most 2^19 / 256 elements per thread); fp32 pairs take 64 bits.
+template <bool BF16>
+struct Sel;
+template <>
+struct Sel<true> {
+    using P = uint32_t;
+    static constexpr int kShift = 16, kKeyBits = 16, kEPT = 8;
+    static constexpr uint32_t kNegInf = 0x007Fu, kIdx = 0xFFFFu, kNegInfBits = 0xFF80u;
+    static __device__ __forceinline__ uint32_t key(uint32_t bits) { return key_bf16(bits); }
+    static __device__ __forceinline__ float val(uint32_t k) { return val_bf16(k); }
+};
+template <>
+struct Sel<false> {
+    using P = uint64_t;
+    static constexpr int kShift = 32, kKeyBits = 32, kEPT = 4;
+    static constexpr uint32_t kNegInf = 0x007FFFFFu, kIdx = 0xFFFFFFFFu, kNegInfBits = 0xFF800000u;
+    static __device__ __forceinline__ uint32_t key(uint32_t bits) { return key_f32(bits); }
+    static __device__ __forceinline__ float val(uint32_t k) { return val_f32(k); }
+};
+
+__device__ __forceinline__ float tload(const unsigned char* row, bool bf16, int v) {
+    return bf16 ? __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16) : ((const float*)row)[v];
+}
+
+// ---------------------------------------------------------------- block helpers
+
+struct SelShared {
+    int hist[2048];  // radix passes only
+    int tok[kMaxTopK];
+    float val[kMaxTopK];
+    int stok[kMaxTopK];
+    float sval[kMaxTopK];
+    int red[2][kTBlock / 64];
+    double dred[kTBlock / 64];
+    double dsel;
+    int s4[kTBlock / 64];
+    int n_keep;
+    uint32_t prefix;
+    int above;
+};
+
+// Sum of one int per thread over the workgroup; every thread gets it.  The two LDS
+// buffers alternate (parity `it`), so one barrier per call suffices.
+__device__ __forceinline__ int block_sum(SelShared& sm, int x, int& it) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    int* r = sm.red[it & 1];
+    ++it;
+    if ((threadIdx.x & 63) == 0) r[threadIdx.x >> 6] = x;
+    __syncthreads();
+    int t = 0;
+#pragma unroll
+    for (int w = 0; w < kTBlock / 64; ++w) t += r[w];
+    return t;
+}
+
+// Inclusive prefix sum of one int per thread (thread order); *total gets the sum.
+__device__ __forceinline__ int block_incl_sum(SelShared& sm, int x, int& total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) sm.s4[wave] = x;
+    __syncthreads();
+    int base = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kTBlock / 64; ++w) {
+        if (w < wave) base += sm.s4[w];
+        tot += sm.s4[w];
+    }
+    __syncthreads();
+    total = tot;
+    return x + base;
+}
+
+// Inclusive prefix sum of one double per thread (thread order); *total gets the sum.
+__device__ __forceinline__ double block_incl_sum_f64(SelShared& sm, double x, double& total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const double y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) sm.dred[wave] = x;
+    __syncthreads();
+    double base = 0.0, tot = 0.0;
+#pragma unroll
+    for (int w = 0; w < kTBlock / 64; ++w) {
+        if (w < wave) base += sm.dred[w];
+        tot += sm.dred[w];
+    }
+    __syncthreads();
+    total = tot;
+    return x + base;
+}
+
+// ---------------------------------------------------------------- one-pass selection
+
+// Insert x into the descending list r (the smallest of the nine falls out and, if
+// larger than *dropped, becomes the new best dropped pair).
+template <typename P>
+__device__ __forceinline__ void keep_insert(P (&r)[kKeep], P& dropped, P x) {
+#pragma unroll
+    for (int q = 0; q < kKeep; ++q) {
+        const P hi = r[q] > x ? r[q] : x;
+        x = r[q] > x ? x : r[q];
+        r[q] = hi;
+    }
+    dropped = dropped > x ? dropped : x;
+}
+
+// Stream the row: thread t's elements are, chunk by chunk, the kEPT consecutive
+// tokens at c * 256 * kEPT + t * kEPT; local element number j = c * kEPT + i.
+template <bool BF16>
+__device__ __forceinline__ void stream_row(const unsigned char* row, int V, typename Sel<BF16>::P (&r)[kKeep],
+                                           typename Sel<BF16>::P& dropped, int& nfin) {
+    using S = Sel<BF16>;
+    using P = typename S::P;
+    constexpr int EPT = S::kEPT, CH = kTBlock * EPT;
+    constexpr size_t ES = BF16 ? 2 : 4;
+    const int tid = threadIdx.x;
+    const bool vec = ((uintptr_t)row & 15u) == 0;
+    for (int c0 = 0, cn = 0; c0 < V; c0 += CH * kUnroll, cn += kUnroll) {
+        uint32_t w[kUnroll][4];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int base = c0 + u * CH + tid * EPT;
+            if (vec && base + EPT <= V) {
+                const u32x4 q = __builtin_nontemporal_load((const u32x4*)(row + (size_t)base * ES));
+                w[u][0] = q.x;
+                w[u][1] = q.y;
+                w[u][2] = q.z;
+                w[u][3] = q.w;
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) w[u][i] = 0u;
+#pragma unroll
+                for (int i = 0; i < EPT; ++i) {
+                    const int v = base + i;
+                    if (BF16) {
+                        const uint32_t bits = v < V ? (uint32_t)((const uint16_t*)row)[v] : S::kNegInfBits;
+                        w[u][i >> 1] |= bits << (16 * (i & 1));
+                    } else {
+                        w[u][i] = v < V ? ((const uint32_t*)row)[v] : S::kNegInfBits;
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+            for (int i = 0; i < EPT; ++i) {
+                const uint32_t bits = BF16 ? (w[u][i >> 1] >> (16 * (i & 1))) & 0xFFFFu : w[u][i];
+                const uint32_t k = S::key(bits);
+                nfin += k > S::kNegInf;
+                const uint32_t j = (uint32_t)((cn + u) * EPT + i);
+                keep_insert<P>(r, dropped, ((P)k << S::kShift) | (P)(S::kIdx - j));
+            }
+    }
+}
+
+// Exact radix selection of the need largest (ties to the lowest index) into
+// sm.tok / sm.val, unsorted: three digit passes (11, 11, 10 bits) find the need-th
+// largest key, a fourth collects.  Reads the row four times.
+template <bool BF16>
+__device__ void radix_select(SelShared& sm, const unsigned char* row, int V, int need) {
+    const int tid = threadIdx.x;
+    const int shifts[3] = {21, 10, 0};
+    const int widths[3] = {11, 11, 10};
+    if (tid == 0) {
+        sm.prefix = 0u;
+        sm.above = 0;
+    }
+    for (int pass = 0; pass < 3; ++pass) {
+        const int nb = 1 << widths[pass];
+        for (int i = tid; i < nb; i += kTBlock) sm.hist[i] = 0;
+        __syncthreads();
+        const uint32_t pre = sm.prefix;
+        const int hi_shift = shifts[pass] + widths[pass];  // bits above this digit must equal the prefix
+        for (int v = tid; v < V; v += kTBlock) {
+            const float x = tload(row, BF16, v);
+            if (x == -INFINITY) continue;
+            const uint32_t k = key_f32(__float_as_uint(x));
+            if (hi_shift < 32 && (k >> hi_shift) != (pre >> hi_shift)) continue;
+            atomicAdd(&sm.hist[(k >> shifts[pass]) & (uint32_t)(nb - 1)], 1);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int acc = sm.above, b = nb - 1;
+            for (; b > 0; --b) {
+                if (acc + sm.hist[b] >= need) break;
+                acc += sm.hist[b];
+            }
+            sm.above = acc;
+            sm.prefix = pre | ((uint32_t)b << shifts[pass]);
+        }
+        __syncthreads();
+    }
+    const uint32_t thr = sm.prefix;
+    const int n_eq_take = need - sm.above;
+    if (tid == 0) sm.n_keep = 0;
+    __syncthreads();
+    int ties_before = 0;
+    for (int c0 = 0; c0 < V; c0 += kTBlock * 8) {
+        float x[8];
+        int nt = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int v = c0 + tid * 8 + i;
+            x[i] = v < V ? tload(row, BF16, v) : -INFINITY;
+            nt += x[i] != -INFINITY && key_f32(__float_as_uint(x[i])) == thr;
+        }
+        int total;
+        const int incl = block_incl_sum(sm, nt, total);
+        int rank = ties_before + incl - nt;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            if (x[i] == -INFINITY) continue;
+            const uint32_t k = key_f32(__float_as_uint(x[i]));
+            bool keep = k > thr;
+            if (k == thr) keep = rank++ < n_eq_take;
+            if (keep) {
+                const int j = atomicAdd(&sm.n_keep, 1);
+                if (j < kMaxTopK) {
+                    sm.tok[j] = c0 + tid * 8 + i;
+                    sm.val[j] = x[i] == 0.0f ? 0.0f : x[i];
+                }
+            }
+        }
+        ties_before += total;
+    }
+    __syncthreads();
+}
+
+// One row: kept list, its length and the LSE of the kept set.
+template <bool BF16>
+__global__ __launch_bounds__(kTBlock) void topk_select_kernel(TopkSelectArgs a) {
+    using S = Sel<BF16>;
+    using P = typename S::P;
+    constexpr int EPT = S::kEPT, CH = kTBlock * EPT;
+    __shared__ SelShared sm;
+    const int tid = threadIdx.x;
+    const bool s1 = (int)blockIdx.x >= a.seg[0].n_rows;
+    const TopkSegment& G = s1 ? a.seg[1] : a.seg[0];
+    const int r = (int)blockIdx.x - (s1 ? a.seg[0].n_rows : 0);
+    const unsigned char* row = (const unsigned char*)G.logits + (size_t)r * a.V * (BF16 ? 2 : 4);
+    const int rid = G.row_id_base + (G.group > 0 ? (r / G.group) * G.group_stride + r % G.group : r);
+    const int lse_at = G.lse_index_base + (G.group > 0 ? (r / G.group) * G.lse_group_stride + r % G.group : r);
+
+    P kept[kKeep];
+#pragma unroll
+    for (int q = 0; q < kKeep; ++q) kept[q] = 0;
+    P dropped = 0;
+    int nfin = 0;
+    stream_row<BF16>(row, a.V, kept, dropped, nfin);
+
+    int it = 0;
+    const int n_fin = block_sum(sm, nfin, it);
+    const int need = min(a.top_k, n_fin);
+    if (need == 0) {
+        if (tid == 0) {
+            a.list_len[rid] = 0;
+            a.list_lse[rid] = -INFINITY;
+            if (G.lse_out) G.lse_out[lse_at] = -INFINITY;
+        }
+        return;
+    }
+    // the need-th largest key among the kept pairs: largest t with #{key >= t} >= need
+    auto count_ge = [&](uint32_t t) {
+        int c = 0;
+#pragma unroll
+        for (int q = 0; q < kKeep; ++q) c += (uint32_t)(kept[q] >> S::kShift) >= t;
+        return block_sum(sm, c, it);
+    };
+    uint32_t t = 0;
+    for (int bit = S::kKeyBits - 1; bit >= 0; --bit) {
+        const uint32_t cand = t | (1u << bit);
+        if (count_ge(cand) >= need) t = cand;
+    }
+    // exact unless a thread dropped a pair whose key reaches t (then its thread may
+    // hide one of the row's need best), or fewer than need finite pairs were kept
+    const uint32_t dkey = (uint32_t)(dropped >> S::kShift);
+    const int unsure = block_sum(sm, dkey >= t ? 1 : 0, it);
+    if (t <= S::kNegInf || unsure > 0) {
+        if (tid == 0 && a.radix_rows) atomicAdd(a.radix_rows, 1u);
+        radix_select<BF16>(sm, row, a.V, need);
+    } else {
+        const int n_ge = count_ge(t);
+        const int n_gt = t == 0xFFFFFFFFu ? 0 : count_ge(t + 1u);
+        const int take = need - n_gt;  // ties at t to keep, lowest indices first
+        auto gidx = [&](P p) {
+            const uint32_t j = S::kIdx - (uint32_t)(p & (P)S::kIdx);
+            return (int)((j / EPT) * CH + tid * EPT + j % EPT);
+        };
+        int xmax = 0x7FFFFFFF;  // keep the ties with index <= xmax
+        if (n_ge - n_gt > take) {
+            // the take-th smallest index among the tied pairs: largest x with #{index < x} < take
+            int x = 0;
+            for (int bit = 18; bit >= 0; --bit) {
+                const int cand = x | (1 << bit);
+                int c = 0;
+#pragma unroll
+                for (int q = 0; q < kKeep; ++q)
+                    c += (uint32_t)(kept[q] >> S::kShift) == t && gidx(kept[q]) < cand;
+                if (block_sum(sm, c, it) < take) x = cand;
+            }
+            xmax = x;
+        }
+        // this thread's kept entries are a prefix of its descending list
+        int kc = 0;
+#pragma unroll
+        for (int q = 0; q < kKeep; ++q) {
+            const uint32_t k = (uint32_t)(kept[q] >> S::kShift);
+            kc += k > t || (k == t && gidx(kept[q]) <= xmax);
+        }
+        int total;
+        const int off = block_incl_sum(sm, kc, total) - kc;
+#pragma unroll
+        for (int q = 0; q < kKeep; ++q)
+            if (q < kc && off + q < kMaxTopK) {
+                sm.tok[off + q] = gidx(kept[q]);
+                sm.val[off + q] = S::val((uint32_t)(kept[q] >> S::kShift));
+            }
+        __syncthreads();
+    }
+    const int n = need;  // both branches leave exactly need entries
+    // sort by (logit descending, index ascending): each entry's rank by counting
+    if (tid < n) {
+        const float xv = sm.val[tid];
+        const int tv = sm.tok[tid];
+        int rk = 0;
+        for (int j = 0; j < n; ++j) rk += sm.val[j] > xv || (sm.val[j] == xv && sm.tok[j] < tv);
+        sm.stok[rk] = tv;
+        sm.sval[rk] = xv;
+    }
+    __syncthreads();
+    // top-p on the sorted list: the shortest prefix whose normalised mass at T reaches
+    // top_p; then the LSE of the kept set (fp64)
+    const double T = (double)G.T;
+    const double z0 = (double)sm.sval[0] / T;
+    const double e = tid < n ? exp((double)sm.sval[tid] / T - z0) : 0.0;
+    double tot;
+    const double inc = block_incl_sum_f64(sm, e, tot);
+    int keep = n;
+    if (a.top_p < 1.0f) keep = min(n, block_sum(sm, tid < n && inc / tot < (double)a.top_p ? 1 : 0, it) + 1);
+    if (tid == keep - 1) sm.dsel = inc;
+    __syncthreads();
+    if (tid == 0) {
+        const float lse = (float)(z0 + log(sm.dsel));
+        a.list_len[rid] = keep;
+        a.list_lse[rid] = lse;
+        if (G.lse_out) G.lse_out[lse_at] = lse;
+    }
+    int32_t* out_tok = a.list_tok + (size_t)rid * a.cap;
+    float* out_val = a.list_val + (size_t)rid * a.cap;
+    if (tid < keep) {
+        out_tok[tid] = sm.stok[tid];
+        out_val[tid] = sm.sval[tid];
+    }
+}
+
+// ---------------------------------------------------------------- races over the lists
+
+template <int LAYOUT>
+__device__ __forceinline__ double tclock(uint32_t V, uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
+    return LAYOUT == 0 ? tree_clock_f64(V, slot, v, k0, k1) : flat_clock_f64(slot, v, k0, k1);
+}
+
+__device__ __forceinline__ bool tlex(double s, int v, int j, double s2, int v2, int j2) {
+    return s < s2 || (s == s2 && (v < v2 || (v == v2 && j < j2)));
+}
+
+// Lexicographic minimum of (s, v, j) over the wave, with its entry c; every lane
+// returns the same result (a strict total order on distinct (v, j)).
+__device__ __forceinline__ void wave_lexmin(double& s, int& v, int& j, int& c) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const double os = __shfl_xor(s, o);
+        const int ov = __shfl_xor(v, o), oj = __shfl_xor(j, o), oc = __shfl_xor(c, o);
+        if (tlex(os, ov, oj, s, v, j)) {
+            s = os;
+            v = ov;
+            j = oj;
+            c = oc;
+        }
+    }
+}
+
+struct RaceShared {
+    int path[32 * 33];    // drafts of each path ([path][depth])
+    int chain[33];        // shared target chain
+    int pchain[32 * 33];  // per-path target chains
+};
+
+// Context key of the token at absolute position t whose previous tokens are the last
+// m of prefix (m tokens) || path[0 .. d); every lane of the wave computes it.
+__device__ __forceinline__ void list_key(const TopkRaceArgs& a, int b, int64_t t, const int* path, int d,
+                                         uint32_t& k0, uint32_t& k1) {
+    k0 = (uint32_t)a.key;
+    k1 = (uint32_t)(a.key >> 32);
+    fold(k0, k1, (uint32_t)(uint64_t)t, (uint32_t)((uint64_t)t >> 32), 0u);
+    for (int i = 0; i < a.m; ++i) {
+        const int g = d + i;  // index in prefix || path
+        const int w = g < a.m ? a.prefix[(size_t)b * a.m + g] : path[g - a.m];
+        fold(k0, k1, (uint32_t)w, (uint32_t)i, 1u);
+    }
+}
+
+// The race of one row's list over slots [slot0, slot0 + nslots), by one wave: argmin
+// of ln E_j[v] - l_v / T (exact, fp64); -1 for an empty list.
+template <int LAYOUT>
+__device__ int wave_race(const TopkRaceArgs& a, int rid, int slot0, int nslots, float T, uint32_t k0, uint32_t k1) {
+    const int lane = threadIdx.x & 63;
+    const int n = a.list_len[rid];
+    const int* lt = a.list_tok + (size_t)rid * a.cap;
+    const float* lv = a.list_val + (size_t)rid * a.cap;
+    double bs = INFINITY;
+    int bv = 0x7FFFFFFF, bj = 0x7FFFFFFF, bc = -1;
+    for (int e = lane; e < n * nslots; e += 64) {
+        const int c = e / nslots, j = slot0 + e % nslots;
+        const int v = lt[c];
+        const double s = log(tclock<LAYOUT>((uint32_t)a.V, (uint32_t)j, (uint32_t)v, k0, k1)) - (double)lv[c] / (double)T;
+        if (tlex(s, v, j, bs, bv, bj)) {
+            bs = s;
+            bv = v;
+            bj = j;
+            bc = c;
+        }
+    }
+    wave_lexmin(bs, bv, bj, bc);
+    return bs < INFINITY ? bv : -1;
+}
+
+// The nu MPFR samples of one context from its row's list, by one wave: the nu
+// smallest of ln G_{v,j} - l_v / T over (v, j < nu), G_{v,j} = E_0[v] + ... + E_j[v];
+// the r-th goes to the r-th path of `members` (ascending) at depth s.
+template <int LAYOUT>
+__device__ void wave_mpfr(const TopkRaceArgs& a, RaceShared& sm, int rid, uint32_t members, int s, float T,
+                          uint32_t k0, uint32_t k1) {
+    constexpr int Q = kMaxTopK / 64;
+    const int lane = threadIdx.x & 63;
+    const int n = a.list_len[rid];
+    const int nu = __popc(members);
+    const int* lt = a.list_tok + (size_t)rid * a.cap;
+    const float* lv = a.list_val + (size_t)rid * a.cap;
+    double Gs[Q], sc[Q], lT[Q];
+    int tok[Q], jj[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int c = lane + 64 * q;
+        jj[q] = 0;
+        if (c < n) {
+            tok[q] = lt[c];
+            lT[q] = (double)lv[c] / (double)T;
+            Gs[q] = tclock<LAYOUT>((uint32_t)a.V, 0u, (uint32_t)tok[q], k0, k1);
+            sc[q] = log(Gs[q]) - lT[q];
+        } else {
+            tok[q] = 0x7FFFFFFF;
+            lT[q] = 0.0;
+            Gs[q] = 0.0;
+            sc[q] = INFINITY;
+        }
+    }
+    uint32_t mm = members;
+    for (int r = 0; r < nu; ++r) {
+        double bs = INFINITY;
+        int bv = 0x7FFFFFFF, bj = 0x7FFFFFFF, bc = -1;
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            if (tlex(sc[q], tok[q], jj[q], bs, bv, bj)) {
+                bs = sc[q];
+                bv = tok[q];
+                bj = jj[q];
+                bc = lane + 64 * q;
+            }
+        wave_lexmin(bs, bv, bj, bc);
+        const int member = __ffs((int)mm) - 1;
+        mm &= mm - 1u;
+        if (lane == 0) sm.path[member * 33 + s] = bs < INFINITY ? bv : -1;
+        if (bs < INFINITY && lane == (bc & 63)) {
+            // the winner's next arrival (one clock, then back into its register slot)
+            const int qb = bc >> 6;
+            int j = 0;
+            double g = 0.0, l = 0.0;
+#pragma unroll
+            for (int q = 0; q < Q; ++q)
+                if (q == qb) {
+                    j = jj[q] + 1;
+                    g = Gs[q];
+                    l = lT[q];
+                }
+            double ns = INFINITY;
+            if (j < nu) {
+                g += tclock<LAYOUT>((uint32_t)a.V, (uint32_t)j, (uint32_t)bv, k0, k1);
+                ns = log(g) - l;
+            }
+#pragma unroll
+            for (int q = 0; q < Q; ++q)
+                if (q == qb) {
+                    Gs[q] = g;
+                    sc[q] = ns;
+                    jj[q] = j;
+                }
+        }
+    }
+}
+
+template <int LAYOUT>
+__global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
+    __shared__ RaceShared sm;
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6, nw = (int)(blockDim.x >> 6);
+    const int K = a.K, G = a.gamma;
+    const int D = a.B * K * G;
+    const int64_t t0 = a.start_pos[b];
+    // drafts known before the call (depths < s_begin, or all of them as input)
+    for (int e = tid; e < K * G; e += blockDim.x)
+        sm.path[(e / G) * 33 + e % G] = a.draft_tokens[((size_t)b * K + e / G) * G + e % G];
+    __syncthreads();
+    const bool per = a.target_rows > 1;
+    const int tslots = a.mpfr ? 1 : K;
+    const int tw = K % nw;  // the wave racing the shared target chain
+    const int d_end = a.s_begin + a.s_count;
+    const int s_lo = a.target_rows > 0 ? 0 : a.s_begin;
+    const int s_hi = a.target_rows > 0 ? G : d_end - 1;
+    uint32_t k0, k1;
+    for (int s = s_lo; s <= s_hi; ++s) {
+        if (s >= a.s_begin && s < d_end) {
+            for (int k = w; k < K; k += nw) {
+                if (!a.mpfr) {
+                    list_key(a, b, t0 + s, &sm.path[k * 33], s, k0, k1);
+                    const int y = wave_race<LAYOUT>(a, (b * K + k) * G + s, k, 1, a.T_draft, k0, k1);
+                    if (lane == 0) sm.path[k * 33 + s] = y;
+                } else {
+                    // the context of path k: the paths with its drafts at depths < s; its
+                    // lowest path draws the context's samples (wave-uniform)
+                    uint32_t members = 0u;
+                    bool rep = true;
+                    for (int q = 0; q < K; ++q) {
+                        bool same = true;
+                        for (int d = 0; d < s && same; ++d) same = sm.path[q * 33 + d] == sm.path[k * 33 + d];
+                        if (same) {
+                            members |= 1u << q;
+                            if (q < k) rep = false;
+                        }
+                    }
+                    if (!rep) continue;
+                    list_key(a, b, t0 + s, &sm.path[k * 33], s, k0, k1);
+                    wave_mpfr<LAYOUT>(a, sm, (b * K + k) * G + s, members, s, a.T_draft, k0, k1);
+                }
+            }
+        }
+        if (a.target_rows == 1 && w == tw) {
+            list_key(a, b, t0 + s, sm.chain, s, k0, k1);
+            const int y = wave_race<LAYOUT>(a, D + b * (G + 1) + s, 0, tslots, a.T_target, k0, k1);
+            if (lane == 0) sm.chain[s] = y;
+        }
+        if (per)
+            for (int k = w; k < K; k += nw) {
+                list_key(a, b, t0 + s, &sm.path[k * 33], s, k0, k1);
+                const int y = wave_race<LAYOUT>(a, D + (b * K + k) * (G + 1) + s, 0, tslots, a.T_target, k0, k1);
+                if (lane == 0) sm.pchain[k * 33 + s] = y;
+            }
+        __syncthreads();
+    }
+    if (a.s_count > 0)
+        for (int e = tid; e < K * a.s_count; e += blockDim.x) {
+            const int k = e / a.s_count, s = a.s_begin + e % a.s_count;
+            a.draft_tokens[((size_t)b * K + k) * G + s] = sm.path[k * 33 + s];
+        }
+    if (a.target_rows == 0 || tid != 0) return;
+    auto target = [&](int k, int s) { return per ? sm.pchain[k * 33 + s] : sm.chain[s]; };
+    if (a.target_tokens)
+        for (int k = 0; k < (per ? K : 1); ++k)
+            for (int s = 0; s <= G; ++s) a.target_tokens[((size_t)b * (per ? K : 1) + k) * (G + 1) + s] = target(k, s);
+    // ---- the walk (as in the fused kernel)
+    uint32_t act = K >= 32 ? 0xFFFFFFFFu : ((1u << K) - 1u);
+    int tau = 0;
+    bool done = false;
+    for (int s = 0; s < G && !done; ++s) {
+        const int y = target(__ffs((int)act) - 1, s);
+        a.out_tokens[(size_t)b * (G + 1) + s] = y;
+        tau = s + 1;
+        if (y < 0) {
+            done = true;
+            break;
+        }
+        uint32_t na = 0u;
+        for (int k = 0; k < K; ++k)
+            if (((act >> k) & 1u) && sm.path[k * 33 + s] == y) na |= 1u << k;
+        if (!na) {
+            done = true;
+            break;
+        }
+        act = na;
+    }
+    if (!done) {
+        a.out_tokens[(size_t)b * (G + 1) + G] = target(__ffs((int)act) - 1, G);
+        tau = G + 1;
+    }
+    for (int s = tau; s <= G; ++s) a.out_tokens[(size_t)b * (G + 1) + s] = -1;
+    a.out_len[b] = tau;
+}
+
+}  // namespace
+
+hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t stream) {
+    const int n = a.seg[0].n_rows + a.seg[1].n_rows;
+    if (n <= 0) return hipSuccess;
+    if (bf16)
+        hipLaunchKernelGGL(topk_select_kernel<true>, dim3(n), dim3(kTBlock), 0, stream, a);
+    else
+        hipLaunchKernelGGL(topk_select_kernel<false>, dim3(n), dim3(kTBlock), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t stream) {
+    // one wave per independent chain (the K draft paths, and the shared target chain),
+    // at most 8: the TREE clocks need more than 128 registers per lane
+    const int chains = a.K + (a.target_rows == 1 ? 1 : 0);
+    const int threads = 64 * (chains < 8 ? chains : 8);
+    if (layout == 0)
+        hipLaunchKernelGGL(topk_race_kernel<0>, dim3(a.B), dim3(threads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(topk_race_kernel<1>, dim3(a.B), dim3(threads), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace psd

@@ -38,6 +38,8 @@ class Params(ctypes.Structure):
         ("dtype", ctypes.c_int32),
         ("mode", ctypes.c_int32),
         ("clocks", ctypes.c_int32),
+        ("top_k", ctypes.c_int32),
+        ("top_p", ctypes.c_float),
     ]
 
 
@@ -114,10 +116,10 @@ def _stream(stream=None):
 
 def make_params(key: int, vocab: int, num_drafts: int, ctx_window: int, temp_target: float = 1.0,
                 temp_draft: float = 1.0, dtype=torch.bfloat16, mode: int = PSD_MODE_HET,
-                clocks: int = PSD_CLOCKS_TREE) -> Params:
+                clocks: int = PSD_CLOCKS_TREE, top_k: int = 0, top_p: float = 1.0) -> Params:
     dt = dtype if isinstance(dtype, int) else (PSD_BF16 if dtype == torch.bfloat16 else PSD_F32)
     return Params(key & 0xFFFFFFFFFFFFFFFF, vocab, num_drafts, ctx_window, temp_target, temp_draft, dt, mode,
-                  clocks)
+                  clocks, top_k, top_p)
 
 
 def workspace_bytes(params: Params, batch: int, gamma: int) -> int:

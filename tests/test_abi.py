@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol(psd):
     for n in names:
         assert hasattr(psd.lib(), n), n
         assert n in psd.EXPORTS
-    assert psd.lib().psd_abi_version() == 2
+    assert psd.lib().psd_abi_version() == 3
 
 
 def test_workspace_bytes(psd):
@@ -92,6 +92,34 @@ def test_mode_mpfr_validated_like_het(psd):
     assert psd.lib().psd_draft(ctypes.byref(p), ctypes.byref(blk), 0, 4, FAKE, FAKE, None, None) == psd.PSD_E_ARG
     p.mode = 2
     assert _verify(psd, p) == psd.PSD_E_ARG
+
+
+@pytest.mark.parametrize("top_k,top_p", [(-1, 1.0), (257, 1.0), (50, 0.0), (50, -0.5), (50, 1.5),
+                                         (50, float("nan")), (0, 0.9)])
+def test_truncation_params_validated(psd, top_k, top_p):
+    """top_k in [0, 256]; top_p in (0, 1]; top_p < 1 needs top_k >= 1 (the nucleus is
+    taken inside the top-k set)."""
+    p = psd.make_params(1, 1000, 2, 4, top_k=top_k, top_p=top_p)
+    assert _verify(psd, p, ws_bytes=1 << 30) == psd.PSD_E_ARG
+    assert "top_" in psd.lib().psd_last_error().decode()
+
+
+def test_truncation_workspace(psd):
+    """Truncated calls need room for the kept lists: the workspace grows with top_k and a
+    block sized for untruncated calls is rejected."""
+    base = psd.make_params(1, 32000, 4, 4)
+    n0 = psd.workspace_bytes(base, 16, 5)
+    n50 = psd.workspace_bytes(psd.make_params(1, 32000, 4, 4, top_k=50), 16, 5)
+    n256 = psd.workspace_bytes(psd.make_params(1, 32000, 4, 4, top_k=256, top_p=0.9), 16, 5)
+    rows = 16 * 4 * 5 + 16 * 4 * 6  # draft rows and per-path target rows
+    assert n0 < n50 < n256 and n50 - n0 >= rows * 50 * 8 and n256 % 256 == 0
+    assert psd.workspace_bytes(psd.make_params(1, 32000, 4, 4, top_k=300), 16, 5) == 0
+    p = psd.make_params(1, 32000, 4, 4, top_k=50)
+    assert _verify(psd, p, B=16, gamma=5, ws_bytes=n0) == psd.PSD_E_WORKSPACE
+    for mode in (psd.PSD_MODE_HET, psd.PSD_MODE_MPFR):
+        p = psd.make_params(1, 1000, 2, 4, mode=mode, top_k=5, top_p=0.5)
+        assert _verify(psd, p, tl=None) == psd.PSD_E_ARG
+        assert _verify(psd, p, target_rows=3) == psd.PSD_E_ARG
 
 
 def test_draft_and_detect_reject_bad_args(psd):
