@@ -276,6 +276,60 @@ def topk_leg(psd, torch, w, sets, clocks_id, dev, mpfr=False, top_k=50, top_p=1.
             "mean_tau": float(outs[(launches - 1) % len(sets)]["out_len"].float().mean())}
 
 
+def generation_leg(psd, torch, clocks_id, dev, n_pos=512):
+    """The stress workload's generation statement on the device: 256 sequences x 512
+    positions, V=256000, K=16, gamma=4, bf16, with the position-indexed toy model
+    (psd_generate: toy rows -> fused verify -> commit, the active count read every 16
+    blocks), once as captured-graph replays and once eagerly; and, for comparison, the
+    same blocks driven from Python with a host synchronisation per block."""
+    import workloads
+    w = workloads.WORKLOADS[5]
+    params = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype, clocks=clocks_id)
+    lm = psd.make_toy_lm(2026, 12, w.sigma, w.alpha, w.tau, w.B // 2)
+    g = torch.Generator().manual_seed(77)
+    prompts = torch.randint(0, w.V, (w.B, w.m), generator=g, dtype=torch.int64).to(torch.int32).to(dev)
+    ws = torch.empty(psd.generate_workspace_bytes(params, w.B, w.gamma), dtype=torch.uint8, device=dev)
+    out = {"workload": f"{w.name}, {w.B} x {n_pos} positions, position-indexed toy model", "tokens": w.B * n_pos}
+    texts = {}
+    for name, graph in (("graph", True), ("eager", False)):
+        psd.generate(params, lm, prompts, 32, w.gamma, check_every=16, use_graph=graph, ws=ws)  # warm-up
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        text, blocks, bits = psd.generate(params, lm, prompts, n_pos, w.gamma, check_every=16, use_graph=graph, ws=ws)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        if bits:
+            raise RuntimeError(f"generation reported error bits {bits}")
+        texts[name] = text
+        out[name] = {"wall_s": dt, "blocks": blocks, "tokens_per_s": w.B * n_pos / dt, "ms_per_block": dt / blocks * 1e3}
+    # host-driven loop: the same calls, a synchronisation and a host read per block
+    m = w.m
+    text = torch.full((w.B, m + n_pos), -1, dtype=torch.int32, device=dev)
+    text[:, :m] = prompts
+    length = torch.empty(w.B, dtype=torch.int64, device=dev)
+    start = torch.empty(w.B, dtype=torch.int64, device=dev)
+    prefix = torch.empty((w.B, m), dtype=torch.int32, device=dev)
+    act = torch.empty(1, dtype=torch.int32, device=dev)
+    bws = psd.new_workspace(params, w.B, w.gamma, dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    psd.advance(params, w.gamma, m + n_pos, text, length, prefix, start, act)
+    blocks = 0
+    while True:
+        tl, dl = psd.toy_logits(params, lm, w.gamma, start)
+        o = psd.verify(params, bws, prefix, start, tl, dl)
+        psd.advance(params, w.gamma, m + n_pos, text, length, prefix, start, act, o["out_tokens"], o["out_len"])
+        blocks += 1
+        if int(act[0]) == 0:  # the host read synchronises
+            break
+    dt = time.perf_counter() - t0
+    out["host_loop"] = {"wall_s": dt, "blocks": blocks, "tokens_per_s": w.B * n_pos / dt,
+                        "ms_per_block": dt / blocks * 1e3}
+    out["same_text"] = bool(torch.equal(texts["graph"], texts["eager"]) and torch.equal(texts["graph"], text))
+    out["positions_per_block"] = n_pos / float(blocks)  # of the sequence that needed the most blocks
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -287,6 +341,7 @@ def main():
     ap.add_argument("--cpu-seqs", type=int, default=64, help="sequences of the all-cores oracle leg")
     ap.add_argument("--cpu-seqs-single", type=int, default=16, help="sequences of the single-thread leg")
     ap.add_argument("--no-detect-100x", action="store_true")
+    ap.add_argument("--no-generation", action="store_true")
     ap.add_argument("--pmc-copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for FETCH/WRITE_SIZE scaling)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -391,6 +446,8 @@ def main():
                    topk_leg(psd, torch, w, sets, clocks_id, dev, mpfr=True),
                    topk_leg(psd, torch, w, sets, clocks_id, dev, top_p=0.9)]
     res["detect"] = detect_leg(psd, torch, clocks_id, dev)
+    if not args.no_generation:
+        res["generation"] = generation_leg(psd, torch, clocks_id, dev)
     if not args.no_detect_100x:
         res["detect_100x"] = detect_leg(psd, torch, clocks_id, dev, launches=5, replicate=100)
     if not args.no_cpu_baseline:

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "lib", "libpsd.so")
-SOURCES = ["psd_race.hip", "psd_mpfr.hip", "psd_topk.hip", "psd_detect.hip", "psd_api.cpp"]
+SOURCES = ["psd_race.hip", "psd_mpfr.hip", "psd_topk.hip", "psd_gen.hip", "psd_detect.hip", "psd_api.cpp"]
 ARCH = "gfx950"
 # Packed-fp32 VALU forms are kept out of every kernel.
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
@@ -19,7 +19,8 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-ta
 # atomic optimizer turns a same-address atomic with per-lane values into a scalar
 # loop over the active lanes (about 70 cycles per lane), far slower than the LDS
 # serialising the lanes' atomics itself.
-EXTRA = {"psd_race.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
+EXTRA = {"psd_race.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
+         "psd_gen.hip": ["-ffp-contract=off"]}
 
 
 def hipcc() -> str:

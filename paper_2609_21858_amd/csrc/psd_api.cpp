@@ -570,3 +570,260 @@ psd_status psd_clock_values(const psd_params* params, int32_t n, const uint32_t*
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------- multi-block generation
+
+namespace {
+
+// psd_generate's scratch: the block workspace first (so it keeps its alignment),
+// then both logits buffers and the loop's state.
+struct GenLayout {
+    size_t ws_bytes, tl, dl, dt, ot, ol, len, start, prefix, active, total;
+};
+
+GenLayout gen_layout(const psd_params* p, int B, int G) {
+    GenLayout L;
+    const size_t es = p->dtype == PSD_BF16 ? 2 : 4, V = (size_t)p->vocab, K = (size_t)p->num_drafts;
+    L.ws_bytes = workspace_need(p, B, G);
+    size_t o = psd::align256(L.ws_bytes);
+    L.tl = o;
+    o = psd::align256(o + (size_t)B * (G + 1) * V * es);
+    L.dl = o;
+    o = psd::align256(o + (size_t)B * K * G * V * es);
+    L.dt = o;
+    o = psd::align256(o + (size_t)B * K * G * 4);
+    L.ot = o;
+    o = psd::align256(o + (size_t)B * (G + 1) * 4);
+    L.ol = o;
+    o = psd::align256(o + (size_t)B * 4);
+    L.len = o;
+    o = psd::align256(o + (size_t)B * 8);
+    L.start = o;
+    o = psd::align256(o + (size_t)B * 8);
+    L.prefix = o;
+    o = psd::align256(o + (size_t)B * (size_t)p->ctx_window * 4 + 4);
+    L.active = o;
+    o = psd::align256(o + 4);
+    L.total = o;
+    return L;
+}
+
+psd_status check_toy(const psd_toy_lm* lm) {
+    if (!lm) return fail(PSD_E_ARG, "toy model is NULL");
+    if (!isfinite(lm->sigma) || !isfinite(lm->alpha) || !isfinite(lm->tau[0]) || !isfinite(lm->tau[1]))
+        return fail(PSD_E_ARG, "toy model parameters must be finite");
+    return PSD_OK;
+}
+
+psd::ToyArgs toy_args(const psd_params* p, const psd_toy_lm* lm, int B, int G, const int64_t* start, void* tl,
+                      void* dl) {
+    psd::ToyArgs a;
+    memset(&a, 0, sizeof a);
+    a.start_pos = start;
+    a.target_logits = tl;
+    a.draft_logits = dl;
+    a.seed = lm->seed;
+    a.draft_seed = lm->draft_seed;
+    a.sigma = lm->sigma;
+    a.w = (float)(-(double)lm->alpha * 0.69314718055994531 * 0x1p-23);
+    a.tau0 = lm->tau[0];
+    a.tau1 = lm->tau[1];
+    a.tau_split = lm->tau_split;
+    a.V = p->vocab;
+    a.K = p->num_drafts;
+    a.B = B;
+    a.gamma = G;
+    return a;
+}
+
+psd::AdvanceArgs advance_args(int B, int G, int m, int64_t max_len, const int32_t* out_tokens, const int32_t* out_len,
+                              int32_t* text, int64_t text_stride, int64_t* length, int32_t* prefix, int64_t* start,
+                              int32_t* n_active) {
+    psd::AdvanceArgs a;
+    memset(&a, 0, sizeof a);
+    a.out_tokens = out_tokens;
+    a.out_len = out_len;
+    a.text = text;
+    a.text_stride = text_stride;
+    a.length = length;
+    a.start_pos = start;
+    a.prefix = prefix;
+    a.n_active = n_active;
+    a.B = B;
+    a.gamma = G;
+    a.m = m;
+    a.max_len = max_len;
+    return a;
+}
+
+psd_status check_shape(int32_t batch, int32_t gamma) {
+    if (batch < 1 || batch > PSD_MAX_BATCH) return fail(PSD_E_ARG, "batch %d outside [1, %d]", batch, PSD_MAX_BATCH);
+    if (gamma < 1 || gamma > PSD_MAX_GAMMA) return fail(PSD_E_ARG, "gamma %d outside [1, %d]", gamma, PSD_MAX_GAMMA);
+    return PSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+psd_status psd_advance(const psd_params* params, int32_t batch, int32_t gamma, int64_t max_len,
+                       const int32_t* out_tokens, const int32_t* out_len, int32_t* text, int64_t text_stride,
+                       int64_t* length, int32_t* prefix_tokens, int64_t* start_pos, int32_t* n_active,
+                       hipStream_t stream) {
+    if (!params) return fail(PSD_E_ARG, "params is NULL");
+    const int m = params->ctx_window;
+    if (m < 0 || m > PSD_MAX_WINDOW) return fail(PSD_E_ARG, "ctx_window %d outside [0, %d]", m, PSD_MAX_WINDOW);
+    psd_status st = check_shape(batch, gamma);
+    if (st != PSD_OK) return st;
+    if (max_len <= m) return fail(PSD_E_ARG, "max_len must exceed the prompt length m = %d", m);
+    if (text_stride < max_len) return fail(PSD_E_ARG, "text_stride is below max_len");
+    if (!text || !length || !start_pos || !n_active || (m > 0 && !prefix_tokens))
+        return fail(PSD_E_ARG, "text / length / start_pos / n_active / prefix_tokens is NULL");
+    if (out_len && !out_tokens) return fail(PSD_E_ARG, "out_tokens is NULL");
+    hipError_t e = psd::launch_advance(advance_args(batch, gamma, m, max_len, out_tokens, out_len, text, text_stride,
+                                                    length, prefix_tokens, start_pos, n_active),
+                                       stream);
+    if (e != hipSuccess) return hip_fail(e, "advance kernel launch");
+    return PSD_OK;
+}
+
+psd_status psd_toy_logits(const psd_params* params, const psd_toy_lm* lm, int32_t batch, int32_t gamma,
+                          const int64_t* start_pos, void* target_logits, void* draft_logits, hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    if ((st = check_toy(lm)) != PSD_OK) return st;
+    if ((st = check_shape(batch, gamma)) != PSD_OK) return st;
+    if (!start_pos || !target_logits) return fail(PSD_E_ARG, "start_pos / target_logits is NULL");
+    hipError_t e = psd::launch_toy_rows(toy_args(params, lm, batch, gamma, start_pos, target_logits, draft_logits),
+                                        params->dtype == PSD_BF16, stream);
+    if (e != hipSuccess) return hip_fail(e, "toy model kernel launch");
+    return PSD_OK;
+}
+
+size_t psd_generate_workspace_bytes(const psd_params* params, int32_t batch, int32_t gamma) {
+    if (psd_workspace_bytes(params, batch, gamma) == 0) return 0;
+    if (params->ctx_window < 0 || params->ctx_window > PSD_MAX_WINDOW) return 0;
+    return gen_layout(params, batch, gamma).total;
+}
+
+psd_status psd_generate(const psd_params* params, const psd_toy_lm* lm, int32_t batch, int32_t gamma, int32_t n_pos,
+                        int32_t* text, int64_t text_stride, void* workspace, size_t workspace_bytes,
+                        int32_t check_every, int32_t use_graph, int32_t* out_blocks, uint32_t* out_status,
+                        hipStream_t stream) {
+    psd_status st = check_params(params);
+    if (st != PSD_OK) return st;
+    if ((st = check_toy(lm)) != PSD_OK) return st;
+    if ((st = check_shape(batch, gamma)) != PSD_OK) return st;
+    const int m = params->ctx_window;
+    if (n_pos < 1) return fail(PSD_E_ARG, "n_pos must be at least 1");
+    if (!text) return fail(PSD_E_ARG, "text is NULL");
+    if (text_stride < (int64_t)m + n_pos) return fail(PSD_E_ARG, "text_stride is below m + n_pos");
+    if (check_every < 1) return fail(PSD_E_ARG, "check_every must be at least 1");
+    const GenLayout L = gen_layout(params, batch, gamma);
+    if (!workspace) return fail(PSD_E_WORKSPACE, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(PSD_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if (workspace_bytes < L.total)
+        return fail(PSD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, L.total);
+    unsigned char* ws = (unsigned char*)workspace;
+    const int64_t max_len = (int64_t)m + n_pos;
+    const bool bf16 = params->dtype == PSD_BF16;
+    void* tl = ws + L.tl;
+    void* dl = ws + L.dl;
+    int32_t* dt = (int32_t*)(ws + L.dt);
+    int32_t* ot = (int32_t*)(ws + L.ot);
+    int32_t* ol = (int32_t*)(ws + L.ol);
+    int64_t* len = (int64_t*)(ws + L.len);
+    int64_t* start = (int64_t*)(ws + L.start);
+    int32_t* prefix = (int32_t*)(ws + L.prefix);
+    int32_t* active = (int32_t*)(ws + L.active);
+    psd_block blk;
+    memset(&blk, 0, sizeof blk);
+    blk.batch = batch;
+    blk.gamma = gamma;
+    blk.prefix_tokens = prefix;
+    blk.start_pos = start;
+    blk.workspace = ws;
+    blk.workspace_bytes = L.ws_bytes;
+    const psd::ToyArgs toy = toy_args(params, lm, batch, gamma, start, tl, dl);
+    const psd::AdvanceArgs adv = advance_args(batch, gamma, m, max_len, ot, ol, text, text_stride, len, prefix, start,
+                                              active);
+    // one block: the model's rows, the race and the walk, the commit
+    auto body = [&](hipStream_t s) -> psd_status {
+        hipError_t e = psd::launch_toy_rows(toy, bf16, s);
+        if (e != hipSuccess) return hip_fail(e, "toy model kernel launch");
+        psd_status r = verify_impl(params, &blk, 1, tl, dl, dt, ot, ol, nullptr, nullptr, nullptr, s);
+        if (r != PSD_OK) return r;
+        if ((e = psd::launch_advance(adv, s)) != hipSuccess) return hip_fail(e, "advance kernel launch");
+        return PSD_OK;
+    };
+
+    hipStream_t s = stream, own = nullptr;
+    hipEvent_t ev = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    int32_t* host_active = nullptr;
+    int blocks = 0;
+    hipError_t e = hipSuccess;
+    st = PSD_OK;
+    do {
+        if (use_graph) {
+            // capture needs a stream of its own (the caller's may be the null stream)
+            if ((e = hipStreamCreateWithFlags(&own, hipStreamNonBlocking)) != hipSuccess) break;
+            if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) break;
+            if ((e = hipEventRecord(ev, stream)) != hipSuccess) break;
+            if ((e = hipStreamWaitEvent(own, ev, 0)) != hipSuccess) break;
+            s = own;
+        }
+        if ((e = hipHostMalloc((void**)&host_active, sizeof(int32_t), hipHostMallocDefault)) != hipSuccess) break;
+        // a fresh block workspace, and the first block's windows from the prompts
+        if ((e = psd::launch_fill_zero((uint32_t*)ws, L.ws_bytes / 4, s)) != hipSuccess) break;
+        psd::AdvanceArgs first = adv;
+        first.out_len = nullptr;
+        if ((e = psd::launch_advance(first, s)) != hipSuccess) break;
+        if (use_graph) {
+            if ((e = hipStreamBeginCapture(s, hipStreamCaptureModeRelaxed)) != hipSuccess) break;
+            for (int i = 0; i < check_every && st == PSD_OK; ++i) st = body(s);
+            hipGraph_t g = nullptr;
+            const hipError_t ec = hipStreamEndCapture(s, &g);
+            graph = g;
+            if (st != PSD_OK) break;
+            if ((e = ec) != hipSuccess) break;
+            if ((e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0)) != hipSuccess) break;
+        }
+        // every active sequence gains at least one token per block, so n_pos blocks suffice
+        while (true) {
+            if (use_graph) {
+                if ((e = hipGraphLaunch(exec, s)) != hipSuccess) break;
+            } else {
+                for (int i = 0; i < check_every && st == PSD_OK; ++i) st = body(s);
+                if (st != PSD_OK) break;
+            }
+            blocks += check_every;
+            if ((e = hipMemcpyAsync(host_active, active, sizeof(int32_t), hipMemcpyDeviceToHost, s)) != hipSuccess)
+                break;
+            if ((e = hipStreamSynchronize(s)) != hipSuccess) break;
+            if (*host_active == 0) break;
+            if (blocks >= n_pos + check_every) {
+                st = fail(PSD_E_HIP, "generation did not finish within %d blocks", blocks);
+                break;
+            }
+        }
+    } while (false);
+    if (e != hipSuccess && st == PSD_OK) st = hip_fail(e, "generation loop");
+    if (own) hipStreamSynchronize(own);
+    if (exec) hipGraphExecDestroy(exec);
+    if (graph) hipGraphDestroy(graph);
+    if (host_active) hipHostFree(host_active);
+    if (ev) hipEventDestroy(ev);
+    if (own) hipStreamDestroy(own);
+    if (st != PSD_OK) return st;
+    if (out_blocks) *out_blocks = blocks;
+    if (out_status) {
+        uint32_t bits = 0;
+        if ((st = psd_workspace_errors(ws, stream, &bits)) != PSD_OK) return st;
+        *out_status = bits;
+    }
+    return PSD_OK;
+}
+
+}  // extern "C"

@@ -120,6 +120,36 @@ struct TopkRaceArgs {
     float T_target, T_draft;
 };
 
+// Position-indexed toy language model: target rows [B][gamma+1][V] at positions
+// start_pos[b] + s and draft rows [B][K][gamma][V] (nullable).
+struct ToyArgs {
+    const int64_t* start_pos;
+    void* target_logits;
+    void* draft_logits;
+    uint64_t seed, draft_seed;
+    float sigma, w;      // noise scale; weight of the rank term (-alpha ln 2 / 2^23)
+    float tau0, tau1;    // draft noise of sequences b < tau_split, and of the others
+    int tau_split;
+    int V, K, B, gamma;
+};
+
+// Commit one block's emitted tokens into the texts (out_len NULL: first block, from
+// the prompts), then the next block's start positions, windows and active count.
+struct AdvanceArgs {
+    const int32_t* out_tokens;  // [B][gamma+1]
+    const int32_t* out_len;     // [B], nullable
+    int32_t* text;              // [B][text_stride]
+    int64_t text_stride;
+    int64_t* length;            // [B]
+    int64_t* start_pos;         // [B]
+    int32_t* prefix;            // [B][m]
+    int32_t* n_active;          // one word
+    int B, gamma, m;
+    int64_t max_len;
+};
+
+hipError_t launch_toy_rows(const ToyArgs& a, bool bf16, hipStream_t stream);
+hipError_t launch_advance(const AdvanceArgs& a, hipStream_t stream);
 hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t stream);
 hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t stream);
 

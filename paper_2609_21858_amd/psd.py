@@ -55,6 +55,25 @@ class Block(ctypes.Structure):
     ]
 
 
+class ToyLM(ctypes.Structure):
+    """psd_toy_lm: the synthetic position-indexed model of psd_toy_logits / psd_generate."""
+    _fields_ = [
+        ("seed", ctypes.c_uint64),
+        ("draft_seed", ctypes.c_uint64),
+        ("sigma", ctypes.c_float),
+        ("alpha", ctypes.c_float),
+        ("tau", ctypes.c_float * 2),
+        ("tau_split", ctypes.c_int32),
+    ]
+
+
+def make_toy_lm(seed: int, draft_seed: int, sigma: float, alpha: float, tau=(1.0, 1.0), tau_split: int = 0) -> ToyLM:
+    lm = ToyLM(seed & 0xFFFFFFFFFFFFFFFF, draft_seed & 0xFFFFFFFFFFFFFFFF, sigma, alpha)
+    lm.tau[0], lm.tau[1] = float(tau[0]), float(tau[1])
+    lm.tau_split = int(tau_split)
+    return lm
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built: run __graft_entry__.build() (hipcc, gfx950)")
@@ -80,6 +99,11 @@ def _load():
         "psd_detect_scores": ([P, vp, i32, i32, i32, vp, vp, vp, vp, vp], i32),
         "psd_detect_scores_pvalue": ([vp, i32, vp, vp, vp, vp], i32),
         "psd_detection_rate": ([i32, vp, i32, ctypes.c_double, vp, vp], i32),
+        "psd_advance": ([P, i32, i32, ctypes.c_int64, vp, vp, vp, ctypes.c_int64, vp, vp, vp, vp, vp], i32),
+        "psd_toy_logits": ([P, ctypes.POINTER(ToyLM), i32, i32, vp, vp, vp, vp], i32),
+        "psd_generate_workspace_bytes": ([P, i32, i32], sz),
+        "psd_generate": ([P, ctypes.POINTER(ToyLM), i32, i32, i32, vp, ctypes.c_int64, vp, sz, i32, i32,
+                          ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_uint32), vp], i32),
     }
     for name, (args, res) in sigs.items():
         f = getattr(lib, name)
@@ -92,7 +116,8 @@ _lib = _load()
 EXPORTS = ("psd_abi_version", "psd_last_error", "psd_workspace_bytes", "psd_workspace_clear",
            "psd_workspace_errors", "psd_draft", "psd_verify", "psd_verify_static", "psd_detect", "psd_detect_pvalue", "psd_philox",
            "psd_context_keys", "psd_clock_values", "psd_set_spin_limit", "psd_detect_scores",
-           "psd_detect_scores_pvalue", "psd_detection_rate")
+           "psd_detect_scores_pvalue", "psd_detection_rate", "psd_advance", "psd_toy_logits",
+           "psd_generate_workspace_bytes", "psd_generate")
 
 
 def lib():
@@ -299,3 +324,52 @@ def clock_values(params: Params, kappa, slot, token, stream=None):
     _check(_lib.psd_clock_values(ctypes.byref(params), n, _ptr(kappa), _ptr(slot), _ptr(token), _ptr(out),
                                  _stream(stream)))
     return out
+
+
+# ---------------------------------------------------------------- multi-block generation
+
+def advance(params: Params, gamma: int, max_len: int, text, length, prefix, start_pos, n_active, out_tokens=None,
+            out_len=None, stream=None):
+    """psd_advance: commit one block (out_len None: set up the first block from the prompts)."""
+    B = int(text.shape[0])
+    _check(_lib.psd_advance(ctypes.byref(params), B, gamma, int(max_len), _ptr(out_tokens), _ptr(out_len),
+                            _ptr(text), int(text.stride(0)), _ptr(length),
+                            _ptr(prefix) if prefix is not None and prefix.numel() else None, _ptr(start_pos),
+                            _ptr(n_active), _stream(stream)))
+
+
+def toy_logits(params: Params, lm: ToyLM, gamma: int, start_pos, drafts: bool = True, stream=None):
+    """psd_toy_logits -> (target rows [B][gamma+1][V], draft rows [B][K][gamma][V] or None)."""
+    B, V, K = int(start_pos.shape[0]), params.vocab, params.num_drafts
+    dt = torch.bfloat16 if params.dtype == PSD_BF16 else torch.float32
+    tl = torch.empty((B, gamma + 1, V), dtype=dt, device=start_pos.device)
+    dl = torch.empty((B, K, gamma, V), dtype=dt, device=start_pos.device) if drafts else None
+    _check(_lib.psd_toy_logits(ctypes.byref(params), ctypes.byref(lm), B, gamma, _ptr(start_pos), _ptr(tl), _ptr(dl),
+                               _stream(stream)))
+    return tl, dl
+
+
+def generate_workspace_bytes(params: Params, batch: int, gamma: int) -> int:
+    return int(_lib.psd_generate_workspace_bytes(ctypes.byref(params), batch, gamma))
+
+
+def generate(params: Params, lm: ToyLM, prompts, n_pos: int, gamma: int, check_every: int = 16,
+             use_graph: bool = False, ws=None, stream=None):
+    """psd_generate: n_pos tokens after each prompt (int32 [B][m], m = ctx_window) on the device.
+    Returns (text int32 [B][m + n_pos], blocks, error bits)."""
+    B, m = int(prompts.shape[0]), params.ctx_window
+    assert prompts.shape[1] == m
+    text = torch.full((B, m + n_pos), -1, dtype=torch.int32, device=prompts.device)
+    text[:, :m] = prompts
+    if ws is None:
+        n = generate_workspace_bytes(params, B, gamma)
+        if n == 0:
+            raise PsdError(PSD_E_ARG, "invalid parameters for generation")
+        ws = torch.empty(n, dtype=torch.uint8, device=prompts.device)
+    blocks = ctypes.c_int32(0)
+    bits = ctypes.c_uint32(0)
+    _check(_lib.psd_generate(ctypes.byref(params), ctypes.byref(lm), B, gamma, n_pos, _ptr(text), int(text.stride(0)),
+                             _ptr(ws), ws.numel(), check_every, 1 if use_graph else 0, ctypes.byref(blocks),
+                             ctypes.byref(bits), _stream(stream)))
+    return text, int(blocks.value), int(bits.value)
+

@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol(psd):
     for n in names:
         assert hasattr(psd.lib(), n), n
         assert n in psd.EXPORTS
-    assert psd.lib().psd_abi_version() == 3
+    assert psd.lib().psd_abi_version() == 4
 
 
 def test_workspace_bytes(psd):
@@ -120,6 +120,44 @@ def test_truncation_workspace(psd):
         p = psd.make_params(1, 1000, 2, 4, mode=mode, top_k=5, top_p=0.5)
         assert _verify(psd, p, tl=None) == psd.PSD_E_ARG
         assert _verify(psd, p, target_rows=3) == psd.PSD_E_ARG
+
+
+def test_generation_entry_points_reject_bad_args(psd):
+    """psd_advance, psd_toy_logits and psd_generate validate every argument before any
+    launch (dummy device addresses are never dereferenced)."""
+    L = psd.lib()
+    p = psd.make_params(1, 1000, 2, 3)
+    i64 = ctypes.c_int64
+
+    def adv(B=2, G=3, max_len=10, stride=12, ot=FAKE, ol=FAKE, text=FAKE, length=FAKE, prefix=FAKE, start=FAKE,
+            act=FAKE, params=p):
+        return L.psd_advance(ctypes.byref(params), B, G, i64(max_len), ot, ol, text, i64(stride), length, prefix,
+                             start, act, None)
+    assert adv(B=0) == psd.PSD_E_ARG and adv(G=0) == psd.PSD_E_ARG and adv(G=33) == psd.PSD_E_ARG
+    assert adv(max_len=3) == psd.PSD_E_ARG          # max_len must exceed the prompt (m = 3)
+    assert adv(stride=9) == psd.PSD_E_ARG           # rows shorter than max_len
+    for k in ("text", "length", "prefix", "start", "act"):
+        assert adv(**{k: None}) == psd.PSD_E_ARG, k
+    assert adv(ot=None) == psd.PSD_E_ARG            # out_len without out_tokens
+    lm = psd.make_toy_lm(1, 2, 3.0, 1.2)
+    assert L.psd_toy_logits(ctypes.byref(p), None, 2, 3, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
+    bad = psd.make_toy_lm(1, 2, float("nan"), 1.2)
+    assert L.psd_toy_logits(ctypes.byref(p), ctypes.byref(bad), 2, 3, FAKE, FAKE, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_toy_logits(ctypes.byref(p), ctypes.byref(lm), 2, 3, None, FAKE, FAKE, None) == psd.PSD_E_ARG
+    assert L.psd_toy_logits(ctypes.byref(p), ctypes.byref(lm), 2, 3, FAKE, None, FAKE, None) == psd.PSD_E_ARG
+    n = psd.generate_workspace_bytes(p, 2, 3)
+    assert n > psd.workspace_bytes(p, 2, 3) and n % 256 == 0
+    assert psd.generate_workspace_bytes(psd.make_params(1, 2000, 2, 3), 2, 3) > n
+    assert psd.generate_workspace_bytes(psd.make_params(1, 0, 2, 3), 2, 3) == 0
+    blocks, bits = ctypes.c_int32(0), ctypes.c_uint32(0)
+
+    def gen(n_pos=8, stride=11, ws=FAKE, nb=n, every=4, text=FAKE, lmp=lm):
+        return L.psd_generate(ctypes.byref(p), ctypes.byref(lmp) if lmp else None, 2, 3, n_pos, text, i64(stride),
+                              ws, nb, every, 0, ctypes.byref(blocks), ctypes.byref(bits), None)
+    assert gen(n_pos=0) == psd.PSD_E_ARG and gen(stride=10) == psd.PSD_E_ARG and gen(every=0) == psd.PSD_E_ARG
+    assert gen(text=None) == psd.PSD_E_ARG and gen(lmp=None) == psd.PSD_E_ARG
+    assert gen(ws=None) == psd.PSD_E_WORKSPACE and gen(nb=n - 1) == psd.PSD_E_WORKSPACE
+    assert gen(ws=FAKE + 16) == psd.PSD_E_WORKSPACE
 
 
 def test_draft_and_detect_reject_bad_args(psd):

@@ -167,6 +167,105 @@ def zipf_probs(V: int, sigma: float, alpha: float, T: float, seed: int):
     return logits, p
 
 
+# ---------------------------------------------------------------- position-indexed toy model
+
+@dataclasses.dataclass(frozen=True)
+class ToyModel:
+    """A synthetic position-indexed language model for multi-block generation.
+
+    The target row of sequence b at absolute position t is a fixed function of
+    (seed, b, t) and drafter k's row adds noise keyed by (draft_seed, b, k, t), both
+    built from integer hashes (SplitMix64 per row, Wellons' lowbias32 per element)
+    and fp32 operations rounded one at a time, so that any implementation of the
+    definition gives the same bits (the library's psd_toy_logits is another one):
+
+    * R_T = sm(seed ^ sm(b << 32 | t)), R_P = sm(R_T ^ 0xD1B54A32D192ED03),
+      R_D = sm(draft_seed ^ sm((k + 1) << 56 ^ b << 32 ^ t)), t mod 2^32;
+    * rank r(v) = (a v + c) mod V, c = R_P mod V, a = (R_P >> 32) mod V (0 -> 1)
+      moved up (V wraps to 1) to the first value coprime to V;
+    * x = lo32(R) + v * 0x9E3779B9 mod 2^32; a word h gives the uniforms
+      (lo16(h) + 1/2) / 2^16 and (hi16(h) + 1/2) / 2^16;
+    * target: n = (4 uniforms of lowbias32(x), lowbias32(x ^ hi32(R_T)) summed - 2) * sqrt(3),
+      q(r) = fp32(bits(fp32(1 + r)) - 0x3F800000) (2^23 x a piecewise-linear log2),
+      w = fp32(-alpha ln 2 / 2^23), z = sigma * n + w * q(r(v));
+    * draft: n' = (2 uniforms of lowbias32(x) summed - 1) * sqrt(6) (x from R_D),
+      d = z + tau_b * n', tau_b = tau[0] for b < tau_split, else tau[1];
+    * bf16 rows: round-to-nearest-even of the fp32 values.
+    """
+    seed: int
+    draft_seed: int
+    sigma: float
+    alpha: float
+    tau: tuple = (1.0, 1.0)
+    tau_split: int = 0
+
+    def _words(self, b: int, t: int):
+        t32 = t & 0xFFFFFFFF
+        rt = splitmix64(self.seed ^ splitmix64(((b << 32) | t32) & MASK64))
+        rp = splitmix64(rt ^ 0xD1B54A32D192ED03)
+        return rt, rp
+
+    def target_row(self, b: int, t: int, V: int, bf16: bool = True, fp32_values: bool = False):
+        """float32 [V]: the target row (bf16 values widened, unless bf16 is False)."""
+        import numpy as np
+        rt, rp = self._words(b, t)
+        c = rp % V
+        a = (rp >> 32) % V
+        if a == 0:
+            a = 1
+        while _gcd(a, V) != 1:
+            a = 1 if a + 1 == V else a + 1
+        v = np.arange(V, dtype=np.uint32)
+        x = np.uint32(rt & 0xFFFFFFFF) + v * np.uint32(0x9E3779B9)
+        u4 = _two_uniforms(_lowbias32(x)) + _two_uniforms(_lowbias32(x ^ np.uint32(rt >> 32)))
+        n = (u4 - np.float32(2.0)) * np.float32(1.7320508075688772)
+        r = (np.arange(V, dtype=np.int64) * a + c) % V
+        q = ((r + 1).astype(np.float32).view(np.uint32) - np.uint32(0x3F800000)).astype(np.int32).astype(np.float32)
+        w = np.float32(-float(np.float32(self.alpha)) * 0.69314718055994531 * 2.0 ** -23)
+        z = np.float32(self.sigma) * n + w * q
+        return z if (fp32_values or not bf16) else _bf16_rne(z)
+
+    def draft_row(self, b: int, k: int, t: int, V: int, bf16: bool = True):
+        """float32 [V]: drafter k's row at (b, t)."""
+        import numpy as np
+        z = self.target_row(b, t, V, fp32_values=True)
+        rd = splitmix64(self.draft_seed ^ splitmix64((((k + 1) << 56) ^ (b << 32) ^ (t & 0xFFFFFFFF)) & MASK64))
+        x = np.uint32(rd & 0xFFFFFFFF) + np.arange(V, dtype=np.uint32) * np.uint32(0x9E3779B9)
+        n2 = (_two_uniforms(_lowbias32(x)) - np.float32(1.0)) * np.float32(2.449489742783178)
+        tau = np.float32(self.tau[0] if b < self.tau_split else self.tau[1])
+        d = z + tau * n2
+        return _bf16_rne(d) if bf16 else d
+
+
+def _gcd(a: int, b: int) -> int:
+    while b:
+        a, b = b, a % b
+    return a
+
+
+def _lowbias32(x):
+    import numpy as np
+    x = x ^ (x >> np.uint32(16))
+    x = x * np.uint32(0x7FEB352D)
+    x = x ^ (x >> np.uint32(15))
+    x = x * np.uint32(0x846CA68B)
+    return x ^ (x >> np.uint32(16))
+
+
+def _two_uniforms(h):
+    import numpy as np
+    return ((h & np.uint32(0xFFFF)).astype(np.float32) + (h >> np.uint32(16)).astype(np.float32)
+            + np.float32(1.0)) * np.float32(2.0 ** -16)
+
+
+def _bf16_rne(z):
+    """float32 array -> the bf16 round-to-nearest-even values, as float32."""
+    import numpy as np
+    u = np.asarray(z, np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return (r << np.uint32(16)).view(np.float32)
+
+
 def mib(n_bytes: int) -> float:
     return n_bytes / float(1 << 20)
 
@@ -176,4 +275,4 @@ def ceil_div(a: int, b: int) -> int:
 
 
 __all__ = ["Workload", "WORKLOADS", "custom", "make_block", "as_f32_numpy", "uniform_tokens", "splitmix64",
-           "zipf_probs", "mib", "ceil_div"]
+           "zipf_probs", "mib", "ceil_div", "ToyModel"]
