@@ -4,16 +4,18 @@
 // top-p; Alg. "Batched-target direct-top-k MPFR speculative sampling"): every
 // token outside a row's kept set has probability 0.  With at most 256 kept tokens
 // per row the race needs no pruning, so this path has two kernels:
-//  * topk_select_kernel, one workgroup per row, one pass over the row in HBM: every
-//    thread keeps the 8 best (key, index) pairs of its elements (order-preserving
-//    keys; ties to the lowest index) through a branch-free max/min network and
-//    remembers the best pair it dropped; bisections over the kept pairs' keys and
-//    then their indices give the k-th best pair of the 2048 kept ones, which is the
-//    row's k-th best unless some thread dropped a pair at least as good -- such rows
-//    (rare: it needs 9 of the row's k best in one thread, or many ties at the cut)
-//    are selected again by exact radix passes.  Then the kept list is sorted by
-//    (logit descending, index ascending), its top-p prefix and the log-sum-exp of the
-//    kept set at the row's temperature are formed in fp64;
+//  * topk_select_kernel, one workgroup per row, one pass over the row in HBM: each
+//    wave streams its share of the row against a running threshold of its own and
+//    appends the logits that reach it to an LDS buffer (ballot and lane prefix, no
+//    atomics); a full buffer is compacted by a wave-level bisection that raises the
+//    threshold to the top_k-th largest key it holds.  Every logit left out is below
+//    the row's top_k-th largest, so the union of the buffers holds the top-k set,
+//    ties at the cut included; block-wide bisections over its keys and then its
+//    indices pick the k largest (order-preserving keys, ties to the lowest index).
+//    Rows whose ties at the cut overflow a buffer are selected by exact radix passes
+//    instead.  Then the kept list is sorted by (logit descending, index ascending),
+//    its top-p prefix and the log-sum-exp of the kept set at the row's temperature
+//    are formed in fp64;
 //  * topk_race_kernel, one workgroup per sequence with one wave per independent
 //    chain (each draft path, the target chain): the block's races in dependency
 //    order over the lists, with exact fp64 clocks of every (token, slot) -- distinct
@@ -34,7 +36,6 @@ namespace psd {
 namespace {
 
 constexpr int kTBlock = 256;
-constexpr int kKeep = 8;    // pairs each thread keeps while streaming its elements
 constexpr int kUnroll = 4;  // 16-byte loads in flight per thread
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -49,86 +50,85 @@ __device__ __forceinline__ uint32_t key_f32(uint32_t u) {
 __device__ __forceinline__ float val_f32(uint32_t k) {
     return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
-__device__ __forceinline__ uint32_t key_bf16(uint32_t b) {
-    if (b == 0x8000u) b = 0u;
-    return (b & 0x8000u) ? (~b & 0xFFFFu) : (b | 0x8000u);
-}
-__device__ __forceinline__ float val_bf16(uint32_t k) {
-    const uint32_t b = (k & 0x8000u) ? (k & 0x7FFFu) : (~k & 0xFFFFu);
-    return __uint_as_float(b << 16);
-}
-
-// A kept pair packs (key, kIdx - local element number): a larger pair is a larger
-// logit, or the same logit at a lower index.  bf16 keys are 16 bits, so a pair fits
-// 32 bits (at most 2^19 / 256 elements per thread); fp32 pairs take 64 bits.
-template <bool BF16>
-struct Sel;
-template <>
-struct Sel<true> {
-    using P = uint32_t;
-    static constexpr int kShift = 16, kKeyBits = 16, kEPT = 8;
-    static constexpr uint32_t kNegInf = 0x007Fu, kIdx = 0xFFFFu, kNegInfBits = 0xFF80u;
-    static __device__ __forceinline__ uint32_t key(uint32_t bits) { return key_bf16(bits); }
-    static __device__ __forceinline__ float val(uint32_t k) { return val_bf16(k); }
-};
-template <>
-struct Sel<false> {
-    using P = uint64_t;
-    static constexpr int kShift = 32, kKeyBits = 32, kEPT = 4;
-    static constexpr uint32_t kNegInf = 0x007FFFFFu, kIdx = 0xFFFFFFFFu, kNegInfBits = 0xFF800000u;
-    static __device__ __forceinline__ uint32_t key(uint32_t bits) { return key_f32(bits); }
-    static __device__ __forceinline__ float val(uint32_t k) { return val_f32(k); }
-};
-
 __device__ __forceinline__ float tload(const unsigned char* row, bool bf16, int v) {
     return bf16 ? __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16) : ((const float*)row)[v];
 }
 
+constexpr int kWaves = kTBlock / 64;
+constexpr int kWaveCap = 512;  // candidates a wave holds
+constexpr int kSub = 2;        // elements per lane between buffer checks (at most 128 appends)
+
 // ---------------------------------------------------------------- block helpers
 
 struct SelShared {
-    int hist[2048];  // radix passes only
+    union {
+        struct {
+            uint32_t key[kWaves][kWaveCap];  // each wave's candidates: order-preserving key,
+            int32_t idx[kWaves][kWaveCap];   // token index
+        } wb;
+        int hist[2048];  // radix passes (the candidates are given up first)
+    } u;
     int tok[kMaxTopK];
     float val[kMaxTopK];
     int stok[kMaxTopK];
     float sval[kMaxTopK];
-    int red[2][kTBlock / 64];
-    double dred[kTBlock / 64];
+    int red[2][kWaves];
+    double dred[kWaves];
     double dsel;
-    int s4[kTBlock / 64];
-    int n_keep;
+    int s4[kWaves];
+    int wcount[kWaves], wover[kWaves];
+    int n_keep, n_fin;
     uint32_t prefix;
     int above;
 };
 
-// Sum of one int per thread over the workgroup; every thread gets it.  The two LDS
-// buffers alternate (parity `it`), so one barrier per call suffices.
-__device__ __forceinline__ int block_sum(SelShared& sm, int x, int& it) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    int* r = sm.red[it & 1];
-    ++it;
-    if ((threadIdx.x & 63) == 0) r[threadIdx.x >> 6] = x;
-    __syncthreads();
-    int t = 0;
-#pragma unroll
-    for (int w = 0; w < kTBlock / 64; ++w) t += r[w];
-    return t;
-}
-
-// Inclusive prefix sum of one int per thread (thread order); *total gets the sum.
-__device__ __forceinline__ int block_incl_sum(SelShared& sm, int x, int& total) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+__device__ __forceinline__ int wave_incl(int x) {
+    const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
         const int y = __shfl_up(x, o);
         if (lane >= o) x += y;
     }
-    if (lane == 63) sm.s4[wave] = x;
+    return x;
+}
+
+// Lanes below this one whose bit is set in m.
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Entries of the wave (Q per lane) passing a test, counted with ballots (scalar
+// popcounts: no lane shuffles).
+template <int Q, typename F>
+__device__ __forceinline__ int wave_count(F&& pass) {
+    int c = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) c += __popcll(__ballot(pass(q)));
+    return c;
+}
+
+// Sum over the workgroup of a wave-uniform count; the two LDS buffers alternate
+// (parity `it`), so one barrier per call suffices.
+__device__ __forceinline__ int block_sum_waves(SelShared& sm, int wave_total, int& it) {
+    int* r = sm.red[it & 1];
+    ++it;
+    if ((threadIdx.x & 63) == 0) r[threadIdx.x >> 6] = wave_total;
+    __syncthreads();
+    int t = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) t += r[w];
+    return t;
+}
+
+// Inclusive prefix sum of one int per thread (thread order); *total gets the sum.
+__device__ __forceinline__ int block_incl_sum(SelShared& sm, int x, int& total) {
+    const int wave = threadIdx.x >> 6;
+    x = wave_incl(x);
+    if ((threadIdx.x & 63) == 63) sm.s4[wave] = x;
     __syncthreads();
     int base = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < kTBlock / 64; ++w) {
+    for (int w = 0; w < kWaves; ++w) {
         if (w < wave) base += sm.s4[w];
         tot += sm.s4[w];
     }
@@ -149,7 +149,7 @@ __device__ __forceinline__ double block_incl_sum_f64(SelShared& sm, double x, do
     __syncthreads();
     double base = 0.0, tot = 0.0;
 #pragma unroll
-    for (int w = 0; w < kTBlock / 64; ++w) {
+    for (int w = 0; w < kWaves; ++w) {
         if (w < wave) base += sm.dred[w];
         tot += sm.dred[w];
     }
@@ -160,100 +160,188 @@ __device__ __forceinline__ double block_incl_sum_f64(SelShared& sm, double x, do
 
 // ---------------------------------------------------------------- one-pass selection
 
-// Insert x into the descending list r (the smallest of the nine falls out and, if
-// larger than *dropped, becomes the new best dropped pair).
-template <typename P>
-__device__ __forceinline__ void keep_insert(P (&r)[kKeep], P& dropped, P x) {
+// Keys of bf16 logits differ only in their top 16 bits (the low half is 0x0000 or
+// 0xFFFF by sign), so searches over them stop at bit 16; one key class is one value.
+template <bool BF16>
+struct KeyBits {
+    static constexpr int kLow = BF16 ? 16 : 0;
+};
+
+// One wave's candidate buffer: raise its threshold to the need-th largest key class it
+// holds and drop the entries below it (ties stay).  Every dropped key is below the
+// row's need-th largest, since the buffer's need-th largest is at most the row's.
+// Returns the new count; *t gets the threshold key.
+template <bool BF16>
+__device__ __forceinline__ int wave_compact(uint32_t* bk, int32_t* bi, int cnt, int need, uint32_t& t) {
+    constexpr int Q = kWaveCap / 64;
+    const int lane = threadIdx.x & 63;
+    uint32_t kk[Q];
+    int32_t ii[Q];
 #pragma unroll
-    for (int q = 0; q < kKeep; ++q) {
-        const P hi = r[q] > x ? r[q] : x;
-        x = r[q] > x ? x : r[q];
-        r[q] = hi;
+    for (int q = 0; q < Q; ++q) {
+        const int j = lane + 64 * q;
+        kk[q] = j < cnt ? bk[j] : 0u;
+        ii[q] = j < cnt ? bi[j] : 0;
     }
-    dropped = dropped > x ? dropped : x;
+    uint32_t th = 0u;
+    for (int bit = 31; bit >= KeyBits<BF16>::kLow; --bit) {
+        const uint32_t cand = th | (1u << bit);
+        if (wave_count<Q>([&](int q) { return kk[q] >= cand; }) >= need) th = cand;
+    }
+    int kc = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) kc += kk[q] >= th;
+    const int incl = wave_incl(kc);
+    const int total = __shfl(incl, 63);
+    int o = incl - kc;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        if (kk[q] >= th) {
+            bk[o] = kk[q];
+            bi[o] = ii[q];
+            ++o;
+        }
+    t = th;
+    return total;
 }
 
-// Stream the row: thread t's elements are, chunk by chunk, the kEPT consecutive
-// tokens at c * 256 * kEPT + t * kEPT; local element number j = c * kEPT + i.
 template <bool BF16>
-__device__ __forceinline__ void stream_row(const unsigned char* row, int V, typename Sel<BF16>::P (&r)[kKeep],
-                                           typename Sel<BF16>::P& dropped, int& nfin) {
-    using S = Sel<BF16>;
-    using P = typename S::P;
-    constexpr int EPT = S::kEPT, CH = kTBlock * EPT;
+__device__ __forceinline__ uint32_t elem_bits(const uint32_t (&w)[4], int i) {
+    return BF16 ? ((i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16)) : w[i];
+}
+
+// Stream the row, one wave per 64 x kEPT-token chunk in turn (wave w takes chunks w,
+// w + 4, ...; four 16-byte loads per lane in flight): every finite logit at least the
+// wave's threshold (initially the lowest finite value) joins the wave's buffer
+// (ballot + lane prefix, no atomics); a chunk is skipped with one ballot when no
+// lane's maximum reaches the threshold, and a buffer that could not take kSub more
+// logits per lane is compacted.  Returns false if ties at the cut fill a buffer
+// (then the caller selects by radix passes).
+template <bool BF16>
+__device__ __forceinline__ bool stream_row(SelShared& sm, const unsigned char* row, int V, int top_k) {
+    constexpr int EPT = BF16 ? 8 : 4, WCH = 64 * EPT, STEP = kWaves * kUnroll;
     constexpr size_t ES = BF16 ? 2 : 4;
-    const int tid = threadIdx.x;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const bool vec = ((uintptr_t)row & 15u) == 0;
-    for (int c0 = 0, cn = 0; c0 < V; c0 += CH * kUnroll, cn += kUnroll) {
-        uint32_t w[kUnroll][4];
+    const int nch = (V + WCH - 1) / WCH;
+    uint32_t* bk = sm.u.wb.key[w];
+    int32_t* bi = sm.u.wb.idx[w];
+    int cnt = 0;
+    float th = -3.40282347e38f;  // the lowest finite value: -inf never joins
+    bool over = false;
+    for (int c0 = w; c0 < nch; c0 += STEP) {
+        uint32_t wv[kUnroll][4];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int base = c0 + u * CH + tid * EPT;
+            const int base = (c0 + u * kWaves) * WCH + lane * EPT;
             if (vec && base + EPT <= V) {
                 const u32x4 q = __builtin_nontemporal_load((const u32x4*)(row + (size_t)base * ES));
-                w[u][0] = q.x;
-                w[u][1] = q.y;
-                w[u][2] = q.z;
-                w[u][3] = q.w;
+                wv[u][0] = q.x;
+                wv[u][1] = q.y;
+                wv[u][2] = q.z;
+                wv[u][3] = q.w;
             } else {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) w[u][i] = 0u;
+                for (int i = 0; i < 4; ++i) wv[u][i] = BF16 ? 0xFF80FF80u : 0xFF800000u;  // -inf
 #pragma unroll
                 for (int i = 0; i < EPT; ++i) {
                     const int v = base + i;
-                    if (BF16) {
-                        const uint32_t bits = v < V ? (uint32_t)((const uint16_t*)row)[v] : S::kNegInfBits;
-                        w[u][i >> 1] |= bits << (16 * (i & 1));
-                    } else {
-                        w[u][i] = v < V ? ((const uint32_t*)row)[v] : S::kNegInfBits;
+                    if (v < V) {
+                        if (BF16) {
+                            const uint32_t h = ((const uint16_t*)row)[v];
+                            wv[u][i >> 1] = (wv[u][i >> 1] & ~(0xFFFFu << (16 * (i & 1)))) | (h << (16 * (i & 1)));
+                        } else {
+                            wv[u][i] = ((const uint32_t*)row)[v];
+                        }
                     }
                 }
             }
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+        for (int u = 0; u < kUnroll; ++u) {
+            float mx = __uint_as_float(elem_bits<BF16>(wv[u], 0));
 #pragma unroll
-            for (int i = 0; i < EPT; ++i) {
-                const uint32_t bits = BF16 ? (w[u][i >> 1] >> (16 * (i & 1))) & 0xFFFFu : w[u][i];
-                const uint32_t k = S::key(bits);
-                nfin += k > S::kNegInf;
-                const uint32_t j = (uint32_t)((cn + u) * EPT + i);
-                keep_insert<P>(r, dropped, ((P)k << S::kShift) | (P)(S::kIdx - j));
+            for (int i = 1; i < EPT; ++i) mx = fmaxf(mx, __uint_as_float(elem_bits<BF16>(wv[u], i)));
+            if (!__ballot(mx >= th && !over)) continue;
+            const int base = (c0 + u * kWaves) * WCH + lane * EPT;
+#pragma unroll
+            for (int i0 = 0; i0 < EPT; i0 += kSub) {
+#pragma unroll
+                for (int i = i0; i < i0 + kSub; ++i) {
+                    const uint32_t bits = elem_bits<BF16>(wv[u], i);
+                    const bool p = __uint_as_float(bits) >= th && !over;
+                    const uint64_t m = __ballot(p);
+                    if (m) {
+                        if (p) {
+                            const int pos = cnt + lanes_below(m);
+                            bk[pos] = key_f32(bits);
+                            bi[pos] = base + i;
+                        }
+                        cnt += __popcll(m);
+                    }
+                }
+                if (cnt > kWaveCap - 64 * kSub) {
+                    uint32_t tk;
+                    cnt = wave_compact<BF16>(bk, bi, cnt, top_k, tk);
+                    th = val_f32(tk);
+                    if (cnt > kWaveCap - 64 * kSub) {  // ties at the cut: stop collecting
+                        over = true;
+                        cnt = 0;
+                    }
+                }
             }
+        }
     }
+    if (lane == 0) {
+        sm.wcount[w] = cnt;
+        sm.wover[w] = over ? 1 : 0;
+    }
+    __syncthreads();
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) ok = ok && !sm.wover[q];
+    return ok;
 }
 
-// Exact radix selection of the need largest (ties to the lowest index) into
-// sm.tok / sm.val, unsorted: three digit passes (11, 11, 10 bits) find the need-th
-// largest key, a fourth collects.  Reads the row four times.
+// Exact radix selection of the need = min(top_k, finite logits) largest (ties to the
+// lowest index) into sm.tok / sm.val, unsorted: three digit passes (11, 11, 10 bits)
+// find the need-th largest key, a fourth collects.  Reads the row four times.
+// Returns need.
 template <bool BF16>
-__device__ void radix_select(SelShared& sm, const unsigned char* row, int V, int need) {
+__device__ int radix_select(SelShared& sm, const unsigned char* row, int V, int top_k) {
     const int tid = threadIdx.x;
     const int shifts[3] = {21, 10, 0};
     const int widths[3] = {11, 11, 10};
     if (tid == 0) {
         sm.prefix = 0u;
         sm.above = 0;
+        sm.n_fin = 0;
     }
+    int need = 0;
     for (int pass = 0; pass < 3; ++pass) {
         const int nb = 1 << widths[pass];
-        for (int i = tid; i < nb; i += kTBlock) sm.hist[i] = 0;
+        for (int i = tid; i < nb; i += kTBlock) sm.u.hist[i] = 0;
         __syncthreads();
         const uint32_t pre = sm.prefix;
         const int hi_shift = shifts[pass] + widths[pass];  // bits above this digit must equal the prefix
+        int nf = 0;
         for (int v = tid; v < V; v += kTBlock) {
             const float x = tload(row, BF16, v);
             if (x == -INFINITY) continue;
+            ++nf;
             const uint32_t k = key_f32(__float_as_uint(x));
             if (hi_shift < 32 && (k >> hi_shift) != (pre >> hi_shift)) continue;
-            atomicAdd(&sm.hist[(k >> shifts[pass]) & (uint32_t)(nb - 1)], 1);
+            atomicAdd(&sm.u.hist[(k >> shifts[pass]) & (uint32_t)(nb - 1)], 1);
         }
+        if (pass == 0) atomicAdd(&sm.n_fin, nf);
         __syncthreads();
+        if (pass == 0) need = min(top_k, sm.n_fin);
+        if (need == 0) return 0;
         if (tid == 0) {
             int acc = sm.above, b = nb - 1;
             for (; b > 0; --b) {
-                if (acc + sm.hist[b] >= need) break;
-                acc += sm.hist[b];
+                if (acc + sm.u.hist[b] >= need) break;
+                acc += sm.u.hist[b];
             }
             sm.above = acc;
             sm.prefix = pre | ((uint32_t)b << shifts[pass]);
@@ -294,14 +382,12 @@ __device__ void radix_select(SelShared& sm, const unsigned char* row, int V, int
         ties_before += total;
     }
     __syncthreads();
+    return need;
 }
 
 // One row: kept list, its length and the LSE of the kept set.
 template <bool BF16>
 __global__ __launch_bounds__(kTBlock) void topk_select_kernel(TopkSelectArgs a) {
-    using S = Sel<BF16>;
-    using P = typename S::P;
-    constexpr int EPT = S::kEPT, CH = kTBlock * EPT;
     __shared__ SelShared sm;
     const int tid = threadIdx.x;
     const bool s1 = (int)blockIdx.x >= a.seg[0].n_rows;
@@ -311,16 +397,71 @@ __global__ __launch_bounds__(kTBlock) void topk_select_kernel(TopkSelectArgs a) 
     const int rid = G.row_id_base + (G.group > 0 ? (r / G.group) * G.group_stride + r % G.group : r);
     const int lse_at = G.lse_index_base + (G.group > 0 ? (r / G.group) * G.lse_group_stride + r % G.group : r);
 
-    P kept[kKeep];
-#pragma unroll
-    for (int q = 0; q < kKeep; ++q) kept[q] = 0;
-    P dropped = 0;
-    int nfin = 0;
-    stream_row<BF16>(row, a.V, kept, dropped, nfin);
-
     int it = 0;
-    const int n_fin = block_sum(sm, nfin, it);
-    const int need = min(a.top_k, n_fin);
+    int need;
+    if (!stream_row<BF16>(sm, row, a.V, a.top_k)) {
+        __syncthreads();  // the candidate buffers are reused by the radix passes
+        if (tid == 0 && a.radix_rows) atomicAdd(a.radix_rows, 1u);
+        need = radix_select<BF16>(sm, row, a.V, a.top_k);
+    } else {
+        // the union of the wave buffers holds every logit at least the row's top_k-th
+        // largest (ties included), or every finite logit when there are fewer
+        constexpr int Q = kWaves * kWaveCap / kTBlock;
+        constexpr int PW = kWaveCap / kTBlock;  // entries of one wave's buffer per thread
+        uint32_t kk[Q];
+        int32_t ii[Q];
+        int tot = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) tot += sm.wcount[w];
+        need = min(a.top_k, tot);
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int w = q / PW, p = tid + kTBlock * (q % PW);
+            const bool ok = p < sm.wcount[w];
+            kk[q] = ok ? sm.u.wb.key[w][p] : 0u;
+            ii[q] = ok ? sm.u.wb.idx[w][p] : 0;
+        }
+        if (need > 0) {
+            // the need-th largest key class: largest t with #{key >= t} >= need
+            uint32_t t = 0u;
+            for (int bit = 31; bit >= KeyBits<BF16>::kLow; --bit) {
+                const uint32_t cand = t | (1u << bit);
+                if (block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= cand; }), it) >= need) t = cand;
+            }
+            // keys of the next class up (key >= t_up) are strictly larger logits
+            const uint32_t t_up = t + (1u << KeyBits<BF16>::kLow);
+            const int n_gt = block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= t_up; }), it);
+            const int n_ge = block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= t; }), it);
+            const int take = need - n_gt;  // ties at t to keep, lowest indices first
+            int xmax = 0x7FFFFFFF;         // keep the ties with index <= xmax
+            if (n_ge - n_gt > take) {
+                // the take-th smallest index among the tied entries: largest x with #{index < x} < take
+                int x = 0;
+                for (int bit = 18; bit >= 0; --bit) {
+                    const int cand = x | (1 << bit);
+                    if (block_sum_waves(sm, wave_count<Q>([&](int q) {
+                                            return kk[q] >= t && kk[q] < t_up && ii[q] < cand;
+                                        }),
+                                        it) < take)
+                        x = cand;
+                }
+                xmax = x;
+            }
+            int kc = 0;
+#pragma unroll
+            for (int q = 0; q < Q; ++q) kc += kk[q] >= t_up || (kk[q] >= t && ii[q] <= xmax);
+            int total;
+            int off = block_incl_sum(sm, kc, total) - kc;
+#pragma unroll
+            for (int q = 0; q < Q; ++q)
+                if ((kk[q] >= t_up || (kk[q] >= t && ii[q] <= xmax)) && off < kMaxTopK) {
+                    sm.tok[off] = ii[q];
+                    sm.val[off] = val_f32(kk[q]);
+                    ++off;
+                }
+            __syncthreads();
+        }
+    }
     if (need == 0) {
         if (tid == 0) {
             a.list_len[rid] = 0;
@@ -328,64 +469,6 @@ __global__ __launch_bounds__(kTBlock) void topk_select_kernel(TopkSelectArgs a) 
             if (G.lse_out) G.lse_out[lse_at] = -INFINITY;
         }
         return;
-    }
-    // the need-th largest key among the kept pairs: largest t with #{key >= t} >= need
-    auto count_ge = [&](uint32_t t) {
-        int c = 0;
-#pragma unroll
-        for (int q = 0; q < kKeep; ++q) c += (uint32_t)(kept[q] >> S::kShift) >= t;
-        return block_sum(sm, c, it);
-    };
-    uint32_t t = 0;
-    for (int bit = S::kKeyBits - 1; bit >= 0; --bit) {
-        const uint32_t cand = t | (1u << bit);
-        if (count_ge(cand) >= need) t = cand;
-    }
-    // exact unless a thread dropped a pair whose key reaches t (then its thread may
-    // hide one of the row's need best), or fewer than need finite pairs were kept
-    const uint32_t dkey = (uint32_t)(dropped >> S::kShift);
-    const int unsure = block_sum(sm, dkey >= t ? 1 : 0, it);
-    if (t <= S::kNegInf || unsure > 0) {
-        if (tid == 0 && a.radix_rows) atomicAdd(a.radix_rows, 1u);
-        radix_select<BF16>(sm, row, a.V, need);
-    } else {
-        const int n_ge = count_ge(t);
-        const int n_gt = t == 0xFFFFFFFFu ? 0 : count_ge(t + 1u);
-        const int take = need - n_gt;  // ties at t to keep, lowest indices first
-        auto gidx = [&](P p) {
-            const uint32_t j = S::kIdx - (uint32_t)(p & (P)S::kIdx);
-            return (int)((j / EPT) * CH + tid * EPT + j % EPT);
-        };
-        int xmax = 0x7FFFFFFF;  // keep the ties with index <= xmax
-        if (n_ge - n_gt > take) {
-            // the take-th smallest index among the tied pairs: largest x with #{index < x} < take
-            int x = 0;
-            for (int bit = 18; bit >= 0; --bit) {
-                const int cand = x | (1 << bit);
-                int c = 0;
-#pragma unroll
-                for (int q = 0; q < kKeep; ++q)
-                    c += (uint32_t)(kept[q] >> S::kShift) == t && gidx(kept[q]) < cand;
-                if (block_sum(sm, c, it) < take) x = cand;
-            }
-            xmax = x;
-        }
-        // this thread's kept entries are a prefix of its descending list
-        int kc = 0;
-#pragma unroll
-        for (int q = 0; q < kKeep; ++q) {
-            const uint32_t k = (uint32_t)(kept[q] >> S::kShift);
-            kc += k > t || (k == t && gidx(kept[q]) <= xmax);
-        }
-        int total;
-        const int off = block_incl_sum(sm, kc, total) - kc;
-#pragma unroll
-        for (int q = 0; q < kKeep; ++q)
-            if (q < kc && off + q < kMaxTopK) {
-                sm.tok[off + q] = gidx(kept[q]);
-                sm.val[off + q] = S::val((uint32_t)(kept[q] >> S::kShift));
-            }
-        __syncthreads();
     }
     const int n = need;  // both branches leave exactly need entries
     // sort by (logit descending, index ascending): each entry's rank by counting
@@ -406,7 +489,8 @@ __global__ __launch_bounds__(kTBlock) void topk_select_kernel(TopkSelectArgs a) 
     double tot;
     const double inc = block_incl_sum_f64(sm, e, tot);
     int keep = n;
-    if (a.top_p < 1.0f) keep = min(n, block_sum(sm, tid < n && inc / tot < (double)a.top_p ? 1 : 0, it) + 1);
+    if (a.top_p < 1.0f)
+        keep = min(n, block_sum_waves(sm, __popcll(__ballot(tid < n && inc / tot < (double)a.top_p)), it) + 1);
     if (tid == keep - 1) sm.dsel = inc;
     __syncthreads();
     if (tid == 0) {
