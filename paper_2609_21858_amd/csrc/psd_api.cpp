@@ -57,7 +57,9 @@ psd_status check_params(const psd_params* p) {
 // lists of every row when logits are truncated.
 size_t workspace_need(const psd_params* p, int B, int gamma) {
     const psd::WsLayout L = psd::ws_layout(B, p->num_drafts, gamma, p->vocab, p->dtype == PSD_BF16);
-    return p->top_k > 0 ? psd::topk_layout(L, p->top_k).total : L.total;
+    if (p->top_k > 0) return psd::topk_layout(L, p->top_k).total;
+    if (p->mode == PSD_MODE_MPFR) return psd::mpfr_layout(L, B, p->num_drafts, gamma).total;
+    return L.total;
 }
 
 psd_status check_block(const psd_params* p, const psd_block* b) {
@@ -170,6 +172,14 @@ psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_be
     m.s_count = s_count;
     m.T = p->temp_draft;
     m.invT = 1.0f / p->temp_draft;
+    // every draft row of the call streamed once (group maxima, maxima, LSE), then the
+    // contexts sampled depth by depth from those
+    const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
+    const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);
+    m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
+    m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
+    hipError_t e0 = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, vec, stream);
+    if (e0 != hipSuccess) return hip_fail(e0, "MPFR stream kernel launch");
     for (int s = s_begin; s < s_begin + s_count; ++s) {
         m.s = s;
         hipError_t e = psd::launch_mpfr_draft(m, p->dtype == PSD_BF16, vec, p->clocks, stream);

@@ -50,7 +50,24 @@ struct MpfrArgs {
     int V, K, m, B, gamma;
     int s_begin, s_count, s;    // depth of this launch: s_begin <= s < s_begin + s_count
     float T, invT;
+    float* row_gm;              // [B*K*gamma][groups] group maxima of the draft rows, and
+    float* row_max;             // [B*K*gamma] their maxima (draft row ids), written by
+                                // the streaming launch and read by the sampling launches
 };
+
+// Identical drafters: the draft rows' group maxima and maxima, streamed once per call
+// ahead of the depth-by-depth sampling, after the race kernel's workspace.
+struct MpfrLayout {
+    size_t gm, rmax, total;
+};
+inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
+    MpfrLayout M;
+    const size_t rows = (size_t)B * K * gamma;
+    M.gm = L.total;
+    M.rmax = align256(M.gm + rows * (size_t)L.ng * 4);
+    M.total = align256(M.rmax + rows * 4);
+    return M;
+}
 
 // Truncation before the race (top-k, then top-p): per row a kept list of at most
 // top_k (token, logit) pairs, sorted, its length and LSE, after the race kernel's
@@ -155,6 +172,7 @@ hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t strea
 
 hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
 hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
+hipError_t launch_mpfr_stream(const MpfrArgs& a, bool bf16, bool vec, hipStream_t stream);
 hipError_t launch_finish_status(uint32_t* ctrl, uint32_t* status, hipStream_t stream);
 hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream);
 hipError_t launch_pvalue(int n, const double* score, const int32_t* count, double* out_log_p,

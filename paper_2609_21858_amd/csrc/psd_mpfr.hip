@@ -160,37 +160,21 @@ __device__ __forceinline__ void eval_chunk(MShared& sm, const MpfrArgs& a, const
     }
 }
 
-template <bool BF16, bool VEC, int LAYOUT>
-__global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
-    __shared__ MShared sm;
+// Stream one row: log-sum-exp at T (to *lse_out when non-null), the maximum of every
+// 128-token group (to gm, in LDS or global memory) and the row maximum (returned to
+// every thread).  red_* are LDS scratch of kMBlock / 64 entries.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ float mstream_row(const unsigned char* row, int V, float invT, float* gm, float* lse_out,
+                                             float* red_m, float* red_s, float* red_x, float* rowmax) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int b = (int)blockIdx.x / a.K, k = (int)blockIdx.x % a.K, s = a.s;
-    const uint32_t V = (uint32_t)a.V;
-    const int ng = (a.V + 127) / 128, n3 = (ng + 15) / 16, n4 = (n3 + 15) / 16;
-    const size_t esize = BF16 ? 2 : 4;
-    const unsigned char* row = (const unsigned char*)a.logits +
-                               (((size_t)b * a.K + k) * a.s_count + (size_t)(s - a.s_begin)) * (size_t)a.V * esize;
-
-    // ---- the context of path k: the paths whose drafts at depths < s equal its own
-    for (int e = tid; e < a.K * s; e += kMBlock)
-        sm.path_tok[e] = a.draft_tokens[((size_t)b * a.K + e / s) * a.gamma + e % s];
-    if (tid == 0) sm.n_l4 = sm.n_l3 = sm.n_cand = 0;
-    __syncthreads();
-    if (wave == 0) {
-        bool same = lane < a.K;
-        for (int d = 0; d < s && same; ++d) same = sm.path_tok[lane * s + d] == sm.path_tok[k * s + d];
-        const uint64_t bal = __ballot(same);
-        if (lane == 0) sm.mask = (uint32_t)bal;
-    }
-
-    // ---- stream the row: log-sum-exp, group maxima, row maximum
-    const float c2 = a.invT * 1.4426950408889634f;
+    const int ng = (V + 127) / 128;
+    const float c2 = invT * 1.4426950408889634f;
     float mrun = -INFINITY, srun = 0.f, xmax = -INFINITY;
-    const int nstep = (a.V + 2047) / 2048;
+    const int nstep = (V + 2047) / 2048;
     for (int st0 = 0; st0 < nstep; st0 += 4) {
         float x[4][8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) mload8<BF16, VEC>(row, a.V, (st0 + q) * 2048 + 8 * tid, x[q]);
+        for (int q = 0; q < 4; ++q) mload8<BF16, VEC>(row, V, (st0 + q) * 2048 + 8 * tid, x[q]);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             if (st0 + q >= nstep) break;
@@ -199,7 +183,7 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
             for (int i = 1; i < 8; ++i) um = fmaxf(um, x[q][i]);
             const float g = row16_max(um);
             const int gi = (st0 + q) * 16 + (tid >> 4);
-            if ((lane & 15) == 0 && gi < ng) sm.gm[gi] = g;
+            if ((lane & 15) == 0 && gi < ng) gm[gi] = g;
             xmax = fmaxf(xmax, um);
             if (um > -INFINITY) {
                 const float mn = fmaxf(mrun, um * c2);
@@ -223,26 +207,82 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
         }
     }
     if (lane == 0) {
-        sm.red_m[wave] = mrun;
-        sm.red_s[wave] = srun;
-        sm.red_x[wave] = xmax;
+        red_m[wave] = mrun;
+        red_s[wave] = srun;
+        red_x[wave] = xmax;
     }
     __syncthreads();
     if (tid == 0) {
-        float m = sm.red_m[0], sacc = sm.red_s[0], xm = sm.red_x[0];
+        float m = red_m[0], sacc = red_s[0], xm = red_x[0];
         for (int w = 1; w < kMBlock / 64; ++w) {
-            xm = fmaxf(xm, sm.red_x[w]);
-            const float om = sm.red_m[w], os = sm.red_s[w], mn = fmaxf(m, om);
+            xm = fmaxf(xm, red_x[w]);
+            const float om = red_m[w], os = red_s[w], mn = fmaxf(m, om);
             if (mn > -INFINITY) {
                 sacc = (m == -INFINITY ? 0.f : sacc * __builtin_amdgcn_exp2f(m - mn)) +
                        (om == -INFINITY ? 0.f : os * __builtin_amdgcn_exp2f(om - mn));
                 m = mn;
             }
         }
-        sm.rowmax = xm;
-        if (a.draft_lse)
-            a.draft_lse[((size_t)b * a.K + k) * a.gamma + s] =
-                m == -INFINITY ? -INFINITY : (m + __builtin_amdgcn_logf(sacc)) * 0.69314718055994531f;
+        *rowmax = xm;
+        if (lse_out) *lse_out = m == -INFINITY ? -INFINITY : (m + __builtin_amdgcn_logf(sacc)) * 0.69314718055994531f;
+    }
+    __syncthreads();
+    return *rowmax;
+}
+
+// The streaming launch of a call: one workgroup per draft row of depths
+// [s_begin, s_begin + s_count), writing its group maxima, maximum and LSE.
+template <bool BF16, bool VEC>
+__global__ __launch_bounds__(kMBlock) void mpfr_stream_kernel(MpfrArgs a) {
+    __shared__ float red_m[kMBlock / 64], red_s[kMBlock / 64], red_x[kMBlock / 64], rowmax;
+    const int r = (int)blockIdx.x;
+    const int b = r / (a.K * a.s_count), k = (r / a.s_count) % a.K, s = a.s_begin + r % a.s_count;
+    const int ng = (a.V + 127) / 128;
+    const size_t esize = BF16 ? 2 : 4;
+    const unsigned char* row = (const unsigned char*)a.logits + (size_t)r * (size_t)a.V * esize;
+    const size_t rid = ((size_t)b * a.K + k) * a.gamma + s;
+    const float xm = mstream_row<BF16, VEC>(row, a.V, a.invT, a.row_gm + rid * ng,
+                                            a.draft_lse ? a.draft_lse + rid : nullptr, red_m, red_s, red_x, &rowmax);
+    if (threadIdx.x == 0) a.row_max[rid] = xm;
+}
+
+template <bool BF16, bool VEC, int LAYOUT>
+__global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
+    __shared__ MShared sm;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = (int)blockIdx.x / a.K, k = (int)blockIdx.x % a.K, s = a.s;
+    const uint32_t V = (uint32_t)a.V;
+    const int ng = (a.V + 127) / 128, n3 = (ng + 15) / 16, n4 = (n3 + 15) / 16;
+    const size_t esize = BF16 ? 2 : 4;
+    const unsigned char* row = (const unsigned char*)a.logits +
+                               (((size_t)b * a.K + k) * a.s_count + (size_t)(s - a.s_begin)) * (size_t)a.V * esize;
+
+    // ---- the context of path k: the paths whose drafts at depths < s equal its own
+    for (int e = tid; e < a.K * s; e += kMBlock)
+        sm.path_tok[e] = a.draft_tokens[((size_t)b * a.K + e / s) * a.gamma + e % s];
+    if (tid == 0) sm.n_l4 = sm.n_l3 = sm.n_cand = 0;
+    __syncthreads();
+    if (wave == 0) {
+        bool same = lane < a.K;
+        for (int d = 0; d < s && same; ++d) same = sm.path_tok[lane * s + d] == sm.path_tok[k * s + d];
+        const uint64_t bal = __ballot(same);
+        if (lane == 0) sm.mask = (uint32_t)bal;
+    }
+
+    if (a.row_gm) {
+        // the row was streamed ahead (group maxima, maximum and LSE): only the context's
+        // lowest path goes on, loading them
+        __syncthreads();
+        if (k != __ffs((int)sm.mask) - 1) return;  // uniform
+        const size_t rid = ((size_t)b * a.K + k) * a.gamma + s;
+        for (int g = tid; g < ng; g += kMBlock) sm.gm[g] = a.row_gm[rid * ng + g];
+        if (tid == 0) sm.rowmax = a.row_max[rid];
+    } else {
+        // ---- stream the row: log-sum-exp, group maxima, row maximum
+        __syncthreads();
+        mstream_row<BF16, VEC>(row, a.V, a.invT, sm.gm,
+                               a.draft_lse ? a.draft_lse + ((size_t)b * a.K + k) * a.gamma + s : nullptr, sm.red_m,
+                               sm.red_s, sm.red_x, &sm.rowmax);
     }
     __syncthreads();
     const uint32_t mask = sm.mask;
@@ -592,6 +632,18 @@ hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout,
             if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<false, false, 0>), grid, block, 0, stream, a);
             else hipLaunchKernelGGL((mpfr_draft_kernel<false, false, 1>), grid, block, 0, stream, a);
         }
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_mpfr_stream(const MpfrArgs& a, bool bf16, bool vec, hipStream_t stream) {
+    const dim3 grid((unsigned)(a.B * a.K * a.s_count)), block(kMBlock);
+    if (bf16) {
+        if (vec) hipLaunchKernelGGL((mpfr_stream_kernel<true, true>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((mpfr_stream_kernel<true, false>), grid, block, 0, stream, a);
+    } else {
+        if (vec) hipLaunchKernelGGL((mpfr_stream_kernel<false, true>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((mpfr_stream_kernel<false, false>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }
