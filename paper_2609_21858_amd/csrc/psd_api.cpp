@@ -172,14 +172,18 @@ psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_be
     m.s_count = s_count;
     m.T = p->temp_draft;
     m.invT = 1.0f / p->temp_draft;
-    // every draft row of the call streamed once (group maxima, maxima, LSE), then the
-    // contexts sampled depth by depth from those
-    const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
-    const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);
-    m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
-    m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
-    hipError_t e0 = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, vec, stream);
-    if (e0 != hipSuccess) return hip_fail(e0, "MPFR stream kernel launch");
+    // A depth's launch has one workgroup per (sequence, path), each streaming its row.
+    // When those cannot fill the device (B K < 1024), every draft row of the call is
+    // streamed first in one launch (group maxima, maxima, LSE) and the depth launches
+    // only sample; otherwise each depth's streaming overlaps its contexts' sampling.
+    if ((long)b->batch * p->num_drafts < 1024) {
+        const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
+        const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);
+        m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
+        m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
+        hipError_t e0 = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, vec, stream);
+        if (e0 != hipSuccess) return hip_fail(e0, "MPFR stream kernel launch");
+    }
     for (int s = s_begin; s < s_begin + s_count; ++s) {
         m.s = s;
         hipError_t e = psd::launch_mpfr_draft(m, p->dtype == PSD_BF16, vec, p->clocks, stream);

@@ -134,6 +134,15 @@ def test_mpfr_two_call_and_per_path(psd, layout):
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_wide_batch_streams_in_each_depth(psd, layout):
+    """B K >= 1024 drafts with every depth's launch streaming its own rows (smaller
+    batches stream all draft rows in one launch first): same parity bar, every 16th
+    sequence checked."""
+    w = workloads.custom(3000, 4, 3, 256, dtype="bf16", m=3, tau=0.5, sigma=2.0, alpha=1.0, T_draft=0.6)
+    run_mpfr(psd, w, 21, layout, gen_device=DEV, seqs=range(0, w.B, 16))
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
 def test_mpfr_config2_full(psd, layout):
     run_mpfr(psd, workloads.WORKLOADS[2], 2, layout)
 
