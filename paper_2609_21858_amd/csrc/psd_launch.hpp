@@ -135,6 +135,7 @@ struct TopkRaceArgs {
     int target_rows;         // 0 (drafting only), 1, K
     int mpfr;
     float T_target, T_draft;
+    int target_waves;        // waves sharing each shared-chain target race (set by the launcher)
 };
 
 // Position-indexed toy language model: target rows [B][gamma+1][V] at positions

@@ -538,6 +538,8 @@ struct RaceShared {
     int path[32 * 33];    // drafts of each path ([path][depth])
     int chain[33];        // shared target chain
     int pchain[32 * 33];  // per-path target chains
+    double ts[8];         // partial minima of a shared-chain target race, one per target wave
+    int tv[8], tj[8];
 };
 
 // Context key of the token at absolute position t whose previous tokens are the last
@@ -554,17 +556,20 @@ __device__ __forceinline__ void list_key(const TopkRaceArgs& a, int b, int64_t t
     }
 }
 
-// The race of one row's list over slots [slot0, slot0 + nslots), by one wave: argmin
-// of ln E_j[v] - l_v / T (exact, fp64); -1 for an empty list.
+// The race of one row's list over slots [slot0, slot0 + nslots) -- argmin of
+// ln E_j[v] - l_v / T (exact, fp64) -- over the (token, slot) entries of 64-entry units
+// part, part + nparts, ... by one wave.  Returns the wave's winning token (-1 when it
+// has none) and, when asked, its score and slot.
 template <int LAYOUT>
-__device__ int wave_race(const TopkRaceArgs& a, int rid, int slot0, int nslots, float T, uint32_t k0, uint32_t k1) {
+__device__ int wave_race(const TopkRaceArgs& a, int rid, int slot0, int nslots, float T, uint32_t k0, uint32_t k1,
+                         int part = 0, int nparts = 1, double* out_s = nullptr, int* out_j = nullptr) {
     const int lane = threadIdx.x & 63;
     const int n = a.list_len[rid];
     const int* lt = a.list_tok + (size_t)rid * a.cap;
     const float* lv = a.list_val + (size_t)rid * a.cap;
     double bs = INFINITY;
     int bv = 0x7FFFFFFF, bj = 0x7FFFFFFF, bc = -1;
-    for (int e = lane; e < n * nslots; e += 64) {
+    for (int e = part * 64 + lane; e < n * nslots; e += 64 * nparts) {
         const int c = e / nslots, j = slot0 + e % nslots;
         const int v = lt[c];
         const double s = log(tclock<LAYOUT>((uint32_t)a.V, (uint32_t)j, (uint32_t)v, k0, k1)) - (double)lv[c] / (double)T;
@@ -576,6 +581,10 @@ __device__ int wave_race(const TopkRaceArgs& a, int rid, int slot0, int nslots, 
         }
     }
     wave_lexmin(bs, bv, bj, bc);
+    if (out_s) {
+        *out_s = bs;
+        *out_j = bj;
+    }
     return bs < INFINITY ? bv : -1;
 }
 
@@ -666,14 +675,15 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
     __syncthreads();
     const bool per = a.target_rows > 1;
     const int tslots = a.mpfr ? 1 : K;
-    const int tw = K % nw;  // the wave racing the shared target chain
+    // waves [dw, nw) share each shared-chain target race; the others race the drafts
+    const int twv = a.target_rows == 1 ? a.target_waves : 0, dw = nw - twv;
     const int d_end = a.s_begin + a.s_count;
     const int s_lo = a.target_rows > 0 ? 0 : a.s_begin;
     const int s_hi = a.target_rows > 0 ? G : d_end - 1;
     uint32_t k0, k1;
     for (int s = s_lo; s <= s_hi; ++s) {
-        if (s >= a.s_begin && s < d_end) {
-            for (int k = w; k < K; k += nw) {
+        if (s >= a.s_begin && s < d_end && w < dw) {
+            for (int k = w; k < K; k += dw) {
                 if (!a.mpfr) {
                     list_key(a, b, t0 + s, &sm.path[k * 33], s, k0, k1);
                     const int y = wave_race<LAYOUT>(a, (b * K + k) * G + s, k, 1, a.T_draft, k0, k1);
@@ -697,10 +707,17 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
                 }
             }
         }
-        if (a.target_rows == 1 && w == tw) {
+        if (a.target_rows == 1 && w >= dw) {
+            const int ti = w - dw;
             list_key(a, b, t0 + s, sm.chain, s, k0, k1);
-            const int y = wave_race<LAYOUT>(a, D + b * (G + 1) + s, 0, tslots, a.T_target, k0, k1);
-            if (lane == 0) sm.chain[s] = y;
+            double ps;
+            int pj;
+            const int pv = wave_race<LAYOUT>(a, D + b * (G + 1) + s, 0, tslots, a.T_target, k0, k1, ti, twv, &ps, &pj);
+            if (lane == 0) {
+                sm.ts[ti] = ps;
+                sm.tv[ti] = pv;
+                sm.tj[ti] = pj;
+            }
         }
         if (per)
             for (int k = w; k < K; k += nw) {
@@ -709,6 +726,21 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
                 if (lane == 0) sm.pchain[k * 33 + s] = y;
             }
         __syncthreads();
+        if (twv > 0) {
+            // the shared-chain target of depth s: the lexicographic minimum of the waves' parts
+            if (tid == 0) {
+                double bs = sm.ts[0];
+                int bv = sm.tv[0], bj = sm.tj[0];
+                for (int i = 1; i < twv; ++i)
+                    if (tlex(sm.ts[i], sm.tv[i], sm.tj[i], bs, bv, bj)) {
+                        bs = sm.ts[i];
+                        bv = sm.tv[i];
+                        bj = sm.tj[i];
+                    }
+                sm.chain[s] = bs < INFINITY ? bv : -1;
+            }
+            __syncthreads();
+        }
     }
     if (a.s_count > 0)
         for (int e = tid; e < K * a.s_count; e += blockDim.x) {
@@ -762,14 +794,22 @@ hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t st
 }
 
 hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t stream) {
-    // one wave per independent chain (the K draft paths, and the shared target chain),
-    // at most 8: the TREE clocks need more than 128 registers per lane
-    const int chains = a.K + (a.target_rows == 1 ? 1 : 0);
-    const int threads = 64 * (chains < 8 ? chains : 8);
+    // at most 8 waves (the TREE clocks need more than 128 registers per lane): one per
+    // draft path, and for a shared target chain up to four sharing each of its races
+    // (its K-slot races are the longest of a depth)
+    TopkRaceArgs b = a;
+    int waves;
+    if (a.target_rows == 1) {
+        b.target_waves = a.K >= 7 ? 1 : (8 - a.K < 4 ? 8 - a.K : 4);
+        waves = (a.K < 8 - b.target_waves ? a.K : 8 - b.target_waves) + b.target_waves;
+    } else {
+        b.target_waves = 0;
+        waves = a.K < 8 ? a.K : 8;
+    }
     if (layout == 0)
-        hipLaunchKernelGGL(topk_race_kernel<0>, dim3(a.B), dim3(threads), 0, stream, a);
+        hipLaunchKernelGGL(topk_race_kernel<0>, dim3(a.B), dim3(64 * waves), 0, stream, b);
     else
-        hipLaunchKernelGGL(topk_race_kernel<1>, dim3(a.B), dim3(threads), 0, stream, a);
+        hipLaunchKernelGGL(topk_race_kernel<1>, dim3(a.B), dim3(64 * waves), 0, stream, b);
     return hipGetLastError();
 }
 
