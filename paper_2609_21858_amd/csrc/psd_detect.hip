@@ -25,7 +25,8 @@ namespace psd {
 namespace {
 
 constexpr int kDetBlock = 1024;  // threads per detection workgroup
-constexpr int kDetParts = 2;     // lanes per scored token (adjacent), each taking every other slot
+constexpr int kDetParts = 2;     // lanes per scored token (adjacent, a power of two), each taking
+                                 // every kDetParts-th slot
 
 // The further per-token scores of a pivot r = e^{-c}: the U-score r, Li et al.'s
 // h*_{gum,Delta}(r) = log(k r^{Delta/(1-Delta)} + [q > 0] r^{(1-q)/q}) in log-sum-exp
@@ -86,7 +87,9 @@ __global__ __launch_bounds__(kDetBlock) void detect_kernel(DetectArgs a) {
         // Float clocks err by less than 1e-6 relative plus 1e-6 absolute (a few
         // roundings of positive terms, hardware log2); every slot within twice that
         // of the token's float minimum is rebuilt exactly.
-        const float tmin = fminf(emin, __shfl_xor(emin, 1));
+        float tmin = emin;
+#pragma unroll
+        for (int o = 1; o < kDetParts; o <<= 1) tmin = fminf(tmin, __shfl_xor(tmin, o));
         const float lim = tmin + (tmin * 2e-6f + 2e-6f);
         double cmin = INFINITY;
         if (scored && emin <= lim) {
@@ -100,7 +103,8 @@ __global__ __launch_bounds__(kDetBlock) void detect_kernel(DetectArgs a) {
                                    : flat_clock_f64((uint32_t)jmin, (uint32_t)w, k0, k1);
             }
         }
-        cmin = fmin(cmin, __shfl_xor(cmin, 1));
+#pragma unroll
+        for (int o = 1; o < kDetParts; o <<= 1) cmin = fmin(cmin, __shfl_xor(cmin, o));
         if (sub == 0 && t < a.seq_len) {
             if (scored) {
                 const double cc = (double)a.K * cmin;  // the target's clock of w_t; pivot e^{-cc}
