@@ -211,13 +211,15 @@ def test_generate_is_plain_keyed_decoding(psd, layout, mpfr):
     assert blocks - 4 < hb <= blocks
 
 
+@pytest.mark.parametrize("mpfr", [False, True])
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_generate_graph_replay_and_drafter_substitution(psd, layout):
+def test_generate_graph_replay_and_drafter_substitution(psd, layout, mpfr):
     """The captured loop replays to the eager run's text; other drafters (another noise
     stream, other scales) change how many blocks it takes, not the text."""
     B, V, K, G, m, n_pos = 8, 5000, 4, 4, 4, 64
     key = 0x5A5A5A5A12345678
-    params = psd.make_params(key, V, K, m, 1.0, 1.0, dtype=torch.bfloat16, clocks=layout)
+    params = psd.make_params(key, V, K, m, 1.0, 1.0, dtype=torch.bfloat16, clocks=layout,
+                             mode=psd.PSD_MODE_MPFR if mpfr else psd.PSD_MODE_HET)
     prompts = _prompts(B, m, V, 2).to(DEV)
     runs = {}
     for name, tau, dseed, graph, every in (("eager", (0.5, 0.5), 9, False, 8), ("graph", (0.5, 0.5), 9, True, 8),
@@ -240,7 +242,7 @@ def test_generate_graph_replay_and_drafter_substitution(psd, layout):
     tm = workloads.ToyModel(seed=99, draft_seed=9, sigma=3.0, alpha=1.2, tau=(0.5, 0.5))
     rng = np.random.default_rng(layout)
     picks = [(int(b), int(t)) for b, t in zip(rng.integers(0, B, 40), rng.integers(m, m + n_pos, 40))]
-    plain_chain_check(tm, key, K, m, V, 1.0, layout, _np(runs["eager"][0]), picks, False)
+    plain_chain_check(tm, key, K, m, V, 1.0, layout, _np(runs["eager"][0]), picks, mpfr)
 
 
 @pytest.mark.parametrize("mpfr", [False, True])
