@@ -4,18 +4,16 @@
 // top-p; Alg. "Batched-target direct-top-k MPFR speculative sampling"): every
 // token outside a row's kept set has probability 0.  With at most 256 kept tokens
 // per row the race needs no pruning, so this path has two kernels:
-//  * topk_select_kernel, one workgroup per row, one pass over the row in HBM: each
-//    wave streams its share of the row against a running threshold of its own and
-//    appends the logits that reach it to an LDS buffer (ballot and lane prefix, no
-//    atomics); a full buffer is compacted by a wave-level bisection that raises the
-//    threshold to the top_k-th largest key it holds.  Every logit left out is below
-//    the row's top_k-th largest, so the union of the buffers holds the top-k set,
-//    ties at the cut included; block-wide bisections over its keys and then its
-//    indices pick the k largest (order-preserving keys, ties to the lowest index).
-//    Rows whose ties at the cut overflow a buffer are selected by exact radix passes
-//    instead.  Then the kept list is sorted by (logit descending, index ascending),
-//    its top-p prefix and the log-sum-exp of the kept set at the row's temperature
-//    are formed in fp64;
+//  * topk_select_kernel, one workgroup per row, one pass over the row in HBM that
+//    keeps only the maximum of every 128-token group; the top_k-th largest group
+//    maximum bounds the row's top_k-th largest logit from below, so only the groups
+//    whose maximum reaches it are read again and their logits that reach it are the
+//    candidates (wave buffers in LDS: ballot and lane prefix, no atomics).  Block-wide
+//    bisections over the candidates' keys and then their indices pick the k largest
+//    (order-preserving keys, ties to the lowest index).  Rows whose ties at the cut
+//    overflow the buffers are selected by exact radix passes instead.  Then the kept
+//    list is sorted by (logit descending, index ascending), its top-p prefix and the
+//    log-sum-exp of the kept set at the row's temperature are formed in fp64;
 //  * topk_race_kernel, one workgroup per sequence with one wave per independent
 //    chain (each draft path, the target chain): the block's races in dependency
 //    order over the lists, with exact fp64 clocks of every (token, slot) -- distinct
@@ -56,9 +54,11 @@ __device__ __forceinline__ float tload(const unsigned char* row, bool bf16, int 
 
 constexpr int kWaves = kTBlock / 64;
 constexpr int kWaveCap = 512;  // candidates a wave holds
-constexpr int kSub = 2;        // elements per lane between buffer checks (at most 128 appends)
 
 // ---------------------------------------------------------------- block helpers
+
+constexpr int kMaxGroups = (1 << 19) / kGroupTokens;  // 128-token groups of the largest row
+constexpr int kCandGroups = 2 * kMaxTopK;             // groups re-read for candidates
 
 struct SelShared {
     union {
@@ -66,18 +66,25 @@ struct SelShared {
             uint32_t key[kWaves][kWaveCap];  // each wave's candidates: order-preserving key,
             int32_t idx[kWaves][kWaveCap];   // token index
         } wb;
-        int hist[2048];  // radix passes (the candidates are given up first)
+        int hist[2048];         // radix passes (the candidates are given up first)
+        float gm[kMaxGroups];   // group maxima of the streaming pass
     } u;
     int tok[kMaxTopK];
     float val[kMaxTopK];
-    int stok[kMaxTopK];
-    float sval[kMaxTopK];
+    union {
+        struct {
+            int stok[kMaxTopK];
+            float sval[kMaxTopK];
+        };
+        int cgl[kCandGroups];  // groups holding candidates (before the kept list is sorted)
+    };
     int red[2][kWaves];
     double dred[kWaves];
     double dsel;
     int s4[kWaves];
     int wcount[kWaves], wover[kWaves];
     int n_keep, n_fin;
+    uint32_t tsel;  // a key threshold found by one wave
     uint32_t prefix;
     int above;
 };
@@ -158,6 +165,20 @@ __device__ __forceinline__ double block_incl_sum_f64(SelShared& sm, double x, do
     return x + base;
 }
 
+// ---------------------------------------------------------------- one-wave selection
+
+// The need-th largest key class t of Q keys per lane (0: no entry) with the wave's
+// ballots alone (no barrier): largest t (bits below kLow clear) with #{key >= t} >= need.
+template <int Q, int kLow>
+__device__ __forceinline__ uint32_t wave_kth_class(const uint32_t (&kk)[Q], int need) {
+    uint32_t t = 0u;
+    for (int bit = 31; bit >= kLow; --bit) {
+        const uint32_t cand = t | (1u << bit);
+        if (wave_count<Q>([&](int q) { return kk[q] >= cand; }) >= need) t = cand;
+    }
+    return t;
+}
+
 // ---------------------------------------------------------------- one-pass selection
 
 // Keys of bf16 logits differ only in their top 16 bits (the low half is 0x0000 or
@@ -167,68 +188,22 @@ struct KeyBits {
     static constexpr int kLow = BF16 ? 16 : 0;
 };
 
-// One wave's candidate buffer: raise its threshold to the need-th largest key class it
-// holds and drop the entries below it (ties stay).  Every dropped key is below the
-// row's need-th largest, since the buffer's need-th largest is at most the row's.
-// Returns the new count; *t gets the threshold key.
-template <bool BF16>
-__device__ __forceinline__ int wave_compact(uint32_t* bk, int32_t* bi, int cnt, int need, uint32_t& t) {
-    constexpr int Q = kWaveCap / 64;
-    const int lane = threadIdx.x & 63;
-    uint32_t kk[Q];
-    int32_t ii[Q];
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-        const int j = lane + 64 * q;
-        kk[q] = j < cnt ? bk[j] : 0u;
-        ii[q] = j < cnt ? bi[j] : 0;
-    }
-    uint32_t th = 0u;
-    for (int bit = 31; bit >= KeyBits<BF16>::kLow; --bit) {
-        const uint32_t cand = th | (1u << bit);
-        if (wave_count<Q>([&](int q) { return kk[q] >= cand; }) >= need) th = cand;
-    }
-    int kc = 0;
-#pragma unroll
-    for (int q = 0; q < Q; ++q) kc += kk[q] >= th;
-    const int incl = wave_incl(kc);
-    const int total = __shfl(incl, 63);
-    int o = incl - kc;
-#pragma unroll
-    for (int q = 0; q < Q; ++q)
-        if (kk[q] >= th) {
-            bk[o] = kk[q];
-            bi[o] = ii[q];
-            ++o;
-        }
-    t = th;
-    return total;
-}
-
 template <bool BF16>
 __device__ __forceinline__ uint32_t elem_bits(const uint32_t (&w)[4], int i) {
     return BF16 ? ((i & 1) ? (w[i >> 1] & 0xFFFF0000u) : (w[i >> 1] << 16)) : w[i];
 }
 
-// Stream the row, one wave per 64 x kEPT-token chunk in turn (wave w takes chunks w,
-// w + 4, ...; four 16-byte loads per lane in flight): every finite logit at least the
-// wave's threshold (initially the lowest finite value) joins the wave's buffer
-// (ballot + lane prefix, no atomics); a chunk is skipped with one ballot when no
-// lane's maximum reaches the threshold, and a buffer that could not take kSub more
-// logits per lane is compacted.  Returns false if ties at the cut fill a buffer
-// (then the caller selects by radix passes).
+// Group maxima of the row (128-token groups) into sm.u.gm: one wave per 64 x EPT-token
+// chunk in turn (wave w takes chunks w, w + 4, ...; four 16-byte loads per lane in
+// flight), the maximum of each lane's tokens, then of the lanes of a group.  Only a
+// maximum per token: the pass costs little more than reading the row.
 template <bool BF16>
-__device__ __forceinline__ bool stream_row(SelShared& sm, const unsigned char* row, int V, int top_k) {
-    constexpr int EPT = BF16 ? 8 : 4, WCH = 64 * EPT, STEP = kWaves * kUnroll;
+__device__ __forceinline__ void stream_group_max(SelShared& sm, const unsigned char* row, int V) {
+    constexpr int EPT = BF16 ? 8 : 4, WCH = 64 * EPT, STEP = kWaves * kUnroll, LPG = kGroupTokens / EPT;
     constexpr size_t ES = BF16 ? 2 : 4;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const bool vec = ((uintptr_t)row & 15u) == 0;
-    const int nch = (V + WCH - 1) / WCH;
-    uint32_t* bk = sm.u.wb.key[w];
-    int32_t* bi = sm.u.wb.idx[w];
-    int cnt = 0;
-    float th = -3.40282347e38f;  // the lowest finite value: -inf never joins
-    bool over = false;
+    const int nch = (V + WCH - 1) / WCH, ng = (V + kGroupTokens - 1) / kGroupTokens;
     for (int c0 = w; c0 < nch; c0 += STEP) {
         uint32_t wv[kUnroll][4];
 #pragma unroll
@@ -262,32 +237,139 @@ __device__ __forceinline__ bool stream_row(SelShared& sm, const unsigned char* r
             float mx = __uint_as_float(elem_bits<BF16>(wv[u], 0));
 #pragma unroll
             for (int i = 1; i < EPT; ++i) mx = fmaxf(mx, __uint_as_float(elem_bits<BF16>(wv[u], i)));
-            if (!__ballot(mx >= th && !over)) continue;
-            const int base = (c0 + u * kWaves) * WCH + lane * EPT;
+            mx = row16_max(mx);
+            if (LPG == 32) mx = fmaxf(mx, __shfl_xor(mx, 16));
+            const int g = (c0 + u * kWaves) * (WCH / kGroupTokens) + lane / LPG;
+            if (lane % LPG == 0 && g < ng) sm.u.gm[g] = mx;
+        }
+    }
+}
+
+// The candidates of the row's top-k set, without a per-logit pass over the row: t =
+// the top_k-th largest key class among the group maxima (a block-wide bisection), so
+// at least top_k logits reach t and every logit of the top-k set (ties at the cut
+// included) reaches it too; only groups whose maximum reaches t can hold such a
+// logit, and they are read again.  With fewer groups than top_k, every group with a
+// finite logit is read again.  Their finite logits that reach t go to the wave
+// buffers (ballot and lane prefix), as the per-logit selection would leave them.
+// Returns false when the groups or the candidates do not fit (heavy ties at the
+// cut); the caller then selects by radix passes.
+template <bool BF16>
+__device__ __forceinline__ bool select_candidates(SelShared& sm, const unsigned char* row, int V, int top_k) {
+    constexpr int EPT = BF16 ? 8 : 4, LPG = kGroupTokens / EPT, GPW = 64 / LPG;  // groups per wave step
+    constexpr int QG = kMaxGroups / kTBlock;
+    constexpr size_t ES = BF16 ? 2 : 4;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int ng = (V + kGroupTokens - 1) / kGroupTokens;
+    stream_group_max<BF16>(sm, row, V);
+    __syncthreads();
+    uint32_t kg[QG];
+    bool fin[QG];
 #pragma unroll
-            for (int i0 = 0; i0 < EPT; i0 += kSub) {
+    for (int q = 0; q < QG; ++q) {
+        const int g = tid + kTBlock * q;
+        const float m = g < ng ? sm.u.gm[g] : -INFINITY;
+        fin[q] = m >= -3.40282347e38f;  // a finite (or +inf) logit in the group; not NaN
+        kg[q] = fin[q] ? key_f32(__float_as_uint(m)) : 0u;
+    }
+    int it = 0;
+    uint32_t t = 0u;
+    constexpr int QW = 16;  // group maxima per lane when one wave holds them all
+    if (ng >= top_k && ng <= 64 * QW) {
+        // one wave finds t over all the group maxima; the others wait at one barrier
+        if (w == 0) {
+            uint32_t kw[QW];
 #pragma unroll
-                for (int i = i0; i < i0 + kSub; ++i) {
-                    const uint32_t bits = elem_bits<BF16>(wv[u], i);
-                    const bool p = __uint_as_float(bits) >= th && !over;
-                    const uint64_t m = __ballot(p);
-                    if (m) {
-                        if (p) {
-                            const int pos = cnt + lanes_below(m);
-                            bk[pos] = key_f32(bits);
-                            bi[pos] = base + i;
+            for (int q = 0; q < QW; ++q) {
+                const int g = lane + 64 * q;
+                const float m = g < ng ? sm.u.gm[g] : -INFINITY;
+                kw[q] = m >= -3.40282347e38f ? key_f32(__float_as_uint(m)) : 0u;
+            }
+            const uint32_t tw = wave_kth_class<QW, KeyBits<BF16>::kLow>(kw, top_k);
+            if (lane == 0) sm.tsel = tw;
+        }
+        __syncthreads();
+        t = sm.tsel;
+    } else if (ng >= top_k) {
+        for (int bit = 31; bit >= KeyBits<BF16>::kLow; --bit) {
+            const uint32_t cand = t | (1u << bit);
+            if (block_sum_waves(sm, wave_count<QG>([&](int q) { return fin[q] && kg[q] >= cand; }), it) >= top_k)
+                t = cand;
+        }
+    }
+    // the groups to read again, compacted (thread order)
+    int nc = 0;
+#pragma unroll
+    for (int q = 0; q < QG; ++q) nc += fin[q] && kg[q] >= t;
+    int n_cg;
+    int off = block_incl_sum(sm, nc, n_cg) - nc;
+    if (n_cg > kCandGroups) {
+        if (tid == 0) sm.wover[0] = 1;
+        __syncthreads();
+        return false;
+    }
+#pragma unroll
+    for (int q = 0; q < QG; ++q)
+        if (fin[q] && kg[q] >= t) sm.cgl[off++] = tid + kTBlock * q;
+    __syncthreads();  // (the group maxima are dead: the wave buffers reuse their space)
+    // wave w reads groups w*GPW .. of every step of kWaves*GPW list entries
+    uint32_t* bk = sm.u.wb.key[w];
+    int32_t* bi = sm.u.wb.idx[w];
+    const bool vec = ((uintptr_t)row & 15u) == 0;
+    int cnt = 0;
+    bool over = false;
+    for (int e0 = w * GPW; e0 < n_cg; e0 += kWaves * GPW * kUnroll) {
+        uint32_t wv[kUnroll][4];
+        int base[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int e = e0 + u * kWaves * GPW + lane / LPG;
+            base[u] = -1;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) wv[u][i] = BF16 ? 0xFF80FF80u : 0xFF800000u;  // -inf
+            if (e < n_cg && e < e0 + u * kWaves * GPW + GPW) {
+                base[u] = sm.cgl[e] * kGroupTokens + (lane % LPG) * EPT;
+                if (vec && base[u] + EPT <= V) {
+                    const uint4 q = *(const uint4*)(row + (size_t)base[u] * ES);
+                    wv[u][0] = q.x;
+                    wv[u][1] = q.y;
+                    wv[u][2] = q.z;
+                    wv[u][3] = q.w;
+                } else {
+#pragma unroll
+                    for (int i = 0; i < EPT; ++i) {
+                        const int v = base[u] + i;
+                        if (v < V) {
+                            if (BF16) {
+                                const uint32_t h = ((const uint16_t*)row)[v];
+                                wv[u][i >> 1] = (wv[u][i >> 1] & ~(0xFFFFu << (16 * (i & 1)))) | (h << (16 * (i & 1)));
+                            } else {
+                                wv[u][i] = ((const uint32_t*)row)[v];
+                            }
                         }
-                        cnt += __popcll(m);
                     }
                 }
-                if (cnt > kWaveCap - 64 * kSub) {
-                    uint32_t tk;
-                    cnt = wave_compact<BF16>(bk, bi, cnt, top_k, tk);
-                    th = val_f32(tk);
-                    if (cnt > kWaveCap - 64 * kSub) {  // ties at the cut: stop collecting
-                        over = true;
-                        cnt = 0;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+#pragma unroll
+            for (int i = 0; i < EPT; ++i) {
+                const uint32_t bits = elem_bits<BF16>(wv[u], i);
+                const float x = __uint_as_float(bits);
+                const bool pass = base[u] >= 0 && x >= -3.40282347e38f && key_f32(bits) >= t && !over;
+                const uint64_t m = __ballot(pass);
+                if (m) {
+                    if (pass) {
+                        const int pos = cnt + lanes_below(m);
+                        bk[pos] = key_f32(bits);
+                        bi[pos] = base[u] + i;
                     }
+                    cnt += __popcll(m);
+                }
+                if (cnt > kWaveCap - 64) {  // ties at the cut: give up (radix passes)
+                    over = true;
+                    cnt = 0;
                 }
             }
         }
@@ -399,7 +481,7 @@ __global__ __launch_bounds__(kTBlock) void topk_select_kernel(TopkSelectArgs a) 
 
     int it = 0;
     int need;
-    if (!stream_row<BF16>(sm, row, a.V, a.top_k)) {
+    if (!select_candidates<BF16>(sm, row, a.V, a.top_k)) {
         __syncthreads();  // the candidate buffers are reused by the radix passes
         if (tid == 0 && a.radix_rows) atomicAdd(a.radix_rows, 1u);
         need = radix_select<BF16>(sm, row, a.V, a.top_k);
@@ -414,52 +496,100 @@ __global__ __launch_bounds__(kTBlock) void topk_select_kernel(TopkSelectArgs a) 
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) tot += sm.wcount[w];
         need = min(a.top_k, tot);
+        constexpr int QW = 4;  // candidates per lane when one wave holds them all
+        if (need > 0 && tot <= 64 * QW) {
+            // one wave: the same bisections over the concatenated buffers, with ballots
+            if (tid < 64) {
+                const int lane = tid;
+                const int c0 = sm.wcount[0], c1 = c0 + sm.wcount[1], c2 = c1 + sm.wcount[2];
+                uint32_t kk[QW];
+                int32_t ii[QW];
 #pragma unroll
-        for (int q = 0; q < Q; ++q) {
-            const int w = q / PW, p = tid + kTBlock * (q % PW);
-            const bool ok = p < sm.wcount[w];
-            kk[q] = ok ? sm.u.wb.key[w][p] : 0u;
-            ii[q] = ok ? sm.u.wb.idx[w][p] : 0;
-        }
-        if (need > 0) {
-            // the need-th largest key class: largest t with #{key >= t} >= need
-            uint32_t t = 0u;
-            for (int bit = 31; bit >= KeyBits<BF16>::kLow; --bit) {
-                const uint32_t cand = t | (1u << bit);
-                if (block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= cand; }), it) >= need) t = cand;
-            }
-            // keys of the next class up (key >= t_up) are strictly larger logits
-            const uint32_t t_up = t + (1u << KeyBits<BF16>::kLow);
-            const int n_gt = block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= t_up; }), it);
-            const int n_ge = block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= t; }), it);
-            const int take = need - n_gt;  // ties at t to keep, lowest indices first
-            int xmax = 0x7FFFFFFF;         // keep the ties with index <= xmax
-            if (n_ge - n_gt > take) {
-                // the take-th smallest index among the tied entries: largest x with #{index < x} < take
-                int x = 0;
-                for (int bit = 18; bit >= 0; --bit) {
-                    const int cand = x | (1 << bit);
-                    if (block_sum_waves(sm, wave_count<Q>([&](int q) {
-                                            return kk[q] >= t && kk[q] < t_up && ii[q] < cand;
-                                        }),
-                                        it) < take)
-                        x = cand;
+                for (int q = 0; q < QW; ++q) {
+                    const int j = lane + 64 * q;
+                    const int bw = j < c0 ? 0 : j < c1 ? 1 : j < c2 ? 2 : 3;
+                    const int p = j - (bw == 0 ? 0 : bw == 1 ? c0 : bw == 2 ? c1 : c2);
+                    const bool ok = j < tot;
+                    kk[q] = ok ? sm.u.wb.key[bw][p] : 0u;
+                    ii[q] = ok ? sm.u.wb.idx[bw][p] : 0;
                 }
-                xmax = x;
-            }
-            int kc = 0;
-#pragma unroll
-            for (int q = 0; q < Q; ++q) kc += kk[q] >= t_up || (kk[q] >= t && ii[q] <= xmax);
-            int total;
-            int off = block_incl_sum(sm, kc, total) - kc;
-#pragma unroll
-            for (int q = 0; q < Q; ++q)
-                if ((kk[q] >= t_up || (kk[q] >= t && ii[q] <= xmax)) && off < kMaxTopK) {
-                    sm.tok[off] = ii[q];
-                    sm.val[off] = val_f32(kk[q]);
-                    ++off;
+                const uint32_t t = wave_kth_class<QW, KeyBits<BF16>::kLow>(kk, need);
+                const uint32_t t_up = t + (1u << KeyBits<BF16>::kLow);
+                const int n_gt = wave_count<QW>([&](int q) { return kk[q] >= t_up; });
+                const int n_ge = wave_count<QW>([&](int q) { return kk[q] >= t; });
+                const int take = need - n_gt;
+                int xmax = 0x7FFFFFFF;
+                if (n_ge - n_gt > take) {
+                    int x = 0;
+                    for (int bit = 18; bit >= 0; --bit) {
+                        const int cand = x | (1 << bit);
+                        if (wave_count<QW>([&](int q) { return kk[q] >= t && kk[q] < t_up && ii[q] < cand; }) < take)
+                            x = cand;
+                    }
+                    xmax = x;
                 }
+                int off = 0;
+#pragma unroll
+                for (int q = 0; q < QW; ++q) {
+                    const bool keep = kk[q] >= t_up || (kk[q] >= t && ii[q] <= xmax);
+                    const uint64_t m = __ballot(keep);
+                    const int pos = off + lanes_below(m);
+                    if (keep && pos < kMaxTopK) {
+                        sm.tok[pos] = ii[q];
+                        sm.val[pos] = val_f32(kk[q]);
+                    }
+                    off += __popcll(m);
+                }
+            }
             __syncthreads();
+        } else {
+#pragma unroll
+            for (int q = 0; q < Q; ++q) {
+                const int w = q / PW, p = tid + kTBlock * (q % PW);
+                const bool ok = p < sm.wcount[w];
+                kk[q] = ok ? sm.u.wb.key[w][p] : 0u;
+                ii[q] = ok ? sm.u.wb.idx[w][p] : 0;
+            }
+            if (need > 0) {
+                // the need-th largest key class: largest t with #{key >= t} >= need
+                uint32_t t = 0u;
+                for (int bit = 31; bit >= KeyBits<BF16>::kLow; --bit) {
+                    const uint32_t cand = t | (1u << bit);
+                    if (block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= cand; }), it) >= need) t = cand;
+                }
+                // keys of the next class up (key >= t_up) are strictly larger logits
+                const uint32_t t_up = t + (1u << KeyBits<BF16>::kLow);
+                const int n_gt = block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= t_up; }), it);
+                const int n_ge = block_sum_waves(sm, wave_count<Q>([&](int q) { return kk[q] >= t; }), it);
+                const int take = need - n_gt;  // ties at t to keep, lowest indices first
+                int xmax = 0x7FFFFFFF;         // keep the ties with index <= xmax
+                if (n_ge - n_gt > take) {
+                    // the take-th smallest index among the tied entries: largest x with #{index < x} < take
+                    int x = 0;
+                    for (int bit = 18; bit >= 0; --bit) {
+                        const int cand = x | (1 << bit);
+                        if (block_sum_waves(sm, wave_count<Q>([&](int q) {
+                                                return kk[q] >= t && kk[q] < t_up && ii[q] < cand;
+                                            }),
+                                            it) < take)
+                            x = cand;
+                    }
+                    xmax = x;
+                }
+                int kc = 0;
+#pragma unroll
+                for (int q = 0; q < Q; ++q) kc += kk[q] >= t_up || (kk[q] >= t && ii[q] <= xmax);
+                int total;
+                int off = block_incl_sum(sm, kc, total) - kc;
+#pragma unroll
+                for (int q = 0; q < Q; ++q)
+                    if ((kk[q] >= t_up || (kk[q] >= t && ii[q] <= xmax)) && off < kMaxTopK) {
+                        sm.tok[off] = ii[q];
+                        sm.val[off] = val_f32(kk[q]);
+                        ++off;
+                    }
+                __syncthreads();
+            }
         }
     }
     if (need == 0) {

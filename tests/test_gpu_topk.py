@@ -135,7 +135,7 @@ def test_topk50_config3(psd, layout, mpfr):
     """top-k = 50, the paper's setting, on the Llama-3 vocabulary block (every 2nd sequence)."""
     w = workloads.WORKLOADS[3]
     out, _, _ = run_topk(psd, w, 5, layout, mpfr, 50, gen_device=DEV, seqs=range(0, w.B, 2))
-    assert out["_radix_rows"] == 0  # random rows: the one-pass selection is proven exact
+    assert out["_radix_rows"] == 0  # random rows: the group-maximum candidates suffice
 
 
 @pytest.mark.parametrize("mpfr", [False, True])
@@ -196,9 +196,9 @@ def test_topk_ties_and_signed_zeros(psd, mpfr):
         blk[k] = x.to(w.torch_dtype)
     for top_k, top_p in ((20, 1.0), (64, 0.8), (3, 1.0)):
         run_topk(psd, w, 9, 1, mpfr, top_k, top_p, blk=blk)
-    # rows where one pass cannot prove its choice (every logit equal, or two values; V
-    # above 2048, so that threads drop elements): selected again by radix passes, with
-    # the same result as the oracle
+    # rows whose ties at the cut overflow the candidate buffers (every logit equal, or
+    # two values, at V = 5000): selected again by radix passes, with the same result as
+    # the oracle
     w = workloads.custom(5000, 4, 4, 4, dtype="bf16", m=2, tau=0.7, sigma=2.0, alpha=1.0)
     blk = workloads.make_block(w, 9)
     tl, dl = blk["target_logits"], blk["draft_logits"]
