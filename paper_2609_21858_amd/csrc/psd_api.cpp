@@ -261,9 +261,10 @@ psd_status run_topk(const psd_params* p, const psd_block* b, int32_t s_begin, in
     r.mpfr = p->mode == PSD_MODE_MPFR;
     r.T_target = p->temp_target;
     r.T_draft = p->temp_draft;
+    r.chain = (int32_t*)(ws + T.chain);
+    r.ctrl = (uint32_t*)(ws + L.ctrl);
+    r.status = b->status;
     if ((e = psd::launch_topk_race(r, p->clocks, stream)) != hipSuccess) return hip_fail(e, "top-k race launch");
-    if ((e = psd::launch_finish_status((uint32_t*)(ws + L.ctrl), b->status, stream)) != hipSuccess)
-        return hip_fail(e, "status kernel launch");
     return PSD_OK;
 }
 

@@ -74,7 +74,7 @@ inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
 // workspace (same row identifiers).
 constexpr int kMaxTopK = 256;
 struct TopkLayout {
-    size_t tok, val, len, lse, total;  // offsets from the workspace base; total = end
+    size_t tok, val, len, lse, chain, total;  // offsets from the workspace base; total = end
 };
 inline TopkLayout topk_layout(const WsLayout& L, int top_k) {
     TopkLayout T;
@@ -86,6 +86,8 @@ inline TopkLayout topk_layout(const WsLayout& L, int top_k) {
     T.len = o;
     o = align256(o + (size_t)L.n_rows * 4);
     T.lse = o;
+    o = align256(o + (size_t)L.n_rows * 4);
+    T.chain = o;  // shared target chain tokens [B][gamma + 1] (n_rows >= B (gamma + 1))
     o = align256(o + (size_t)L.n_rows * 4);
     T.total = o;
     return T;
@@ -136,6 +138,9 @@ struct TopkRaceArgs {
     int mpfr;
     float T_target, T_draft;
     int target_waves;        // waves sharing each shared-chain target race (set by the launcher)
+    int32_t* chain;          // workspace [B][gamma + 1]: shared-chain targets for the walk kernel
+    uint32_t* ctrl;          // workspace control words (the call's error bits)
+    uint32_t* status;        // nullable: the call's error bits for the caller
 };
 
 // Position-indexed toy language model: target rows [B][gamma+1][V] at positions

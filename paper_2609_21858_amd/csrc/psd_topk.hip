@@ -14,12 +14,16 @@
 //    overflow the buffers are selected by exact radix passes instead.  Then the kept
 //    list is sorted by (logit descending, index ascending), its top-p prefix and the
 //    log-sum-exp of the kept set at the row's temperature are formed in fp64;
-//  * topk_race_kernel, one workgroup per sequence with one wave per independent
-//    chain (each draft path, the target chain): the block's races in dependency
-//    order over the lists, with exact fp64 clocks of every (token, slot) -- distinct
+//  * the races over the lists, exact fp64 clocks of every (token, slot) -- distinct
 //    drafters race slot k / all K slots, identical drafters draw each context's nu
 //    samples from the cumulative clocks and race the targets on slot 0 -- then the
-//    walk.
+//    walk.  Distinct drafters (drafting, or with the shared target chain):
+//    topk_chain_kernel, one workgroup per (sequence, chain) -- a draft path, or the
+//    target chain, whose races four waves share while a fifth folds the next key --
+//    then topk_walk_kernel (the walk, one thread per sequence, and the status word).
+//    Identical drafters or per-path target rows: topk_race_kernel, one workgroup per
+//    sequence with one wave per chain, depth by depth (identical drafters group the
+//    paths into contexts at every depth).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -670,18 +674,22 @@ struct RaceShared {
     int pchain[32 * 33];  // per-path target chains
     double ts[8];         // partial minima of a shared-chain target race, one per target wave
     int tv[8], tj[8];
+    int pre[16];          // the sequence's context window before the block (m <= 16)
+    uint32_t tp[2][2];    // the shared chain's next key without its newest token (by depth parity)
 };
 
 // Context key of the token at absolute position t whose previous tokens are the last
-// m of prefix (m tokens) || path[0 .. d); every lane of the wave computes it.
-__device__ __forceinline__ void list_key(const TopkRaceArgs& a, int b, int64_t t, const int* path, int d,
-                                         uint32_t& k0, uint32_t& k1) {
+// m of prefix (m tokens, copied to LDS in pre) || path[0 .. d), folded up to window
+// position n (n = m: the whole key; n = m - 1: all but the newest token); every lane
+// of the wave computes it.
+__device__ __forceinline__ void list_key(const TopkRaceArgs& a, const int* pre, int64_t t, const int* path, int d,
+                                         uint32_t& k0, uint32_t& k1, int n) {
     k0 = (uint32_t)a.key;
     k1 = (uint32_t)(a.key >> 32);
     fold(k0, k1, (uint32_t)(uint64_t)t, (uint32_t)((uint64_t)t >> 32), 0u);
-    for (int i = 0; i < a.m; ++i) {
+    for (int i = 0; i < n; ++i) {
         const int g = d + i;  // index in prefix || path
-        const int w = g < a.m ? a.prefix[(size_t)b * a.m + g] : path[g - a.m];
+        const int w = g < a.m ? pre[g] : path[g - a.m];
         fold(k0, k1, (uint32_t)w, (uint32_t)i, 1u);
     }
 }
@@ -716,6 +724,57 @@ __device__ int wave_race(const TopkRaceArgs& a, int rid, int slot0, int nslots, 
         *out_j = bj;
     }
     return bs < INFINITY ? bv : -1;
+}
+
+// A lane's first (token, slot) entry of a list race, loaded ahead: the list's length
+// and the token and logit of the lane's entry (its index clamped into the row's list,
+// so the loads never wait for the length and never leave the list).
+struct ListHead {
+    int n, v;
+    float x;
+};
+
+__device__ __forceinline__ ListHead list_head(const TopkRaceArgs& a, int rid, int nslots, int part) {
+    const int c = min((part * 64 + (int)(threadIdx.x & 63)) / nslots, a.cap - 1);
+    return ListHead{a.list_len[rid], a.list_tok[(size_t)rid * a.cap + c], a.list_val[(size_t)rid * a.cap + c]};
+}
+
+// wave_race with the lane's first entry taken from h (loaded while the previous race
+// of the chain ran); later entries are loaded in place.
+template <int LAYOUT>
+__device__ int wave_race_h(const TopkRaceArgs& a, const ListHead& h, int rid, int slot0, int nslots, float T,
+                           uint32_t k0, uint32_t k1, int part, int nparts, double* out_s, int* out_j) {
+    const int lane = threadIdx.x & 63;
+    const int n = h.n;
+    const int* lt = a.list_tok + (size_t)rid * a.cap;
+    const float* lv = a.list_val + (size_t)rid * a.cap;
+    // (token, slot) packed as token * 32 + slot (tokens < 2^19, slots < 32): the same
+    // order, one word less in each shuffle step
+    double bs = INFINITY;
+    int bvj = 0x7FFFFFFF;
+    for (int e = part * 64 + lane, first = 1; e < n * nslots; e += 64 * nparts, first = 0) {
+        const int c = e / nslots, j = slot0 + e % nslots;
+        const int v = first ? h.v : lt[c];
+        const float x = first ? h.x : lv[c];
+        const double s = log(tclock<LAYOUT>((uint32_t)a.V, (uint32_t)j, (uint32_t)v, k0, k1)) - (double)x / (double)T;
+        const int vj = (v << 5) | j;
+        if (s < bs || (s == bs && vj < bvj)) {
+            bs = s;
+            bvj = vj;
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const double os = __shfl_xor(bs, o);
+        const int ovj = __shfl_xor(bvj, o);
+        if (os < bs || (os == bs && ovj < bvj)) {
+            bs = os;
+            bvj = ovj;
+        }
+    }
+    *out_s = bs;
+    *out_j = bs < INFINITY ? (bvj & 31) : 0x7FFFFFFF;
+    return bs < INFINITY ? (bvj >> 5) : -1;
 }
 
 // The nu MPFR samples of one context from its row's list, by one wave: the nu
@@ -802,6 +861,7 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
     // drafts known before the call (depths < s_begin, or all of them as input)
     for (int e = tid; e < K * G; e += blockDim.x)
         sm.path[(e / G) * 33 + e % G] = a.draft_tokens[((size_t)b * K + e / G) * G + e % G];
+    for (int e = tid; e < a.m; e += blockDim.x) sm.pre[e] = a.prefix[(size_t)b * a.m + e];
     __syncthreads();
     const bool per = a.target_rows > 1;
     const int tslots = a.mpfr ? 1 : K;
@@ -815,7 +875,7 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
         if (s >= a.s_begin && s < d_end && w < dw) {
             for (int k = w; k < K; k += dw) {
                 if (!a.mpfr) {
-                    list_key(a, b, t0 + s, &sm.path[k * 33], s, k0, k1);
+                    list_key(a, sm.pre, t0 + s, &sm.path[k * 33], s, k0, k1, a.m);
                     const int y = wave_race<LAYOUT>(a, (b * K + k) * G + s, k, 1, a.T_draft, k0, k1);
                     if (lane == 0) sm.path[k * 33 + s] = y;
                 } else {
@@ -832,14 +892,22 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
                         }
                     }
                     if (!rep) continue;
-                    list_key(a, b, t0 + s, &sm.path[k * 33], s, k0, k1);
+                    list_key(a, sm.pre, t0 + s, &sm.path[k * 33], s, k0, k1, a.m);
                     wave_mpfr<LAYOUT>(a, sm, (b * K + k) * G + s, members, s, a.T_draft, k0, k1);
                 }
             }
         }
         if (a.target_rows == 1 && w >= dw) {
             const int ti = w - dw;
-            list_key(a, b, t0 + s, sm.chain, s, k0, k1);
+            if (s > 0 && a.m > 0) {
+                // the rest of the key was folded during the previous depth; its newest
+                // token is the previous depth's target
+                k0 = sm.tp[s & 1][0];
+                k1 = sm.tp[s & 1][1];
+                fold(k0, k1, (uint32_t)sm.chain[s - 1], (uint32_t)(a.m - 1), 1u);
+            } else {
+                list_key(a, sm.pre, t0 + s, sm.chain, s, k0, k1, a.m);
+            }
             double ps;
             int pj;
             const int pv = wave_race<LAYOUT>(a, D + b * (G + 1) + s, 0, tslots, a.T_target, k0, k1, ti, twv, &ps, &pj);
@@ -849,9 +917,20 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
                 sm.tj[ti] = pj;
             }
         }
+        if (a.target_rows == 1 && w == 0 && a.m > 0 && s < G) {
+            // the next depth's shared-chain key up to its newest token (this depth's
+            // target, not known yet): folded here by a draft wave, which finishes its
+            // races before the target waves do
+            uint32_t p0, p1;
+            list_key(a, sm.pre, t0 + s + 1, sm.chain, s + 1, p0, p1, a.m - 1);
+            if (lane == 0) {  // (the other parity: this depth's key was read from it)
+                sm.tp[(s + 1) & 1][0] = p0;
+                sm.tp[(s + 1) & 1][1] = p1;
+            }
+        }
         if (per)
             for (int k = w; k < K; k += nw) {
-                list_key(a, b, t0 + s, &sm.path[k * 33], s, k0, k1);
+                list_key(a, sm.pre, t0 + s, &sm.path[k * 33], s, k0, k1, a.m);
                 const int y = wave_race<LAYOUT>(a, D + (b * K + k) * (G + 1) + s, 0, tslots, a.T_target, k0, k1);
                 if (lane == 0) sm.pchain[k * 33 + s] = y;
             }
@@ -911,6 +990,152 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
     a.out_len[b] = tau;
 }
 
+// Distinct drafters, drafting only or with the shared target chain: one workgroup per
+// (sequence, chain) -- a draft path (one wave) or the target chain (four waves sharing
+// each race) -- so the chains' fp64 clocks spread over the CUs instead of sharing
+// one CU's SIMDs (one workgroup per sequence was bound by their throughput).  The
+// chains of a sequence are independent (the target chain is keyed by its own
+// prefix), so no workgroup waits for another; the walk runs in the next launch.
+struct ChainShared {
+    int path[33];          // this workgroup's chain: drafts of one path, or the targets
+    int pre[16];           // the sequence's context window before the block (m <= 16)
+    double ts[4];          // partial minima of a target race, one per wave
+    int tv[4], tj[4];
+    uint32_t tp[2][2];     // the chain's next key without its newest token (by depth parity)
+};
+
+constexpr int kChainWaves = 4;  // waves sharing each target race; one more folds the next key
+
+template <int LAYOUT>
+__global__ __launch_bounds__(64 * (kChainWaves + 1)) void topk_chain_kernel(TopkRaceArgs a) {
+    __shared__ ChainShared sm;
+    const int K = a.K, G = a.gamma;
+    const int nd = a.s_count > 0 ? K : 0, R = nd + (a.target_rows == 1 ? 1 : 0);
+    const int b = (int)blockIdx.x / R, r = (int)blockIdx.x % R;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int64_t t0 = a.start_pos[b];
+    const int d_end = a.s_begin + a.s_count;
+    for (int e = tid; e < a.m; e += blockDim.x) sm.pre[e] = a.prefix[(size_t)b * a.m + e];
+    if (r < nd)
+        for (int e = tid; e < a.s_begin; e += blockDim.x) sm.path[e] = a.draft_tokens[((size_t)b * K + r) * G + e];
+    __syncthreads();
+    uint32_t k0, k1;
+    if (r < nd) {
+        // draft path k: its races in depth order, by one wave (every lane keeps the
+        // same copy of the path, so no lane reads another lane's LDS write)
+        if (w != 0) return;
+        const int k = r;
+        ListHead h = list_head(a, (b * K + k) * G + a.s_begin, 1, 0);
+        for (int s = a.s_begin; s < d_end; ++s) {
+            list_key(a, sm.pre, t0 + s, sm.path, s, k0, k1, a.m);
+            const ListHead hs = h;
+            if (s + 1 < d_end) h = list_head(a, (b * K + k) * G + s + 1, 1, 0);  // the next depth's, in flight
+            double ps;
+            int pj;
+            sm.path[s] = wave_race_h<LAYOUT>(a, hs, (b * K + k) * G + s, k, 1, a.T_draft, k0, k1, 0, 1, &ps, &pj);
+        }
+        for (int s = a.s_begin + lane; s < d_end; s += 64) a.draft_tokens[((size_t)b * K + k) * G + s] = sm.path[s];
+        return;
+    }
+    // the shared target chain: each race's (token, slot) entries shared by the waves
+    const int tslots = K;
+    const int trow = a.B * K * G + b * (G + 1);
+    ListHead h = list_head(a, trow, tslots, w);
+    for (int s = 0; s <= G; ++s) {
+        if (w == kChainWaves) {
+            // the next depth's key up to its newest token (this race's winner), folded
+            // while the other waves race
+            if (a.m > 0 && s < G) {
+                uint32_t p0, p1;
+                list_key(a, sm.pre, t0 + s + 1, sm.path, s + 1, p0, p1, a.m - 1);
+                if (lane == 0) {  // (the other parity: this depth's key was read from it)
+                    sm.tp[(s + 1) & 1][0] = p0;
+                    sm.tp[(s + 1) & 1][1] = p1;
+                }
+            }
+            __syncthreads();
+            __syncthreads();
+            continue;
+        }
+        if (s > 0 && a.m > 0) {
+            k0 = sm.tp[s & 1][0];
+            k1 = sm.tp[s & 1][1];
+            fold(k0, k1, (uint32_t)sm.path[s - 1], (uint32_t)(a.m - 1), 1u);
+        } else {
+            list_key(a, sm.pre, t0 + s, sm.path, s, k0, k1, a.m);
+        }
+        const ListHead hs = h;
+        if (s < G) h = list_head(a, trow + s + 1, tslots, w);  // the next depth's, in flight
+        double ps;
+        int pj;
+        const int pv = wave_race_h<LAYOUT>(a, hs, trow + s, 0, tslots, a.T_target, k0, k1, w, kChainWaves, &ps, &pj);
+        if (lane == 0) {
+            sm.ts[w] = ps;
+            sm.tv[w] = pv;
+            sm.tj[w] = pj;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            double bs = sm.ts[0];
+            int bv = sm.tv[0], bj = sm.tj[0];
+            for (int i = 1; i < kChainWaves; ++i)
+                if (tlex(sm.ts[i], sm.tv[i], sm.tj[i], bs, bv, bj)) {
+                    bs = sm.ts[i];
+                    bv = sm.tv[i];
+                    bj = sm.tj[i];
+                }
+            sm.path[s] = bs < INFINITY ? bv : -1;
+        }
+        __syncthreads();
+    }
+    for (int s = tid; s <= G; s += blockDim.x) {
+        a.chain[(size_t)b * (G + 1) + s] = sm.path[s];
+        if (a.target_tokens) a.target_tokens[(size_t)b * (G + 1) + s] = sm.path[s];
+    }
+}
+
+// The walk of every sequence over its drafts and shared-chain targets (one thread per
+// sequence, as in the fused kernel), then the call's error bits to the sticky word
+// and the caller's status word.
+__global__ __launch_bounds__(256) void topk_walk_kernel(TopkRaceArgs a) {
+    const int b = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    const int K = a.K, G = a.gamma;
+    if (b == 0) {
+        const uint32_t bits = __hip_atomic_exchange(a.ctrl + kCtrlCallErrors, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (bits) __hip_atomic_fetch_or(a.ctrl + kCtrlErrors, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (a.status) *a.status = bits;
+    }
+    if (b >= a.B) return;
+    const int32_t* y = a.chain + (size_t)b * (G + 1);
+    const int32_t* d = a.draft_tokens + (size_t)b * K * G;
+    uint32_t act = K >= 32 ? 0xFFFFFFFFu : ((1u << K) - 1u);
+    int tau = 0;
+    bool done = false;
+    for (int s = 0; s < G && !done; ++s) {
+        const int ys = y[s];
+        a.out_tokens[(size_t)b * (G + 1) + s] = ys;
+        tau = s + 1;
+        if (ys < 0) {
+            done = true;
+            break;
+        }
+        uint32_t na = 0u;
+        for (int k = 0; k < K; ++k)
+            if (((act >> k) & 1u) && d[k * G + s] == ys) na |= 1u << k;
+        if (!na) {
+            done = true;
+            break;
+        }
+        act = na;
+    }
+    if (!done) {
+        a.out_tokens[(size_t)b * (G + 1) + G] = y[G];
+        tau = G + 1;
+    }
+    for (int s = tau; s <= G; ++s) a.out_tokens[(size_t)b * (G + 1) + s] = -1;
+    a.out_len[b] = tau;
+}
+
 }  // namespace
 
 hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t stream) {
@@ -924,9 +1149,28 @@ hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t st
 }
 
 hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t stream) {
-    // at most 8 waves (the TREE clocks need more than 128 registers per lane): one per
-    // draft path, and for a shared target chain up to four sharing each of its races
-    // (its K-slot races are the longest of a depth)
+    hipError_t e;
+    if (!a.mpfr && a.target_rows <= 1) {
+        // one workgroup per (sequence, chain), then the walk and the status
+        const int R = (a.s_count > 0 ? a.K : 0) + (a.target_rows == 1 ? 1 : 0);
+        if (R > 0) {
+            const dim3 grid((unsigned)(a.B * R)), block(64 * (kChainWaves + 1));
+            if (layout == 0)
+                hipLaunchKernelGGL(topk_chain_kernel<0>, grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL(topk_chain_kernel<1>, grid, block, 0, stream, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        if (a.target_rows == 1) {
+            hipLaunchKernelGGL(topk_walk_kernel, dim3((unsigned)((a.B + 255) / 256)), dim3(256), 0, stream, a);
+            return hipGetLastError();
+        }
+        return launch_finish_status(a.ctrl, a.status, stream);
+    }
+    // identical drafters (contexts group paths at every depth) or per-path target rows:
+    // one workgroup per sequence, at most 8 waves (the TREE clocks need more than 128
+    // registers per lane): one per draft path, and for a shared target chain up to four
+    // sharing each of its races (its K-slot races are the longest of a depth)
     TopkRaceArgs b = a;
     int waves;
     if (a.target_rows == 1) {
@@ -940,7 +1184,8 @@ hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t strea
         hipLaunchKernelGGL(topk_race_kernel<0>, dim3(a.B), dim3(64 * waves), 0, stream, b);
     else
         hipLaunchKernelGGL(topk_race_kernel<1>, dim3(a.B), dim3(64 * waves), 0, stream, b);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_finish_status(a.ctrl, a.status, stream);
 }
 
 }  // namespace psd
