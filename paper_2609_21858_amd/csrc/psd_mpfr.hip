@@ -73,6 +73,7 @@ struct MShared {
     float rowmax, theta;
     uint32_t kappa0, kappa1;
     int samples[32];
+    int pre[16];               // the sequence's context window before the block (m <= 16)
 };
 
 __device__ __forceinline__ float mload(const unsigned char* row, bool bf16, int v) {
@@ -260,6 +261,7 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
     // ---- the context of path k: the paths whose drafts at depths < s equal its own
     for (int e = tid; e < a.K * s; e += kMBlock)
         sm.path_tok[e] = a.draft_tokens[((size_t)b * a.K + e / s) * a.gamma + e % s];
+    for (int e = tid; e < a.m; e += kMBlock) sm.pre[e] = a.prefix[(size_t)b * a.m + e];
     if (tid == 0) sm.n_l4 = sm.n_l3 = sm.n_cand = 0;
     __syncthreads();
     if (wave == 0) {
@@ -299,7 +301,7 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
             fold(k0, k1, (uint32_t)t, (uint32_t)(t >> 32), 0u);
             for (int i = 0; i < a.m; ++i) {
                 const int g = s + i;  // index in prefix (m tokens) || path (s tokens)
-                const int w = g < a.m ? a.prefix[(size_t)b * a.m + g] : sm.path_tok[k * s + (g - a.m)];
+                const int w = g < a.m ? sm.pre[g] : sm.path_tok[k * s + (g - a.m)];
                 fold(k0, k1, (uint32_t)w, (uint32_t)i, 1u);
             }
             sm.kappa0 = k0;
@@ -362,15 +364,22 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
             sm.pair[i * 32 + j] = v >= 0 ? clock_f64<LAYOUT>(V, (uint32_t)j, (uint32_t)v, k0, k1) : 0.0;
         }
         __syncthreads();
+        // cumulative sums in arrival order, then every score at once; a seed token holds
+        // its group's maximum, so its logit is that maximum
         if (tid < kSeeds) {
-            const int v = sm.seed_tok[tid];
-            const double xs = v >= 0 ? ((double)mload(row, BF16, v) - (double)shift) / (double)a.T : 0.0;
             double G = 0.0;
             for (int j = 0; j < nu; ++j) {
                 G += sm.pair[tid * 32 + j];
-                sm.pair[tid * 32 + j] = v >= 0 ? log(G) - xs : INFINITY;
+                sm.pair[tid * 32 + j] = G;
             }
-            for (int j = nu; j < 32; ++j) sm.pair[tid * 32 + j] = INFINITY;
+        }
+        __syncthreads();
+        {
+            const int i = tid >> 5, j = tid & 31, v = sm.seed_tok[i];
+            static_assert(kSeeds * 32 == kMBlock, "one seed arrival slot per thread");
+            sm.pair[tid] = v >= 0 && j < nu
+                               ? log(sm.pair[tid]) - ((double)sm.gm[sm.seed_g[i]] - (double)shift) / (double)a.T
+                               : INFINITY;
         }
         __syncthreads();
         if (wave == 0) {
@@ -531,6 +540,67 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
 
         // ---- exact arrivals of the listed tokens; nu rounds of the lexicographic minimum
         const int nc = min(sm.n_cand, kMCand);
+        if (nc * nu <= kMBlock) {
+            // every arrival j < nu of every listed token at once (one fp64 clock per
+            // thread, in the seed array, free by now), the cumulative sums in arrival
+            // order (the same sums as one arrival at a time), then the nu smallest
+            // (score, token, arrival) by one wave: the same samples in the same order
+            const int t = tid, c = t / nu, j = t % nu;
+            if (t < nc * nu) sm.pair[t] = clock_f64<LAYOUT>(V, (uint32_t)j, (uint32_t)sm.cand_v[c], k0, k1);
+            __syncthreads();
+            if (t < nc) {
+                double G = 0.0;
+                for (int i = 0; i < nu; ++i) {
+                    G += sm.pair[t * nu + i];
+                    sm.pair[t * nu + i] = G;
+                }
+            }
+            __syncthreads();
+            if (t < nc * nu)
+                sm.pair[t] = log(sm.pair[t]) - ((double)sm.cand_x[c] - (double)shift) / (double)a.T;
+            __syncthreads();
+            if (wave == 0) {
+                double ps[4];
+                int pv[4], pj[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int e = lane + 64 * q;
+                    const bool ok = e < nc * nu;
+                    ps[q] = ok ? sm.pair[e] : INFINITY;
+                    pv[q] = ok ? sm.cand_v[e / nu] : 0x7FFFFFFF;
+                    pj[q] = ok ? e % nu : 0x7FFFFFFF;
+                }
+                for (int r = 0; r < nu; ++r) {
+                    double bs = INFINITY;
+                    int bv = 0x7FFFFFFF, bj = 0x7FFFFFFF, bi = -1;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        if (lexless(ps[q], pv[q], pj[q], bs, bv, bj)) {
+                            bs = ps[q];
+                            bv = pv[q];
+                            bj = pj[q];
+                            bi = lane + 64 * q;
+                        }
+#pragma unroll
+                    for (int off = 32; off > 0; off >>= 1) {
+                        const double os = __shfl_xor(bs, off);
+                        const int ov = __shfl_xor(bv, off), oj = __shfl_xor(bj, off), oi = __shfl_xor(bi, off);
+                        if (lexless(os, ov, oj, bs, bv, bj)) {
+                            bs = os;
+                            bv = ov;
+                            bj = oj;
+                            bi = oi;
+                        }
+                    }
+                    if (lane == 0) sm.samples[r] = bs < INFINITY ? bv : -1;
+                    if (bi >= 0 && (bi & 63) == lane) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            if (q == (bi >> 6)) ps[q] = INFINITY;
+                    }
+                }
+            }
+        } else {
         for (int c = tid; c < nc; c += kMBlock) {
             const int v = sm.cand_v[c];
             const double G = clock_f64<LAYOUT>(V, 0u, (uint32_t)v, k0, k1);
@@ -590,6 +660,7 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
                 }
             }
             __syncthreads();
+        }
         }
     }
     __syncthreads();
