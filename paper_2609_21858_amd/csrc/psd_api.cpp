@@ -181,6 +181,7 @@ psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_be
         const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);
         m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
         m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
+        m.row_seed = (int32_t*)((unsigned char*)b->workspace + M.seed);
         hipError_t e0 = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, vec, stream);
         if (e0 != hipSuccess) return hip_fail(e0, "MPFR stream kernel launch");
     }

@@ -53,19 +53,21 @@ struct MpfrArgs {
     float* row_gm;              // [B*K*gamma][groups] group maxima of the draft rows, and
     float* row_max;             // [B*K*gamma] their maxima (draft row ids), written by
                                 // the streaming launch and read by the sampling launches
+    int32_t* row_seed;          // [B*K*gamma][8] their seed tokens (-1: none), likewise
 };
 
 // Identical drafters: the draft rows' group maxima and maxima, streamed once per call
 // ahead of the depth-by-depth sampling, after the race kernel's workspace.
 struct MpfrLayout {
-    size_t gm, rmax, total;
+    size_t gm, rmax, seed, total;
 };
 inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
     MpfrLayout M;
     const size_t rows = (size_t)B * K * gamma;
     M.gm = L.total;
     M.rmax = align256(M.gm + rows * (size_t)L.ng * 4);
-    M.total = align256(M.rmax + rows * 4);
+    M.seed = align256(M.rmax + rows * 4);
+    M.total = align256(M.seed + rows * 8 * 4);  // 8 seeds per row
     return M;
 }
 

@@ -40,6 +40,7 @@ constexpr int kMBlock = 256;
 constexpr int kMaxGroups = 4096;  // 128-token groups of V <= 2^19
 constexpr int kMCand = 1024;      // listed candidate tokens of a context
 constexpr int kSeeds = 8;
+static_assert(kSeeds == 8, "the workspace holds 8 seed tokens per streamed row");
 constexpr float kMMargin = 1e-3f;  // fp32 pruning margin (score units)
 constexpr uint32_t kMErrCand = 2u;
 
@@ -231,20 +232,79 @@ __device__ __forceinline__ float mstream_row(const unsigned char* row, int V, fl
     return *rowmax;
 }
 
+// Seed groups of a row: the largest group of each eighth of the row (lowest index on
+// ties; -1 when the eighth has no finite logit), 32 lanes per eighth.  Every thread of
+// the workgroup calls it; no barrier.
+__device__ __forceinline__ void seed_groups(const float* gm, int ng, int* seed_g) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = 2 * wave + (lane >> 5), l32 = lane & 31;
+    const int g0 = r * ng / kSeeds, g1 = (r + 1) * ng / kSeeds;
+    float bv = -INFINITY;
+    int bg = 0x7FFFFFFF;
+    for (int g = g0 + l32; g < g1; g += 32)
+        if (gm[g] > bv) {
+            bv = gm[g];
+            bg = g;
+        }
+#pragma unroll
+    for (int off = 16; off > 0; off >>= 1) {
+        const float ov = __shfl_xor(bv, off);
+        const int og = __shfl_xor(bg, off);
+        if (ov > bv || (ov == bv && og < bg)) {
+            bv = ov;
+            bg = og;
+        }
+    }
+    if (l32 == 0) seed_g[r] = bv == -INFINITY ? -1 : bg;
+}
+
+// Each seed group's largest token (its lowest index holding the maximum), 16 lanes per
+// group (after a barrier that published seed_g).  Every thread calls it.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void seed_tokens(const unsigned char* row, int V, const float* gm, const int* seed_g,
+                                            int* seed_tok) {
+    const int tid = threadIdx.x;
+    if (tid < kSeeds * 16) {
+        const int i = tid >> 4, sub = tid & 15, g = seed_g[i];
+        int tk = 0x7FFFFFFF;
+        if (g >= 0) {
+            float x[8];
+            const int base = g * 128 + sub * 8;
+            mload8<BF16, VEC>(row, V, base, x);
+#pragma unroll
+            for (int t = 7; t >= 0; --t)
+                if (base + t < V && x[t] == gm[g]) tk = base + t;
+        }
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1) tk = min(tk, __shfl_xor(tk, off));
+        if (sub == 0) seed_tok[i] = g >= 0 && tk != 0x7FFFFFFF ? tk : -1;
+    }
+}
+
 // The streaming launch of a call: one workgroup per draft row of depths
 // [s_begin, s_begin + s_count), writing its group maxima, maximum and LSE.
 template <bool BF16, bool VEC>
 __global__ __launch_bounds__(kMBlock) void mpfr_stream_kernel(MpfrArgs a) {
     __shared__ float red_m[kMBlock / 64], red_s[kMBlock / 64], red_x[kMBlock / 64], rowmax;
+    __shared__ float gm[kMaxGroups];
+    __shared__ int seed_g[kSeeds], seed_tok[kSeeds];
     const int r = (int)blockIdx.x;
     const int b = r / (a.K * a.s_count), k = (r / a.s_count) % a.K, s = a.s_begin + r % a.s_count;
     const int ng = (a.V + 127) / 128;
     const size_t esize = BF16 ? 2 : 4;
     const unsigned char* row = (const unsigned char*)a.logits + (size_t)r * (size_t)a.V * esize;
     const size_t rid = ((size_t)b * a.K + k) * a.gamma + s;
-    const float xm = mstream_row<BF16, VEC>(row, a.V, a.invT, a.row_gm + rid * ng,
-                                            a.draft_lse ? a.draft_lse + rid : nullptr, red_m, red_s, red_x, &rowmax);
+    const float xm = mstream_row<BF16, VEC>(row, a.V, a.invT, gm, a.draft_lse ? a.draft_lse + rid : nullptr, red_m,
+                                            red_s, red_x, &rowmax);
+    // (mstream_row ends with a barrier: the group maxima are in LDS)
+    for (int g = threadIdx.x; g < ng; g += kMBlock) a.row_gm[rid * ng + g] = gm[g];
     if (threadIdx.x == 0) a.row_max[rid] = xm;
+    // the row's seed tokens, for every context this row may serve
+    seed_groups(gm, ng, seed_g);
+    __syncthreads();
+    seed_tokens<BF16, VEC>(row, a.V, gm, seed_g, seed_tok);
+    __syncthreads();
+    if (threadIdx.x < kSeeds) a.row_seed[rid * kSeeds + threadIdx.x] = seed_tok[threadIdx.x];
 }
 
 template <bool BF16, bool VEC, int LAYOUT>
@@ -279,6 +339,11 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
         const size_t rid = ((size_t)b * a.K + k) * a.gamma + s;
         for (int g = tid; g < ng; g += kMBlock) sm.gm[g] = a.row_gm[rid * ng + g];
         if (tid == 0) sm.rowmax = a.row_max[rid];
+        if (tid < kSeeds) {
+            const int tk = a.row_seed[rid * kSeeds + tid];
+            sm.seed_tok[tid] = tk;
+            sm.seed_g[tid] = tk >= 0 ? tk / 128 : -1;
+        }
     } else {
         // ---- stream the row: log-sum-exp, group maxima, row maximum
         __syncthreads();
@@ -312,50 +377,14 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
             for (int g = 16 * t; g < min(ng, 16 * t + 16); ++g) mx = fmaxf(mx, sm.gm[g]);
             sm.m3[t] = mx;
         }
-        {
-            // seed groups: the largest group of each eighth of the row (lowest index on ties)
-            const int r = 2 * wave + (lane >> 5), l32 = lane & 31;
-            const int g0 = r * ng / kSeeds, g1 = (r + 1) * ng / kSeeds;
-            float bv = -INFINITY;
-            int bg = 0x7FFFFFFF;
-            for (int g = g0 + l32; g < g1; g += 32)
-                if (sm.gm[g] > bv) {
-                    bv = sm.gm[g];
-                    bg = g;
-                }
-#pragma unroll
-            for (int off = 16; off > 0; off >>= 1) {
-                const float ov = __shfl_xor(bv, off);
-                const int og = __shfl_xor(bg, off);
-                if (ov > bv || (ov == bv && og < bg)) {
-                    bv = ov;
-                    bg = og;
-                }
-            }
-            if (l32 == 0) sm.seed_g[r] = bv == -INFINITY ? -1 : bg;
-        }
+        if (!a.row_seed) seed_groups(sm.gm, ng, sm.seed_g);
         __syncthreads();
         for (int t = tid; t < n4; t += kMBlock) {
             float mx = -INFINITY;
             for (int i = 16 * t; i < min(n3, 16 * t + 16); ++i) mx = fmaxf(mx, sm.m3[i]);
             sm.m4[t] = mx;
         }
-        if (tid < kSeeds * 16) {
-            // the seed group's largest token (its lowest index holding the maximum)
-            const int i = tid >> 4, sub = tid & 15, g = sm.seed_g[i];
-            int tk = 0x7FFFFFFF;
-            if (g >= 0) {
-                float x[8];
-                const int base = g * 128 + sub * 8;
-                mload8<BF16, VEC>(row, a.V, base, x);
-#pragma unroll
-                for (int t = 7; t >= 0; --t)
-                    if (base + t < a.V && x[t] == sm.gm[g]) tk = base + t;
-            }
-#pragma unroll
-            for (int off = 8; off > 0; off >>= 1) tk = min(tk, __shfl_xor(tk, off));
-            if (sub == 0) sm.seed_tok[i] = g >= 0 && tk != 0x7FFFFFFF ? tk : -1;
-        }
+        if (!a.row_seed) seed_tokens<BF16, VEC>(row, a.V, sm.gm, sm.seed_g, sm.seed_tok);
         __syncthreads();
         const uint32_t k0 = sm.kappa0, k1 = sm.kappa1;
         // seed arrivals, exact: E_j for every (seed, j < nu), then cumulative sums
