@@ -107,6 +107,10 @@ template <int LAYOUT>
 __device__ __forceinline__ double clock_f64(uint32_t V, uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
     return LAYOUT == 0 ? tree_clock_f64(V, slot, v, k0, k1) : flat_clock_f64(slot, v, k0, k1);
 }
+template <int LAYOUT>
+__device__ __forceinline__ float clock_f32(uint32_t V, uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
+    return LAYOUT == 0 ? tree_clock_f32(V, slot, v, k0, k1) : flat_clock_f32(slot, v, k0, k1);
+}
 
 __device__ __forceinline__ bool lexless(double s, int v, int j, double s2, int v2, int j2) {
     return s < s2 || (s == s2 && (v < v2 || (v == v2 && j < j2)));
@@ -387,19 +391,22 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
         if (!a.row_seed) seed_tokens<BF16, VEC>(row, a.V, sm.gm, sm.seed_g, sm.seed_tok);
         __syncthreads();
         const uint32_t k0 = sm.kappa0, k1 = sm.kappa1;
-        // seed arrivals, exact: E_j for every (seed, j < nu), then cumulative sums
+        // seed arrivals in float32: E_j for every (seed, j < nu), the cumulative sums in
+        // arrival order, then every score at once.  theta only has to bound the context's
+        // nu-th smallest score from above: float32 scores are within the pruning margin
+        // of the exact ones (the same assumption as every float32 bound of the race), and
+        // theta carries one margin for that on top of its own.  A seed token holds its
+        // group's maximum, so its logit is that maximum.
         for (int e = tid; e < kSeeds * nu; e += kMBlock) {
             const int i = e / nu, j = e % nu, v = sm.seed_tok[i];
-            sm.pair[i * 32 + j] = v >= 0 ? clock_f64<LAYOUT>(V, (uint32_t)j, (uint32_t)v, k0, k1) : 0.0;
+            sm.pair[i * 32 + j] = v >= 0 ? (double)clock_f32<LAYOUT>(V, (uint32_t)j, (uint32_t)v, k0, k1) : 0.0;
         }
         __syncthreads();
-        // cumulative sums in arrival order, then every score at once; a seed token holds
-        // its group's maximum, so its logit is that maximum
         if (tid < kSeeds) {
-            double G = 0.0;
+            float G = 0.f;
             for (int j = 0; j < nu; ++j) {
-                G += sm.pair[tid * 32 + j];
-                sm.pair[tid * 32 + j] = G;
+                G += (float)sm.pair[tid * 32 + j];
+                sm.pair[tid * 32 + j] = (double)G;
             }
         }
         __syncthreads();
@@ -407,7 +414,7 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
             const int i = tid >> 5, j = tid & 31, v = sm.seed_tok[i];
             static_assert(kSeeds * 32 == kMBlock, "one seed arrival slot per thread");
             sm.pair[tid] = v >= 0 && j < nu
-                               ? log(sm.pair[tid]) - ((double)sm.gm[sm.seed_g[i]] - (double)shift) / (double)a.T
+                               ? (double)(ln_f32((float)sm.pair[tid]) - (sm.gm[sm.seed_g[i]] - shift) * a.invT)
                                : INFINITY;
         }
         __syncthreads();
@@ -438,7 +445,7 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
                 th = mv;
                 if ((mi & 63) == lane) v4[mi >> 6] = INFINITY;
             }
-            if (lane == 0) sm.theta = th == INFINITY ? INFINITY : (float)th + kMMargin;
+            if (lane == 0) sm.theta = th == INFINITY ? INFINITY : (float)th + 2.f * kMMargin;
         }
         __syncthreads();
 
