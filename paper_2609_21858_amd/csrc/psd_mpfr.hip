@@ -103,6 +103,46 @@ __device__ __forceinline__ void mload8(const unsigned char* row, int V, int base
     }
 }
 
+// Raw words of 8 logits for a load issued ahead of its use (vector path: one or two
+// 16-byte loads, the address clamped into the row; scalar path: nothing loaded ahead).
+template <bool BF16, bool VEC>
+struct MRaw {
+    uint4 w[BF16 ? 1 : 2];
+};
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void mraw_load(const unsigned char* row, int V, int base, MRaw<BF16, VEC>& r) {
+    if constexpr (VEC) {
+        if constexpr (BF16) {
+            r.w[0] = *(const uint4*)((const uint16_t*)row + min(base, V - 8));
+        } else {
+            r.w[0] = *(const uint4*)((const float*)row + min(base, V - 4));
+            r.w[1] = *(const uint4*)((const float*)row + min(base + 4, V - 4));
+        }
+    }
+}
+// The 8 logits from `base` (-inf past V) out of the raw words (scalar path: loaded here).
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void mraw_unpack(const unsigned char* row, int V, int base, const MRaw<BF16, VEC>& r,
+                                            float (&x)[8]) {
+    if constexpr (VEC) {
+        if constexpr (BF16) {
+            const uint4 u = r.w[0];
+            x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
+            x[4] = bf16_lo(u.z); x[5] = bf16_hi(u.z); x[6] = bf16_lo(u.w); x[7] = bf16_hi(u.w);
+        } else {
+            x[0] = __uint_as_float(r.w[0].x); x[1] = __uint_as_float(r.w[0].y);
+            x[2] = __uint_as_float(r.w[0].z); x[3] = __uint_as_float(r.w[0].w);
+            x[4] = __uint_as_float(r.w[1].x); x[5] = __uint_as_float(r.w[1].y);
+            x[6] = __uint_as_float(r.w[1].z); x[7] = __uint_as_float(r.w[1].w);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (base + i >= V) x[i] = -INFINITY;
+    } else {
+        mload8<BF16, VEC>(row, V, base, x);
+    }
+}
+
 template <int LAYOUT>
 __device__ __forceinline__ double clock_f64(uint32_t V, uint32_t slot, uint32_t v, uint32_t k0, uint32_t k1) {
     return LAYOUT == 0 ? tree_clock_f64(V, slot, v, k0, k1) : flat_clock_f64(slot, v, k0, k1);
@@ -177,10 +217,19 @@ __device__ __forceinline__ float mstream_row(const unsigned char* row, int V, fl
     const float c2 = invT * 1.4426950408889634f;
     float mrun = -INFINITY, srun = 0.f, xmax = -INFINITY;
     const int nstep = (V + 2047) / 2048;
+    // software-pipelined: the next four units' raw words are loaded before the current
+    // four are reduced (words past the row are never used)
+    MRaw<BF16, VEC> wn[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) mraw_load<BF16, VEC>(row, V, q * 2048 + 8 * tid, wn[q]);
     for (int st0 = 0; st0 < nstep; st0 += 4) {
         float x[4][8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) mload8<BF16, VEC>(row, V, (st0 + q) * 2048 + 8 * tid, x[q]);
+        for (int q = 0; q < 4; ++q) mraw_unpack<BF16, VEC>(row, V, (st0 + q) * 2048 + 8 * tid, wn[q], x[q]);
+        if (st0 + 4 < nstep) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) mraw_load<BF16, VEC>(row, V, (st0 + 4 + q) * 2048 + 8 * tid, wn[q]);
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             if (st0 + q >= nstep) break;
