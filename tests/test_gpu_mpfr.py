@@ -143,6 +143,22 @@ def test_mpfr_wide_batch_streams_in_each_depth(psd, layout):
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_many_listed_tokens(psd, layout):
+    """Flat and two-valued draft rows with 16 identical drafters: the seeds bound theta
+    loosely, hundreds of tokens are listed (theta tightened, then nu = 16 arrivals of
+    each), more than one workgroup's threads -- the samples then come from nu rounds
+    that each rebuild only the winner's next arrival; random rows of the same block
+    take the all-arrivals-at-once form.  Same parity bar."""
+    w = workloads.custom(5000, 16, 2, 3, dtype="bf16", m=2, tau=0.5, sigma=2.0, alpha=1.0, T_draft=1.0)
+    blk = workloads.make_block(w, 31)
+    dl = blk["draft_logits"]
+    dl[0] = 0.25                       # every logit equal
+    dl[1, :, :, ::2] = 1.0             # two values
+    dl[1, :, :, 1::2] = -1.0
+    run_mpfr(psd, w, 31, layout, blk=blk)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
 def test_mpfr_config2_full(psd, layout):
     run_mpfr(psd, workloads.WORKLOADS[2], 2, layout)
 
