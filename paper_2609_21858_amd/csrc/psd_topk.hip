@@ -992,10 +992,10 @@ __global__ __launch_bounds__(512) void topk_race_kernel(TopkRaceArgs a) {
 
 // Distinct drafters, drafting only or with the shared target chain: one workgroup per
 // (sequence, chain) -- a draft path (one wave) or the target chain (four waves sharing
-// each race) -- so the chains' fp64 clocks spread over the CUs instead of sharing
-// one CU's SIMDs (one workgroup per sequence was bound by their throughput).  The
-// chains of a sequence are independent (the target chain is keyed by its own
-// prefix), so no workgroup waits for another; the walk runs in the next launch.
+// each race, a fifth folding the next key) -- so a sequence's chains run on different
+// CUs rather than sharing one CU's SIMDs.  The chains of a sequence are independent
+// (the target chain is keyed by its own prefix), so no workgroup waits for another;
+// the walk runs in the next launch.
 struct ChainShared {
     int path[33];          // this workgroup's chain: drafts of one path, or the targets
     int pre[16];           // the sequence's context window before the block (m <= 16)
