@@ -250,7 +250,8 @@ __device__ __forceinline__ void stream_group_max(SelShared& sm, const unsigned c
 }
 
 // The candidates of the row's top-k set, without a per-logit pass over the row: t =
-// the top_k-th largest key class among the group maxima (a block-wide bisection), so
+// the top_k-th largest key class among the group maxima (a bisection with ballot
+// counts, in one wave when it holds every group maximum, else block-wide), so
 // at least top_k logits reach t and every logit of the top-k set (ties at the cut
 // included) reaches it too; only groups whose maximum reaches t can hold such a
 // logit, and they are read again.  With fewer groups than top_k, every group with a
