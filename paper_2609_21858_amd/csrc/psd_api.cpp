@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "../../include/psd.h"
 #include "psd_launch.hpp"
@@ -20,6 +21,42 @@ thread_local char g_err[512] = "";
 // Polls of a bounded cross-workgroup wait before it gives up (test hook, psd_set_spin_limit).
 constexpr uint32_t kDefaultSpinLimit = 1u << 22;
 std::atomic<uint32_t> g_spin_limit{kDefaultSpinLimit};
+
+// A side stream and a fork and a join event per device, created on first use and
+// kept until the process ends.  They let an identical-drafter call race its
+// target chain beside its drafting launches.  The mutex is held from the fork's
+// record to the join's wait, so calls from several host threads never mix up
+// their events.
+constexpr int kMaxForkDevices = 64;
+struct Fork {
+    hipStream_t side;
+    hipEvent_t in, out;
+};
+std::mutex g_fork_mu;
+Fork g_fork[kMaxForkDevices] = {};
+
+// The current device's fork objects (the caller holds g_fork_mu), or nullptr if they
+// cannot be created.
+Fork* fork_objects() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxForkDevices) return nullptr;
+    Fork& f = g_fork[dev];
+    if (!f.side) {
+        hipStream_t st = nullptr;
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+        if (hipEventCreateWithFlags(&e0, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess) {
+            if (e0) (void)hipEventDestroy(e0);
+            (void)hipStreamDestroy(st);
+            return nullptr;
+        }
+        f.in = e0;
+        f.out = e1;
+        f.side = st;
+    }
+    return &f;
+}
 
 psd_status fail(psd_status st, const char* fmt, ...) {
     va_list ap;
@@ -148,11 +185,11 @@ void build_depths(psd::RaceArgs& a, int n_depth) {
 }
 
 // Identical drafters: depths [s_begin, s_begin + s_count) drafted one launch per depth
-// (each depth's contexts depend on the previous depth's drafts).
-psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_begin, int32_t s_count,
-                           const void* draft_logits, int32_t* draft_tokens, float* draft_lse, hipStream_t stream) {
-    const size_t es = p->dtype == PSD_BF16 ? 2 : 4;
-    const bool vec = ((size_t)p->vocab * es) % 16 == 0 && aligned16(draft_logits);
+// (each depth's contexts depend on the previous depth's drafts).  mpfr_args fills
+// the arguments, mpfr_stream_rows launches the call's streaming pass when there is
+// one, mpfr_sample_depths the depth launches.
+psd::MpfrArgs mpfr_args(const psd_params* p, const psd_block* b, int32_t s_begin, int32_t s_count,
+                        const void* draft_logits, int32_t* draft_tokens, float* draft_lse) {
     psd::MpfrArgs m;
     memset(&m, 0, sizeof m);
     m.logits = draft_logits;
@@ -172,25 +209,45 @@ psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_be
     m.s_count = s_count;
     m.T = p->temp_draft;
     m.invT = 1.0f / p->temp_draft;
-    // A depth's launch has one workgroup per (sequence, path), each streaming its row.
-    // When those cannot fill the device (B K < 1024), every draft row of the call is
-    // streamed first in one launch (group maxima, maxima, LSE) and the depth launches
-    // only sample; otherwise each depth's streaming overlaps its contexts' sampling.
-    if ((long)b->batch * p->num_drafts < 1024) {
-        const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
-        const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);
-        m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
-        m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
-        m.row_seed = (int32_t*)((unsigned char*)b->workspace + M.seed);
-        hipError_t e0 = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, vec, stream);
-        if (e0 != hipSuccess) return hip_fail(e0, "MPFR stream kernel launch");
-    }
-    for (int s = s_begin; s < s_begin + s_count; ++s) {
+    return m;
+}
+
+bool mpfr_vec(const psd_params* p, const void* draft_logits) {
+    const size_t es = p->dtype == PSD_BF16 ? 2 : 4;
+    return ((size_t)p->vocab * es) % 16 == 0 && aligned16(draft_logits);
+}
+
+// A depth's launch has one workgroup per (sequence, path), each streaming its row.
+// When those cannot fill the device (B K < 1024), every draft row of the call is
+// streamed first in one launch (group maxima, maxima, LSE) and the depth launches
+// only sample; otherwise each depth's streaming overlaps its contexts' sampling.
+psd_status mpfr_stream_rows(const psd_params* p, const psd_block* b, psd::MpfrArgs& m, hipStream_t stream) {
+    if ((long)b->batch * p->num_drafts >= 1024) return PSD_OK;
+    const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
+    const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);
+    m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
+    m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
+    m.row_seed = (int32_t*)((unsigned char*)b->workspace + M.seed);
+    hipError_t e = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, mpfr_vec(p, m.logits), stream);
+    if (e != hipSuccess) return hip_fail(e, "MPFR stream kernel launch");
+    return PSD_OK;
+}
+
+psd_status mpfr_sample_depths(const psd_params* p, psd::MpfrArgs& m, hipStream_t stream) {
+    for (int s = m.s_begin; s < m.s_begin + m.s_count; ++s) {
         m.s = s;
-        hipError_t e = psd::launch_mpfr_draft(m, p->dtype == PSD_BF16, vec, p->clocks, stream);
+        hipError_t e = psd::launch_mpfr_draft(m, p->dtype == PSD_BF16, mpfr_vec(p, m.logits), p->clocks, stream);
         if (e != hipSuccess) return hip_fail(e, "MPFR draft kernel launch");
     }
     return PSD_OK;
+}
+
+psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_begin, int32_t s_count,
+                           const void* draft_logits, int32_t* draft_tokens, float* draft_lse, hipStream_t stream) {
+    psd::MpfrArgs m = mpfr_args(p, b, s_begin, s_count, draft_logits, draft_tokens, draft_lse);
+    psd_status st = mpfr_stream_rows(p, b, m, stream);
+    if (st != PSD_OK) return st;
+    return mpfr_sample_depths(p, m, stream);
 }
 
 // Truncated logits: the kept list of every row of the call, then one workgroup per
@@ -354,10 +411,72 @@ psd_status psd_draft(const psd_params* params, const psd_block* block, int32_t s
 
 namespace {
 
+// Identical drafters with one shared target chain: the target chain needs no draft
+// until the walk, so the fused kernel races it (without the walk) on the side
+// stream while the drafting launches run on the caller's stream; the walk kernel
+// follows both.  The race kernel's error bits go to a control word that the walk
+// kernel adds to the call's status.
+psd_status verify_mpfr_forked(const psd_params* params, const psd_block* block, const void* target_logits,
+                              const void* draft_logits, int32_t* draft_tokens, int32_t* out_tokens,
+                              int32_t* out_len, float* target_lse, float* draft_lse, int32_t* target_tokens,
+                              hipStream_t stream, Fork& f) {
+    unsigned char* ws = (unsigned char*)block->workspace;
+    const psd::WsLayout L = psd::ws_layout(block->batch, params->num_drafts, block->gamma, params->vocab,
+                                           params->dtype == PSD_BF16);
+    const psd::MpfrLayout M = psd::mpfr_layout(L, block->batch, params->num_drafts, block->gamma);
+    uint32_t* ctrl = (uint32_t*)(ws + L.ctrl);
+    int32_t* y = target_tokens ? target_tokens : (int32_t*)(ws + M.ytok);
+    psd::RaceArgs a = base_args(params, block);
+    a.target_logits = target_logits;
+    a.draft_tokens = draft_tokens;
+    a.out_tokens = out_tokens;
+    a.out_len = out_len;
+    a.target_lse = target_lse;
+    a.target_tokens = y;
+    a.s_begin = 0;
+    a.s_count = 0;
+    a.target_rows = 1;
+    build_depths(a, block->gamma + 1);
+    a.walk_kind = -1;  // no row walks: the walk kernel does, after the drafts
+    a.status = ctrl + psd::kCtrlRaceBits;
+    // The streaming pass first: the race kernel, whose streaming workgroups would
+    // otherwise hold the device while it runs, then overlaps only the depth launches
+    // (236 vs 256 us per call at V=128256, K=4, gamma=4, B=64).
+    psd::MpfrArgs m = mpfr_args(params, block, 0, block->gamma, draft_logits, draft_tokens, draft_lse);
+    psd_status st = mpfr_stream_rows(params, block, m, stream);
+    if (st != PSD_OK) return st;
+    hipError_t e;
+    if ((e = hipEventRecord(f.in, stream)) != hipSuccess) return hip_fail(e, "fork event record");
+    if ((e = hipStreamWaitEvent(f.side, f.in, 0)) != hipSuccess) return hip_fail(e, "fork event wait");
+    if ((st = run_race(params, a, f.side)) != PSD_OK) return st;
+    // from here on the join is always enqueued, so the caller's stream never runs
+    // ahead of the side stream's race
+    psd_status sd = mpfr_sample_depths(params, m, stream);
+    if ((e = hipEventRecord(f.out, f.side)) != hipSuccess) return hip_fail(e, "join event record");
+    if ((e = hipStreamWaitEvent(stream, f.out, 0)) != hipSuccess) return hip_fail(e, "join event wait");
+    if (sd != PSD_OK) return sd;
+    psd::TopkRaceArgs w;
+    memset(&w, 0, sizeof w);
+    w.draft_tokens = draft_tokens;
+    w.out_tokens = out_tokens;
+    w.out_len = out_len;
+    w.chain = y;
+    w.K = params->num_drafts;
+    w.B = block->batch;
+    w.gamma = block->gamma;
+    w.ctrl = ctrl;
+    w.status = block->status;
+    w.status_in = ctrl + psd::kCtrlRaceBits;
+    if ((e = psd::launch_walk(w, stream)) != hipSuccess) return hip_fail(e, "walk kernel launch");
+    return PSD_OK;
+}
+
+// may_fork: the identical-drafter form may use the side stream (not under stream
+// capture, and not from the allocation-free entry point).
 psd_status verify_impl(const psd_params* params, const psd_block* block, int32_t target_rows,
                        const void* target_logits, const void* draft_logits, int32_t* draft_tokens,
                        int32_t* out_tokens, int32_t* out_len, float* target_lse, float* draft_lse,
-                       int32_t* target_tokens, hipStream_t stream) {
+                       int32_t* target_tokens, hipStream_t stream, bool may_fork) {
     psd_status st;
     if ((st = check_block(params, block)) != PSD_OK) return st;
     if (target_rows != 1 && target_rows != params->num_drafts)
@@ -369,6 +488,18 @@ psd_status verify_impl(const psd_params* params, const psd_block* block, int32_t
     if (params->top_k > 0)
         return run_topk(params, block, 0, block->gamma, target_rows, target_logits, draft_logits, draft_tokens,
                         out_tokens, out_len, target_lse, draft_lse, target_tokens, stream);
+    if (params->mode == PSD_MODE_MPFR && draft_logits && target_rows == 1 && may_fork) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(stream, &cs);
+        if (e != hipSuccess) return hip_fail(e, "stream capture query");
+        if (cs == hipStreamCaptureStatusNone) {
+            std::lock_guard<std::mutex> lock(g_fork_mu);
+            Fork* f = fork_objects();
+            if (f)
+                return verify_mpfr_forked(params, block, target_logits, draft_logits, draft_tokens, out_tokens,
+                                          out_len, target_lse, draft_lse, target_tokens, stream, *f);
+        }
+    }
     if (params->mode == PSD_MODE_MPFR && draft_logits) {
         // identical drafters: the context tree is drafted depth by depth first, then the
         // target rows race slot 0 in the fused kernel with the drafts as input
@@ -404,7 +535,7 @@ psd_status psd_verify(const psd_params* params, const psd_block* block, int32_t 
     psd_status st = check_params(params);
     if (st != PSD_OK) return st;
     return verify_impl(params, block, target_rows, target_logits, draft_logits, draft_tokens, out_tokens, out_len,
-                       target_lse, draft_lse, target_tokens, stream);
+                       target_lse, draft_lse, target_tokens, stream, true);
 }
 
 psd_status psd_verify_static(const psd_params* params, const psd_block* block, int32_t target_rows,
@@ -429,7 +560,7 @@ psd_status psd_verify_static(const psd_params* params, const psd_block* block, i
     b.workspace = ws;
     b.workspace_bytes = psd::kStaticScratchBytes;
     return verify_impl(params, &b, target_rows, target_logits, draft_logits, draft_tokens, out_tokens, out_len,
-                       target_lse, draft_lse, target_tokens, stream);
+                       target_lse, draft_lse, target_tokens, stream, false);
 }
 
 psd_status psd_detect(const psd_params* params, int32_t n_seq, int32_t seq_len, const int32_t* tokens,
@@ -767,7 +898,7 @@ psd_status psd_generate(const psd_params* params, const psd_toy_lm* lm, int32_t 
     auto body = [&](hipStream_t s) -> psd_status {
         hipError_t e = psd::launch_toy_rows(toy, bf16, s);
         if (e != hipSuccess) return hip_fail(e, "toy model kernel launch");
-        psd_status r = verify_impl(params, &blk, 1, tl, dl, dt, ot, ol, nullptr, nullptr, nullptr, s);
+        psd_status r = verify_impl(params, &blk, 1, tl, dl, dt, ot, ol, nullptr, nullptr, nullptr, s, false);
         if (r != PSD_OK) return r;
         if ((e = psd::launch_advance(adv, s)) != hipSuccess) return hip_fail(e, "advance kernel launch");
         return PSD_OK;

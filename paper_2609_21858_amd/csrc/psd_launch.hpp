@@ -7,6 +7,10 @@
 
 namespace psd {
 
+// Control word that carries the race kernel's share of a call's error bits to a
+// later walk kernel of the same call (a word the race kernel uses for nothing else).
+constexpr int kCtrlRaceBits = 7;
+
 struct DetectArgs {
     const int32_t* tokens;  // [n_seq][row_stride], positions [0, seq_len) of each row scored
     const int32_t* n0;      // [n_seq]
@@ -57,9 +61,10 @@ struct MpfrArgs {
 };
 
 // Identical drafters: the draft rows' group maxima and maxima, streamed once per call
-// ahead of the depth-by-depth sampling, after the race kernel's workspace.
+// ahead of the depth-by-depth sampling, after the race kernel's workspace, then the
+// shared target chain's tokens for a walk kernel that runs after the drafts.
 struct MpfrLayout {
-    size_t gm, rmax, seed, total;
+    size_t gm, rmax, seed, ytok, total;
 };
 inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
     MpfrLayout M;
@@ -67,7 +72,8 @@ inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
     M.gm = L.total;
     M.rmax = align256(M.gm + rows * (size_t)L.ng * 4);
     M.seed = align256(M.rmax + rows * 4);
-    M.total = align256(M.seed + rows * 8 * 4);  // 8 seeds per row
+    M.ytok = align256(M.seed + rows * 8 * 4);  // 8 seeds per row
+    M.total = align256(M.ytok + (size_t)B * (gamma + 1) * 4);  // shared-chain targets [B][gamma+1]
     return M;
 }
 
@@ -143,6 +149,8 @@ struct TopkRaceArgs {
     int32_t* chain;          // workspace [B][gamma + 1]: shared-chain targets for the walk kernel
     uint32_t* ctrl;          // workspace control words (the call's error bits)
     uint32_t* status;        // nullable: the call's error bits for the caller
+    const uint32_t* status_in;  // nullable: bits already taken from the call by an earlier
+                                // kernel of the same call, added to *status
 };
 
 // Position-indexed toy language model: target rows [B][gamma+1][V] at positions
@@ -177,6 +185,9 @@ hipError_t launch_toy_rows(const ToyArgs& a, bool bf16, hipStream_t stream);
 hipError_t launch_advance(const AdvanceArgs& a, hipStream_t stream);
 hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t stream);
 hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t stream);
+// The walk alone (one thread per sequence) over shared-chain targets a.chain
+// [B][gamma+1] and the drafts, then the call's error bits (with *a.status_in).
+hipError_t launch_walk(const TopkRaceArgs& a, hipStream_t stream);
 
 hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
 hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);

@@ -1104,7 +1104,7 @@ __global__ __launch_bounds__(256) void topk_walk_kernel(TopkRaceArgs a) {
     if (b == 0) {
         const uint32_t bits = __hip_atomic_exchange(a.ctrl + kCtrlCallErrors, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (bits) __hip_atomic_fetch_or(a.ctrl + kCtrlErrors, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (a.status) *a.status = bits;
+        if (a.status) *a.status = bits | (a.status_in ? *a.status_in : 0u);
     }
     if (b >= a.B) return;
     const int32_t* y = a.chain + (size_t)b * (G + 1);
@@ -1138,6 +1138,11 @@ __global__ __launch_bounds__(256) void topk_walk_kernel(TopkRaceArgs a) {
 }
 
 }  // namespace
+
+hipError_t launch_walk(const TopkRaceArgs& a, hipStream_t stream) {
+    hipLaunchKernelGGL(topk_walk_kernel, dim3((unsigned)((a.B + 255) / 256)), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_topk_select(const TopkSelectArgs& a, bool bf16, hipStream_t stream) {
     const int n = a.seg[0].n_rows + a.seg[1].n_rows;

@@ -180,3 +180,67 @@ def test_mpfr_detection_pivot_is_slot0(psd):
         for i in range(8):
             S, M, _ = oracle.detect_sequence(w.key, w.m, 1, w.V, _np(toks)[i], w.m, layout)
             assert int(count[i]) == M and abs(float(score[i]) - S) <= 1e-9 * abs(S)
+
+
+def test_mpfr_side_stream_status_and_forced_wait_timeouts(psd):
+    """With one shared target chain, the target races run on the library's side
+    stream beside the drafting launches, and the walk kernel adds their error bits
+    to the call's status word.  With a spin limit of one poll (set from the host) the
+    race's waits for other workgroups give up at once: every kernel still exits, and
+    bit 0 reaches the status word and the workspace's sticky bits.  With the limit
+    restored and the workspace cleared, the same call is healthy and matches the oracle."""
+    w = workloads.WORKLOADS[2]
+    blk = workloads.make_block(w, 7)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in blk.items()}
+    params = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype,
+                             mode=psd.PSD_MODE_MPFR)
+    ws = psd.new_workspace(params, w.B, w.gamma, DEV)
+    status = torch.full((1,), -1, dtype=torch.int32, device=DEV)
+    print(f"[mpfr] forced wait timeouts {w.name}", flush=True)
+    try:
+        psd.set_spin_limit(1)
+        out = psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], g["draft_logits"],
+                         status=status)
+        torch.cuda.synchronize()
+    finally:
+        psd.set_spin_limit(0)
+    assert int(status[0]) & psd.ERR_SPIN, int(status[0])
+    assert psd.workspace_errors(ws) & psd.ERR_SPIN
+    lens = _np(out["out_len"])
+    assert np.all((lens >= 1) & (lens <= w.gamma + 1))  # outputs unreliable but well formed
+    psd.workspace_clear(ws)
+    status.fill_(-1)
+    psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], g["draft_logits"], status=status)
+    torch.cuda.synchronize()
+    assert int(status[0]) == 0 and psd.workspace_errors(ws) == 0
+    run_mpfr(psd, w, 7, 0, blk=blk)
+
+
+def test_mpfr_side_stream_follows_caller_stream(psd):
+    """The side stream's target races wait for the caller's earlier work on its
+    stream.  On a non-default stream, a copy writes the target rows into a buffer
+    that held other rows (every target race would pick token 5 there), and the call
+    follows at once.  The outputs equal those of the oracle-checked call on rows
+    already in place, and the target winners are returned on the caller's stream."""
+    w = workloads.WORKLOADS[3]
+    blk = workloads.make_block(w, 13, device=DEV)
+    ref, _ = run_mpfr(psd, w, 13, 0, blk=blk, seqs=range(0, w.B, 16))
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in blk.items()}
+    params = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype,
+                             mode=psd.PSD_MODE_MPFR)
+    ws = psd.new_workspace(params, w.B, w.gamma, DEV)
+    buf = torch.zeros_like(g["target_logits"])
+    buf[..., 5] = 30.0
+    status = torch.full((1,), -1, dtype=torch.int32, device=DEV)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    print(f"[mpfr] caller stream ordering {w.name}", flush=True)
+    with torch.cuda.stream(s):
+        buf.copy_(g["target_logits"])
+        out = psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], buf, g["draft_logits"],
+                         want_targets=True, status=status)
+        got = {k: v.clone() for k, v in out.items()}
+    s.synchronize()
+    assert int(status[0]) == 0 and psd.workspace_errors(ws) == 0
+    for k in ("out_tokens", "out_len", "draft_tokens", "target_tokens"):
+        assert torch.equal(got[k], ref[k]), k
