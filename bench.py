@@ -85,10 +85,10 @@ def write_counters(csv_path: str, out: str = COUNTERS_FILE) -> dict:
 
 def headline_race_rows(rows):
     """Race-kernel rows of the headline (distinct-drafter) step: those dispatched before
-    the first identical-drafter draft kernel (the bench's MPFR leg runs afterwards)."""
+    the first identical-drafter kernel (the bench's MPFR leg runs afterwards, and its
+    streaming launch comes before its own race kernel on the side stream)."""
     rows = sorted(rows, key=lambda r: int(r["Dispatch_Id"]))
-    first_mpfr = min((int(r["Dispatch_Id"]) for r in rows if "mpfr_draft_kernel" in r["Kernel_Name"]),
-                     default=1 << 62)
+    first_mpfr = min((int(r["Dispatch_Id"]) for r in rows if "mpfr_" in r["Kernel_Name"]), default=1 << 62)
     return [r for r in rows if "race_kernel<" in r["Kernel_Name"] and int(r["Dispatch_Id"]) < first_mpfr]
 
 

@@ -20,7 +20,7 @@
 //    walk.  Distinct drafters (drafting, or with the shared target chain):
 //    topk_chain_kernel, one workgroup per (sequence, chain) -- a draft path, or the
 //    target chain, whose races four waves share while a fifth folds the next key --
-//    then topk_walk_kernel (the walk, one thread per sequence, and the status word).
+//    then topk_walk_kernel (the walk, one wave per sequence, and the status word).
 //    Identical drafters or per-path target rows: topk_race_kernel, one workgroup per
 //    sequence with one wave per chain, depth by depth (identical drafters group the
 //    paths into contexts at every depth).
@@ -1095,25 +1095,39 @@ __global__ __launch_bounds__(64 * (kChainWaves + 1)) void topk_chain_kernel(Topk
     }
 }
 
-// The walk of every sequence over its drafts and shared-chain targets (one thread per
-// sequence, as in the fused kernel), then the call's error bits to the sticky word
-// and the caller's status word.
-__global__ __launch_bounds__(256) void topk_walk_kernel(TopkRaceArgs a) {
-    const int b = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+// The walk of every sequence over its drafts and shared-chain targets, then the call's
+// error bits to the sticky word and the caller's status word.  One wave per sequence:
+// its lanes load the sequence's targets and drafts into LDS together (one memory
+// latency instead of one per depth), and lane 0 walks, as the fused kernel does.
+constexpr int kWalkWaves = 4;
+constexpr int kWalkVals = kMaxDepth + 32 * (kMaxDepth - 1);  // gamma + 1 targets, K <= 32 paths of gamma drafts
+
+__global__ __launch_bounds__(64 * kWalkWaves) void topk_walk_kernel(TopkRaceArgs a) {
+    __shared__ int32_t vals[kWalkWaves][kWalkVals];
+    const int lane = (int)threadIdx.x & 63, wave = (int)threadIdx.x >> 6;
+    const int b = (int)blockIdx.x * kWalkWaves + wave;
     const int K = a.K, G = a.gamma;
-    if (b == 0) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
         const uint32_t bits = __hip_atomic_exchange(a.ctrl + kCtrlCallErrors, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (bits) __hip_atomic_fetch_or(a.ctrl + kCtrlErrors, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (a.status) *a.status = bits | (a.status_in ? *a.status_in : 0u);
     }
-    if (b >= a.B) return;
-    const int32_t* y = a.chain + (size_t)b * (G + 1);
-    const int32_t* d = a.draft_tokens + (size_t)b * K * G;
+    const bool valid = b < a.B;
+    int32_t* v = vals[wave];
+    const int nt = G + 1, n = nt + K * G;  // n <= kWalkVals (K and gamma are checked by the caller)
+    if (valid) {
+        const int32_t* y = a.chain + (size_t)b * nt;
+        const int32_t* d = a.draft_tokens + (size_t)b * K * G;
+        for (int e = lane; e < n; e += 64) v[e] = e < nt ? y[e] : d[e - nt];
+    }
+    __syncthreads();
+    if (!valid || lane != 0) return;
+    const int32_t* d = v + nt;
     uint32_t act = K >= 32 ? 0xFFFFFFFFu : ((1u << K) - 1u);
     int tau = 0;
     bool done = false;
     for (int s = 0; s < G && !done; ++s) {
-        const int ys = y[s];
+        const int ys = v[s];
         a.out_tokens[(size_t)b * (G + 1) + s] = ys;
         tau = s + 1;
         if (ys < 0) {
@@ -1130,7 +1144,7 @@ __global__ __launch_bounds__(256) void topk_walk_kernel(TopkRaceArgs a) {
         act = na;
     }
     if (!done) {
-        a.out_tokens[(size_t)b * (G + 1) + G] = y[G];
+        a.out_tokens[(size_t)b * (G + 1) + G] = v[G];
         tau = G + 1;
     }
     for (int s = tau; s <= G; ++s) a.out_tokens[(size_t)b * (G + 1) + s] = -1;
@@ -1140,7 +1154,7 @@ __global__ __launch_bounds__(256) void topk_walk_kernel(TopkRaceArgs a) {
 }  // namespace
 
 hipError_t launch_walk(const TopkRaceArgs& a, hipStream_t stream) {
-    hipLaunchKernelGGL(topk_walk_kernel, dim3((unsigned)((a.B + 255) / 256)), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(topk_walk_kernel, dim3((unsigned)((a.B + kWalkWaves - 1) / kWalkWaves)), dim3(64 * kWalkWaves), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -1168,7 +1182,7 @@ hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t strea
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
         if (a.target_rows == 1) {
-            hipLaunchKernelGGL(topk_walk_kernel, dim3((unsigned)((a.B + 255) / 256)), dim3(256), 0, stream, a);
+            hipLaunchKernelGGL(topk_walk_kernel, dim3((unsigned)((a.B + kWalkWaves - 1) / kWalkWaves)), dim3(64 * kWalkWaves), 0, stream, a);
             return hipGetLastError();
         }
         return launch_finish_status(a.ctrl, a.status, stream);
