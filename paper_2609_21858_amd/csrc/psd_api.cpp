@@ -209,6 +209,7 @@ psd::MpfrArgs mpfr_args(const psd_params* p, const psd_block* b, int32_t s_begin
     m.s_count = s_count;
     m.T = p->temp_draft;
     m.invT = 1.0f / p->temp_draft;
+    m.spin_limit = g_spin_limit.load(std::memory_order_relaxed);
     return m;
 }
 
@@ -219,8 +220,9 @@ bool mpfr_vec(const psd_params* p, const void* draft_logits) {
 
 // A depth's launch has one workgroup per (sequence, path), each streaming its row.
 // When those cannot fill the device (B K < 1024), every draft row of the call is
-// streamed first in one launch (group maxima, maxima, LSE) and the depth launches
-// only sample; otherwise each depth's streaming overlaps its contexts' sampling.
+// streamed first in one launch (group maxima, maxima, LSE) and the depths only sample
+// (in one launch when its workgroups fit the device together); otherwise each depth's
+// streaming overlaps its contexts' sampling.
 psd_status mpfr_stream_rows(const psd_params* p, const psd_block* b, psd::MpfrArgs& m, hipStream_t stream) {
     if ((long)b->batch * p->num_drafts >= 1024) return PSD_OK;
     const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
@@ -228,17 +230,15 @@ psd_status mpfr_stream_rows(const psd_params* p, const psd_block* b, psd::MpfrAr
     m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
     m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
     m.row_seed = (int32_t*)((unsigned char*)b->workspace + M.seed);
+    m.tok_slot = (uint64_t*)((unsigned char*)b->workspace + M.slot);  // every depth in one launch
     hipError_t e = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, mpfr_vec(p, m.logits), stream);
     if (e != hipSuccess) return hip_fail(e, "MPFR stream kernel launch");
     return PSD_OK;
 }
 
 psd_status mpfr_sample_depths(const psd_params* p, psd::MpfrArgs& m, hipStream_t stream) {
-    for (int s = m.s_begin; s < m.s_begin + m.s_count; ++s) {
-        m.s = s;
-        hipError_t e = psd::launch_mpfr_draft(m, p->dtype == PSD_BF16, mpfr_vec(p, m.logits), p->clocks, stream);
-        if (e != hipSuccess) return hip_fail(e, "MPFR draft kernel launch");
-    }
+    hipError_t e = psd::launch_mpfr_depths(m, p->dtype == PSD_BF16, mpfr_vec(p, m.logits), p->clocks, stream);
+    if (e != hipSuccess) return hip_fail(e, "MPFR draft kernel launch");
     return PSD_OK;
 }
 

@@ -10,6 +10,10 @@ namespace psd {
 // Control word that carries the race kernel's share of a call's error bits to a
 // later walk kernel of the same call (a word the race kernel uses for nothing else).
 constexpr int kCtrlRaceBits = 7;
+// Epoch of the last identical-drafter launch that ran every depth, and its workgroups
+// that have left (words of their own: the race kernel may run beside it).
+constexpr int kCtrlMpfrEpoch = 8;
+constexpr int kCtrlMpfrExited = 9;
 
 struct DetectArgs {
     const int32_t* tokens;  // [n_seq][row_stride], positions [0, seq_len) of each row scored
@@ -58,13 +62,16 @@ struct MpfrArgs {
     float* row_max;             // [B*K*gamma] their maxima (draft row ids), written by
                                 // the streaming launch and read by the sampling launches
     int32_t* row_seed;          // [B*K*gamma][8] their seed tokens (-1: none), likewise
+    uint64_t* tok_slot;         // nullable [B*K*gamma]: the drafts of a launch that runs every
+                                // depth, as (epoch << 32) | token, for the later depths' waits
+    uint32_t spin_limit;        // polls of a bounded wait before it gives up
 };
 
 // Identical drafters: the draft rows' group maxima and maxima, streamed once per call
 // ahead of the depth-by-depth sampling, after the race kernel's workspace, then the
 // shared target chain's tokens for a walk kernel that runs after the drafts.
 struct MpfrLayout {
-    size_t gm, rmax, seed, ytok, total;
+    size_t gm, rmax, seed, slot, ytok, total;
 };
 inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
     MpfrLayout M;
@@ -72,7 +79,8 @@ inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
     M.gm = L.total;
     M.rmax = align256(M.gm + rows * (size_t)L.ng * 4);
     M.seed = align256(M.rmax + rows * 4);
-    M.ytok = align256(M.seed + rows * 8 * 4);  // 8 seeds per row
+    M.slot = align256(M.seed + rows * 8 * 4);  // 8 seeds per row
+    M.ytok = align256(M.slot + rows * 8);      // one tagged draft per row
     M.total = align256(M.ytok + (size_t)B * (gamma + 1) * 4);  // shared-chain targets [B][gamma+1]
     return M;
 }
@@ -190,7 +198,11 @@ hipError_t launch_topk_race(const TopkRaceArgs& a, int layout, hipStream_t strea
 hipError_t launch_walk(const TopkRaceArgs& a, hipStream_t stream);
 
 hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
-hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout, hipStream_t stream);
+// The sampling of depths [s_begin, s_begin + s_count): one launch that runs every
+// depth when the drafts can be handed over in tagged slots (tok_slot set, more than
+// one depth) and every workgroup of it can be resident at once, else one launch per
+// depth.
+hipError_t launch_mpfr_depths(MpfrArgs a, bool bf16, bool vec, int layout, hipStream_t stream);
 hipError_t launch_mpfr_stream(const MpfrArgs& a, bool bf16, bool vec, hipStream_t stream);
 hipError_t launch_finish_status(uint32_t* ctrl, uint32_t* status, hipStream_t stream);
 hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream);

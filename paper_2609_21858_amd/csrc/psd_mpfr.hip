@@ -10,9 +10,12 @@
 // one context, whose proposal row is its lowest path's row, and the context's i-th
 // sample goes to its i-th path.
 //
-// One launch per depth, one workgroup per draft row (b, k).  Every workgroup
-// streams its row once (log-sum-exp, maxima of 128-token groups).  The workgroup
-// of a context's lowest path then samples the context:
+// One workgroup per draft row (b, k) of a depth.  Either every workgroup streams
+// its row once (log-sum-exp, maxima of 128-token groups), one launch per depth, or
+// a streaming launch has done so for every row of the call; then one launch can run
+// every depth, each workgroup going on to the next depth as soon as the drafts its
+// context depends on have landed.  The workgroup of a context's lowest path samples
+// the context:
 //  1. seeds: the largest token of the top group of each eighth of the row; their
 //     first nu arrivals, exact in fp64, give theta = the nu-th smallest of those
 //     scores, an upper bound on the context's nu-th smallest score;
@@ -75,6 +78,7 @@ struct MShared {
     uint32_t kappa0, kappa1;
     int samples[32];
     int pre[16];               // the sequence's context window before the block (m <= 16)
+    uint32_t epoch;            // this launch's tag of the handed-over drafts (multi-depth launch)
 };
 
 __device__ __forceinline__ float mload(const unsigned char* row, bool bf16, int v) {
@@ -360,11 +364,40 @@ __global__ __launch_bounds__(kMBlock) void mpfr_stream_kernel(MpfrArgs a) {
     if (threadIdx.x < kSeeds) a.row_seed[rid * kSeeds + threadIdx.x] = seed_tok[threadIdx.x];
 }
 
+// A launch that runs every depth hands each draft to the later depths' workgroups in
+// a tagged slot: relaxed device-scope atomics are coherent across the XCDs without
+// cache write-back, and the tag (the launch's epoch) tells a reader that the value
+// of this launch has landed.
+__device__ __forceinline__ void mst_dev(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t mld_dev(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t mld_dev_u32(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Bounded wait for the draft of row rid; on timeout the call's error bit 0 is set and
+// the token reads as -1.
+__device__ __forceinline__ int wait_draft(const MpfrArgs& a, size_t rid, uint32_t ep) {
+    uint64_t v = mld_dev(a.tok_slot + rid);
+    for (uint32_t i = 0; (uint32_t)(v >> 32) != ep; ++i) {
+        if (i >= a.spin_limit) {
+            __hip_atomic_fetch_or(a.ctrl + kCtrlCallErrors, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return -1;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        v = mld_dev(a.tok_slot + rid);
+    }
+    return (int)(uint32_t)v;
+}
+
+// Depth s of path k of sequence b (every thread of the workgroup calls it; its early
+// returns are uniform).  ep: the launch's epoch when it runs every depth.
 template <bool BF16, bool VEC, int LAYOUT>
-__global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
-    __shared__ MShared sm;
+__device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b, int k, int s, uint32_t ep) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int b = (int)blockIdx.x / a.K, k = (int)blockIdx.x % a.K, s = a.s;
     const uint32_t V = (uint32_t)a.V;
     const int ng = (a.V + 127) / 128, n3 = (ng + 15) / 16, n4 = (n3 + 15) / 16;
     const size_t esize = BF16 ? 2 : 4;
@@ -372,8 +405,11 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
                                (((size_t)b * a.K + k) * a.s_count + (size_t)(s - a.s_begin)) * (size_t)a.V * esize;
 
     // ---- the context of path k: the paths whose drafts at depths < s equal its own
-    for (int e = tid; e < a.K * s; e += kMBlock)
-        sm.path_tok[e] = a.draft_tokens[((size_t)b * a.K + e / s) * a.gamma + e % s];
+    // (depths of this launch: from their tagged slots, when one launch runs every depth)
+    for (int e = tid; e < a.K * s; e += kMBlock) {
+        const size_t rid = ((size_t)b * a.K + e / s) * a.gamma + e % s;
+        sm.path_tok[e] = a.tok_slot && e % s >= a.s_begin ? wait_draft(a, rid, ep) : a.draft_tokens[rid];
+    }
     for (int e = tid; e < a.m; e += kMBlock) sm.pre[e] = a.prefix[(size_t)b * a.m + e];
     if (tid == 0) sm.n_l4 = sm.n_l3 = sm.n_cand = 0;
     __syncthreads();
@@ -755,7 +791,41 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
         for (int r = 0; r < nu; ++r) {
             const int kk = __ffs((int)mm) - 1;
             mm &= mm - 1u;
-            a.draft_tokens[((size_t)b * a.K + kk) * a.gamma + s] = sm.samples[r];
+            const size_t rid = ((size_t)b * a.K + kk) * a.gamma + s;
+            a.draft_tokens[rid] = sm.samples[r];
+            if (a.tok_slot) mst_dev(a.tok_slot + rid, ((uint64_t)ep << 32) | (uint32_t)sm.samples[r]);
+        }
+    }
+}
+
+// One workgroup per (sequence, path).  Without tok_slot: depth a.s only.  With it:
+// every depth of the call in turn, each depth's contexts formed from the drafts of the
+// earlier depths as they land; waits are only for workgroups of the same launch, so
+// the launcher uses this form only when all of them can be resident together.  The
+// last workgroup to leave resets the exit count and records the launch's epoch.
+template <bool BF16, bool VEC, int LAYOUT>
+__global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
+    __shared__ MShared sm;
+    const int b = (int)blockIdx.x / a.K, k = (int)blockIdx.x % a.K;
+    if (!a.tok_slot) {
+        mpfr_depth<BF16, VEC, LAYOUT>(a, sm, b, k, a.s, 0u);
+        return;
+    }
+    if (threadIdx.x == 0) {
+        const uint32_t last = mld_dev_u32(a.ctrl + kCtrlMpfrEpoch);
+        sm.epoch = last == 0xFFFFFFFFu ? 1u : last + 1u;  // 1 .. 2^32-1
+    }
+    __syncthreads();
+    const uint32_t ep = sm.epoch;
+    for (int s = a.s_begin; s < a.s_begin + a.s_count; ++s) {
+        mpfr_depth<BF16, VEC, LAYOUT>(a, sm, b, k, s, ep);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(a.ctrl + kCtrlMpfrExited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == gridDim.x - 1) {
+            __hip_atomic_store(a.ctrl + kCtrlMpfrExited, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.ctrl + kCtrlMpfrEpoch, ep, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -770,26 +840,41 @@ __global__ void finish_status_kernel(uint32_t* ctrl, uint32_t* status) {
 
 }  // namespace
 
-hipError_t launch_mpfr_draft(const MpfrArgs& a, bool bf16, bool vec, int layout, hipStream_t stream) {
+namespace {
+
+template <bool BF16, bool VEC, int LAYOUT>
+hipError_t mpfr_depths(MpfrArgs a, hipStream_t stream) {
+    auto fn = mpfr_draft_kernel<BF16, VEC, LAYOUT>;
     const dim3 grid((unsigned)(a.B * a.K)), block(kMBlock);
-    if (bf16) {
-        if (vec) {
-            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<true, true, 0>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((mpfr_draft_kernel<true, true, 1>), grid, block, 0, stream, a);
-        } else {
-            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<true, false, 0>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((mpfr_draft_kernel<true, false, 1>), grid, block, 0, stream, a);
-        }
-    } else {
-        if (vec) {
-            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<false, true, 0>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((mpfr_draft_kernel<false, true, 1>), grid, block, 0, stream, a);
-        } else {
-            if (layout == 0) hipLaunchKernelGGL((mpfr_draft_kernel<false, false, 0>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((mpfr_draft_kernel<false, false, 1>), grid, block, 0, stream, a);
+    hipError_t e;
+    if (a.tok_slot && a.s_count > 1) {
+        int per_cu = 0, dev = 0, cus = 0;
+        if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kMBlock, 0)) != hipSuccess) return e;
+        if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+        if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+        if ((long)per_cu * cus >= (long)a.B * a.K) {
+            hipLaunchKernelGGL(fn, grid, block, 0, stream, a);
+            return hipGetLastError();
         }
     }
-    return hipGetLastError();
+    a.tok_slot = nullptr;
+    for (int s = a.s_begin; s < a.s_begin + a.s_count; ++s) {
+        a.s = s;
+        hipLaunchKernelGGL(fn, grid, block, 0, stream, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_mpfr_depths(MpfrArgs a, bool bf16, bool vec, int layout, hipStream_t stream) {
+    if (bf16) {
+        if (vec) return layout == 0 ? mpfr_depths<true, true, 0>(a, stream) : mpfr_depths<true, true, 1>(a, stream);
+        return layout == 0 ? mpfr_depths<true, false, 0>(a, stream) : mpfr_depths<true, false, 1>(a, stream);
+    }
+    if (vec) return layout == 0 ? mpfr_depths<false, true, 0>(a, stream) : mpfr_depths<false, true, 1>(a, stream);
+    return layout == 0 ? mpfr_depths<false, false, 0>(a, stream) : mpfr_depths<false, false, 1>(a, stream);
 }
 
 hipError_t launch_mpfr_stream(const MpfrArgs& a, bool bf16, bool vec, hipStream_t stream) {
