@@ -59,9 +59,10 @@ def run_mpfr(psd, w, seed, layout, target_rows=1, mode="fused", gen_device="cpu"
     else:
         dt = torch.full((w.B, w.K, w.gamma), -7, dtype=torch.int32, device=DEV)
         st_d = torch.full((1,), -1, dtype=torch.int32, device=DEV)
-        for s in range(w.gamma):
+        step = 2 if mode == "draft2" else 1  # two depths per call: one launch runs both
+        for s in range(0, w.gamma, step):
             psd.draft(params, ws, g["prefix_tokens"], g["start_pos"], w.gamma, s,
-                      g["draft_logits"][:, :, s:s + 1].contiguous(), dt, dl, status=st_d)
+                      g["draft_logits"][:, :, s:s + step].contiguous(), dt, dl, status=st_d)
             torch.cuda.synchronize()
             assert int(st_d[0]) == 0
         out = psd.verify(params, ws, g["prefix_tokens"], g["start_pos"], g["target_logits"], None, dt,
@@ -244,3 +245,13 @@ def test_mpfr_side_stream_follows_caller_stream(psd):
     assert int(status[0]) == 0 and psd.workspace_errors(ws) == 0
     for k in ("out_tokens", "out_len", "draft_tokens", "target_tokens"):
         assert torch.equal(got[k], ref[k]), k
+
+
+@pytest.mark.parametrize("cfg", [1, 3])
+def test_mpfr_draft_calls_of_two_depths(psd, cfg):
+    """psd_draft over two depths per call: the second call's launch takes the first
+    call's drafts from draft_tokens and its own first depth's drafts from the tagged
+    slots of the same launch.  Samples, tokens and lengths as the oracle's."""
+    w = workloads.WORKLOADS[cfg]
+    assert w.gamma % 2 == 0
+    run_mpfr(psd, w, 20 + cfg, 0, mode="draft2", gen_device=DEV, seqs=range(0, w.B, max(1, w.B // 8)))
