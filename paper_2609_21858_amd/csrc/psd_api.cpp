@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 
@@ -223,14 +224,34 @@ bool mpfr_vec(const psd_params* p, const void* draft_logits) {
 // streamed first in one launch (group maxima, maxima, LSE) and the depths only sample
 // (in one launch when its workgroups fit the device together); otherwise each depth's
 // streaming overlaps its contexts' sampling.
-psd_status mpfr_stream_rows(const psd_params* p, const psd_block* b, psd::MpfrArgs& m, hipStream_t stream) {
-    if ((long)b->batch * p->num_drafts >= 1024) return PSD_OK;
+// Sets the streamed rows' words and the form of the sampling (one launch for every
+// depth when it fits the device, else one per depth); *streamed tells whether the call
+// has a streaming launch.
+psd_status mpfr_prepare(const psd_params* p, const psd_block* b, psd::MpfrArgs& m, bool* streamed) {
+    *streamed = (long)b->batch * p->num_drafts < 1024;
+    if (!*streamed) return PSD_OK;
     const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
     const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);
-    m.row_gm = (float*)((unsigned char*)b->workspace + M.gm);
-    m.row_max = (float*)((unsigned char*)b->workspace + M.rmax);
-    m.row_seed = (int32_t*)((unsigned char*)b->workspace + M.seed);
-    m.tok_slot = (uint64_t*)((unsigned char*)b->workspace + M.slot);  // every depth in one launch
+    m.row_gm = (uint64_t*)((unsigned char*)b->workspace + M.gm);
+    m.row_max = (uint64_t*)((unsigned char*)b->workspace + M.rmax);
+    m.row_seed = (uint64_t*)((unsigned char*)b->workspace + M.seed);
+    bool fits = false;
+    hipError_t e = psd::mpfr_all_depths_fit(m, p->dtype == PSD_BF16, mpfr_vec(p, m.logits), p->clocks, &fits);
+    if (e != hipSuccess) return hip_fail(e, "MPFR occupancy query");
+    m.tok_slot = fits ? (uint64_t*)((unsigned char*)b->workspace + M.slot) : nullptr;
+    m.stream_records_epoch = fits ? 0 : 1;
+    // Beside a sampling launch that runs every depth, half as many streaming workgroups as
+    // rows (two rows each, depth-major) land the first depths' rows sooner (at least 512
+    // or every row): 178 vs 185 us per call with one per row at V=128256, K=4, gamma=4,
+    // B=64 (384: 191 us, 256: 209 us).
+    if (fits) {
+        const int rows = b->batch * p->num_drafts * m.s_count;
+        m.stream_grid = std::max((rows + 1) / 2, std::min(rows, 512));
+    }
+    return PSD_OK;
+}
+
+psd_status mpfr_stream_rows(const psd_params* p, psd::MpfrArgs& m, hipStream_t stream) {
     hipError_t e = psd::launch_mpfr_stream(m, p->dtype == PSD_BF16, mpfr_vec(p, m.logits), stream);
     if (e != hipSuccess) return hip_fail(e, "MPFR stream kernel launch");
     return PSD_OK;
@@ -245,7 +266,9 @@ psd_status mpfr_sample_depths(const psd_params* p, psd::MpfrArgs& m, hipStream_t
 psd_status run_mpfr_drafts(const psd_params* p, const psd_block* b, int32_t s_begin, int32_t s_count,
                            const void* draft_logits, int32_t* draft_tokens, float* draft_lse, hipStream_t stream) {
     psd::MpfrArgs m = mpfr_args(p, b, s_begin, s_count, draft_logits, draft_tokens, draft_lse);
-    psd_status st = mpfr_stream_rows(p, b, m, stream);
+    bool streamed = false;
+    psd_status st = mpfr_prepare(p, b, m, &streamed);
+    if (st == PSD_OK && streamed) st = mpfr_stream_rows(p, m, stream);
     if (st != PSD_OK) return st;
     return mpfr_sample_depths(p, m, stream);
 }
@@ -439,19 +462,38 @@ psd_status verify_mpfr_forked(const psd_params* params, const psd_block* block, 
     build_depths(a, block->gamma + 1);
     a.walk_kind = -1;  // no row walks: the walk kernel does, after the drafts
     a.status = ctrl + psd::kCtrlRaceBits;
-    // The streaming pass first: the race kernel, whose streaming workgroups would
-    // otherwise hold the device while it runs, then overlaps only the depth launches
-    // (236 vs 256 us per call at V=128256, K=4, gamma=4, B=64).
     psd::MpfrArgs m = mpfr_args(params, block, 0, block->gamma, draft_logits, draft_tokens, draft_lse);
-    psd_status st = mpfr_stream_rows(params, block, m, stream);
+    bool streamed = false;
+    psd_status st = mpfr_prepare(params, block, m, &streamed);
     if (st != PSD_OK) return st;
     hipError_t e;
-    if ((e = hipEventRecord(f.in, stream)) != hipSuccess) return hip_fail(e, "fork event record");
-    if ((e = hipStreamWaitEvent(f.side, f.in, 0)) != hipSuccess) return hip_fail(e, "fork event wait");
-    if ((st = run_race(params, a, f.side)) != PSD_OK) return st;
-    // from here on the join is always enqueued, so the caller's stream never runs
-    // ahead of the side stream's race
-    psd_status sd = mpfr_sample_depths(params, m, stream);
+    psd_status sd;
+    if (streamed && m.tok_slot) {
+        // One sampling launch for every depth on the caller's stream, which waits for
+        // the streamed rows' tagged words, beside the streaming launch and then the
+        // target race on the side stream (the streaming launch never waits, and both
+        // launches' workgroups fit the device together).  The streaming launch is
+        // enqueued first, so a sampling launch never waits for rows that will not come.
+        if ((e = hipEventRecord(f.in, stream)) != hipSuccess) return hip_fail(e, "fork event record");
+        if ((e = hipStreamWaitEvent(f.side, f.in, 0)) != hipSuccess) return hip_fail(e, "fork event wait");
+        if ((st = mpfr_stream_rows(params, m, f.side)) != PSD_OK) return st;
+        // from here on the join is always enqueued, so the caller's stream never runs
+        // ahead of the side stream
+        sd = mpfr_sample_depths(params, m, stream);
+        if (sd == PSD_OK) sd = run_race(params, a, f.side);
+    } else {
+        // The streaming pass (when there is one) first, on the caller's stream: the race
+        // kernel, whose streaming workgroups would otherwise hold the device while it
+        // runs, then overlaps only the depth launches (236 vs 256 us per call at
+        // V=128256, K=4, gamma=4, B=64 with one launch per depth).
+        if (streamed && (st = mpfr_stream_rows(params, m, stream)) != PSD_OK) return st;
+        if ((e = hipEventRecord(f.in, stream)) != hipSuccess) return hip_fail(e, "fork event record");
+        if ((e = hipStreamWaitEvent(f.side, f.in, 0)) != hipSuccess) return hip_fail(e, "fork event wait");
+        if ((st = run_race(params, a, f.side)) != PSD_OK) return st;
+        // from here on the join is always enqueued, so the caller's stream never runs
+        // ahead of the side stream's race
+        sd = mpfr_sample_depths(params, m, stream);
+    }
     if ((e = hipEventRecord(f.out, f.side)) != hipSuccess) return hip_fail(e, "join event record");
     if ((e = hipStreamWaitEvent(stream, f.out, 0)) != hipSuccess) return hip_fail(e, "join event wait");
     if (sd != PSD_OK) return sd;

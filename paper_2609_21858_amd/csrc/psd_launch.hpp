@@ -58,13 +58,19 @@ struct MpfrArgs {
     int V, K, m, B, gamma;
     int s_begin, s_count, s;    // depth of this launch: s_begin <= s < s_begin + s_count
     float T, invT;
-    float* row_gm;              // [B*K*gamma][groups] group maxima of the draft rows, and
-    float* row_max;             // [B*K*gamma] their maxima (draft row ids), written by
-                                // the streaming launch and read by the sampling launches
-    int32_t* row_seed;          // [B*K*gamma][8] their seed tokens (-1: none), likewise
+    // Written by the streaming launch and read by the sampling launches, each word
+    // (epoch << 32) | payload (draft row ids): a sampling launch that runs every depth
+    // may run beside the streaming launch and waits for the tags.
+    uint64_t* row_gm;           // [B*K*gamma][groups] group maxima of the draft rows (float bits)
+    uint64_t* row_max;          // [B*K*gamma] their maxima (float bits)
+    uint64_t* row_seed;         // [B*K*gamma][8] their seed tokens (-1: none)
     uint64_t* tok_slot;         // nullable [B*K*gamma]: the drafts of a launch that runs every
                                 // depth, as (epoch << 32) | token, for the later depths' waits
     uint32_t spin_limit;        // polls of a bounded wait before it gives up
+    int stream_records_epoch;   // the streaming launch records its epoch (no sampling launch
+                                // that runs every depth follows it to do so)
+    int stream_grid;            // workgroups of the streaming launch (0: one per row); each
+                                // streams rows blockIdx.x, blockIdx.x + grid, ... (depth-major)
 };
 
 // Identical drafters: the draft rows' group maxima and maxima, streamed once per call
@@ -77,9 +83,9 @@ inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
     MpfrLayout M;
     const size_t rows = (size_t)B * K * gamma;
     M.gm = L.total;
-    M.rmax = align256(M.gm + rows * (size_t)L.ng * 4);
-    M.seed = align256(M.rmax + rows * 4);
-    M.slot = align256(M.seed + rows * 8 * 4);  // 8 seeds per row
+    M.rmax = align256(M.gm + rows * (size_t)L.ng * 8);
+    M.seed = align256(M.rmax + rows * 8);
+    M.slot = align256(M.seed + rows * 8 * 8);  // 8 seeds per row
     M.ytok = align256(M.slot + rows * 8);      // one tagged draft per row
     M.total = align256(M.ytok + (size_t)B * (gamma + 1) * 4);  // shared-chain targets [B][gamma+1]
     return M;
@@ -203,6 +209,9 @@ hipError_t launch_race(const RaceArgs& a, bool bf16, bool vec, int layout, hipSt
 // one depth) and every workgroup of it can be resident at once, else one launch per
 // depth.
 hipError_t launch_mpfr_depths(MpfrArgs a, bool bf16, bool vec, int layout, hipStream_t stream);
+// Whether one sampling launch can run every depth of a: more than one depth, and all
+// B K workgroups resident together.  *fits is set; a HIP error of the query is returned.
+hipError_t mpfr_all_depths_fit(const MpfrArgs& a, bool bf16, bool vec, int layout, bool* fits);
 hipError_t launch_mpfr_stream(const MpfrArgs& a, bool bf16, bool vec, hipStream_t stream);
 hipError_t launch_finish_status(uint32_t* ctrl, uint32_t* status, hipStream_t stream);
 hipError_t launch_detect(const DetectArgs& a, int layout, hipStream_t stream);

@@ -338,36 +338,10 @@ __device__ __forceinline__ void seed_tokens(const unsigned char* row, int V, con
     }
 }
 
-// The streaming launch of a call: one workgroup per draft row of depths
-// [s_begin, s_begin + s_count), writing its group maxima, maximum and LSE.
-template <bool BF16, bool VEC>
-__global__ __launch_bounds__(kMBlock) void mpfr_stream_kernel(MpfrArgs a) {
-    __shared__ float red_m[kMBlock / 64], red_s[kMBlock / 64], red_x[kMBlock / 64], rowmax;
-    __shared__ float gm[kMaxGroups];
-    __shared__ int seed_g[kSeeds], seed_tok[kSeeds];
-    const int r = (int)blockIdx.x;
-    const int b = r / (a.K * a.s_count), k = (r / a.s_count) % a.K, s = a.s_begin + r % a.s_count;
-    const int ng = (a.V + 127) / 128;
-    const size_t esize = BF16 ? 2 : 4;
-    const unsigned char* row = (const unsigned char*)a.logits + (size_t)r * (size_t)a.V * esize;
-    const size_t rid = ((size_t)b * a.K + k) * a.gamma + s;
-    const float xm = mstream_row<BF16, VEC>(row, a.V, a.invT, gm, a.draft_lse ? a.draft_lse + rid : nullptr, red_m,
-                                            red_s, red_x, &rowmax);
-    // (mstream_row ends with a barrier: the group maxima are in LDS)
-    for (int g = threadIdx.x; g < ng; g += kMBlock) a.row_gm[rid * ng + g] = gm[g];
-    if (threadIdx.x == 0) a.row_max[rid] = xm;
-    // the row's seed tokens, for every context this row may serve
-    seed_groups(gm, ng, seed_g);
-    __syncthreads();
-    seed_tokens<BF16, VEC>(row, a.V, gm, seed_g, seed_tok);
-    __syncthreads();
-    if (threadIdx.x < kSeeds) a.row_seed[rid * kSeeds + threadIdx.x] = seed_tok[threadIdx.x];
-}
-
-// A launch that runs every depth hands each draft to the later depths' workgroups in
-// a tagged slot: relaxed device-scope atomics are coherent across the XCDs without
-// cache write-back, and the tag (the launch's epoch) tells a reader that the value
-// of this launch has landed.
+// Values that may be read while their launch still runs (the streamed rows' maxima and
+// seeds, the drafts of a launch that runs every depth) are tagged words: relaxed
+// device-scope atomics are coherent across the XCDs without cache write-back, and
+// the tag (the call's epoch) tells a reader that this call's value has landed.
 __device__ __forceinline__ void mst_dev(uint64_t* p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -376,6 +350,61 @@ __device__ __forceinline__ uint64_t mld_dev(const uint64_t* p) {
 }
 __device__ __forceinline__ uint32_t mld_dev_u32(const uint32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The call's epoch for its tagged words: one more than the last recorded (1 .. 2^32-1).
+__device__ __forceinline__ uint32_t next_epoch(const MpfrArgs& a) {
+    const uint32_t last = mld_dev_u32(a.ctrl + kCtrlMpfrEpoch);
+    return last == 0xFFFFFFFFu ? 1u : last + 1u;
+}
+
+// The last workgroup of a launch to leave resets the exit count and records the epoch.
+__device__ __forceinline__ void record_epoch(const MpfrArgs& a, uint32_t ep) {
+    const uint32_t old = __hip_atomic_fetch_add(a.ctrl + kCtrlMpfrExited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == gridDim.x - 1) {
+        __hip_atomic_store(a.ctrl + kCtrlMpfrExited, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(a.ctrl + kCtrlMpfrEpoch, ep, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// The streaming launch of a call over the draft rows of depths [s_begin, s_begin +
+// s_count), depth-major (the first depth's rows are handed out first), one row per
+// workgroup or (stream_grid) several, writing each row's group maxima, maximum and
+// seed tokens as tagged words and its LSE.  It never waits.
+template <bool BF16, bool VEC>
+__global__ __launch_bounds__(kMBlock) void mpfr_stream_kernel(MpfrArgs a) {
+    __shared__ float red_m[kMBlock / 64], red_s[kMBlock / 64], red_x[kMBlock / 64], rowmax;
+    __shared__ float gm[kMaxGroups];
+    __shared__ int seed_g[kSeeds], seed_tok[kSeeds];
+    __shared__ uint32_t ep_s;
+    const int n = a.B * a.K;
+    const int row_end = n * a.s_count;
+    const int ng = (a.V + 127) / 128;
+    const size_t esize = BF16 ? 2 : 4;
+    if (threadIdx.x == 0) ep_s = next_epoch(a);
+    // rows blockIdx.x, blockIdx.x + gridDim.x, ...: with fewer workgroups than rows, the
+    // first depths' rows land first
+    for (int r = (int)blockIdx.x; r < row_end; r += (int)gridDim.x) {
+        const int s = a.s_begin + r / n, b = (r % n) / a.K, k = r % a.K;
+        const unsigned char* row = (const unsigned char*)a.logits +
+                                   (((size_t)b * a.K + k) * a.s_count + (size_t)(s - a.s_begin)) * (size_t)a.V * esize;
+        const size_t rid = ((size_t)b * a.K + k) * a.gamma + s;
+        const float xm = mstream_row<BF16, VEC>(row, a.V, a.invT, gm, a.draft_lse ? a.draft_lse + rid : nullptr,
+                                                red_m, red_s, red_x, &rowmax);
+        // (mstream_row ends with a barrier: the group maxima and the epoch are in LDS)
+        const uint64_t tag = (uint64_t)ep_s << 32;
+        for (int g = threadIdx.x; g < ng; g += kMBlock) mst_dev(a.row_gm + rid * ng + g, tag | __float_as_uint(gm[g]));
+        if (threadIdx.x == 0) mst_dev(a.row_max + rid, tag | __float_as_uint(xm));
+        // the row's seed tokens, for every context this row may serve
+        seed_groups(gm, ng, seed_g);
+        __syncthreads();
+        seed_tokens<BF16, VEC>(row, a.V, gm, seed_g, seed_tok);
+        __syncthreads();
+        if (threadIdx.x < kSeeds)
+            mst_dev(a.row_seed + rid * kSeeds + threadIdx.x, tag | (uint32_t)seed_tok[threadIdx.x]);
+        __syncthreads();  // gm and the seeds are reused by the next row
+    }
+    if (a.stream_records_epoch && threadIdx.x == 0) record_epoch(a, ep_s);
 }
 
 // Bounded wait for the draft of row rid; on timeout the call's error bit 0 is set and
@@ -391,6 +420,23 @@ __device__ __forceinline__ int wait_draft(const MpfrArgs& a, size_t rid, uint32_
         v = mld_dev(a.tok_slot + rid);
     }
     return (int)(uint32_t)v;
+}
+
+// Payload of a word the streaming launch wrote.  A launch that runs every depth may
+// run beside the streaming launch: it waits (bounded) for this call's tag.  Launches of
+// one depth follow the streaming launch in stream order and read the payload.
+__device__ __forceinline__ uint32_t row_word(const MpfrArgs& a, const uint64_t* p, uint32_t ep) {
+    if (!a.tok_slot) return (uint32_t)*p;
+    uint64_t v = mld_dev(p);
+    for (uint32_t i = 0; (uint32_t)(v >> 32) != ep; ++i) {
+        if (i >= a.spin_limit) {
+            __hip_atomic_fetch_or(a.ctrl + kCtrlCallErrors, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        v = mld_dev(p);
+    }
+    return (uint32_t)v;
 }
 
 // Depth s of path k of sequence b (every thread of the workgroup calls it; its early
@@ -426,10 +472,27 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
         __syncthreads();
         if (k != __ffs((int)sm.mask) - 1) return;  // uniform
         const size_t rid = ((size_t)b * a.K + k) * a.gamma + s;
-        for (int g = tid; g < ng; g += kMBlock) sm.gm[g] = a.row_gm[rid * ng + g];
-        if (tid == 0) sm.rowmax = a.row_max[rid];
+        // four loads in flight per thread, then a wait only for words not yet tagged
+        for (int g0 = tid; g0 < ng; g0 += 4 * kMBlock) {
+            uint64_t w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int g = g0 + i * kMBlock;
+                w[i] = g < ng ? (a.tok_slot ? mld_dev(a.row_gm + rid * ng + g) : a.row_gm[rid * ng + g]) : 0;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int g = g0 + i * kMBlock;
+                if (g < ng) {
+                    const uint32_t x = a.tok_slot && (uint32_t)(w[i] >> 32) != ep ? row_word(a, a.row_gm + rid * ng + g, ep)
+                                                                                   : (uint32_t)w[i];
+                    sm.gm[g] = __uint_as_float(x);
+                }
+            }
+        }
+        if (tid == 0) sm.rowmax = __uint_as_float(row_word(a, a.row_max + rid, ep));
         if (tid < kSeeds) {
-            const int tk = a.row_seed[rid * kSeeds + tid];
+            const int tk = (int)row_word(a, a.row_seed + rid * kSeeds + tid, ep);
             sm.seed_tok[tid] = tk;
             sm.seed_g[tid] = tk >= 0 ? tk / 128 : -1;
         }
@@ -811,23 +874,14 @@ __global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
         mpfr_depth<BF16, VEC, LAYOUT>(a, sm, b, k, a.s, 0u);
         return;
     }
-    if (threadIdx.x == 0) {
-        const uint32_t last = mld_dev_u32(a.ctrl + kCtrlMpfrEpoch);
-        sm.epoch = last == 0xFFFFFFFFu ? 1u : last + 1u;  // 1 .. 2^32-1
-    }
+    if (threadIdx.x == 0) sm.epoch = next_epoch(a);
     __syncthreads();
     const uint32_t ep = sm.epoch;
     for (int s = a.s_begin; s < a.s_begin + a.s_count; ++s) {
         mpfr_depth<BF16, VEC, LAYOUT>(a, sm, b, k, s, ep);
         __syncthreads();
     }
-    if (threadIdx.x == 0) {
-        const uint32_t old = __hip_atomic_fetch_add(a.ctrl + kCtrlMpfrExited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (old == gridDim.x - 1) {
-            __hip_atomic_store(a.ctrl + kCtrlMpfrExited, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(a.ctrl + kCtrlMpfrEpoch, ep, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
+    if (threadIdx.x == 0) record_epoch(a, ep);
 }
 
 // The call's error bits to the sticky word and the caller's status word (for calls
@@ -843,21 +897,31 @@ __global__ void finish_status_kernel(uint32_t* ctrl, uint32_t* status) {
 namespace {
 
 template <bool BF16, bool VEC, int LAYOUT>
+hipError_t mpfr_fit(const MpfrArgs& a, bool* fits) {
+    *fits = false;
+    if (!a.row_gm || a.s_count < 2) return hipSuccess;
+    int per_cu = 0, dev = 0, cus = 0;
+    hipError_t e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, mpfr_draft_kernel<BF16, VEC, LAYOUT>, kMBlock, 0)) !=
+        hipSuccess)
+        return e;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    *fits = (long)per_cu * cus >= (long)a.B * a.K;
+    return hipSuccess;
+}
+
+// tok_slot set (the caller checked mpfr_all_depths_fit): one launch for every depth;
+// otherwise one launch per depth.
+template <bool BF16, bool VEC, int LAYOUT>
 hipError_t mpfr_depths(MpfrArgs a, hipStream_t stream) {
     auto fn = mpfr_draft_kernel<BF16, VEC, LAYOUT>;
     const dim3 grid((unsigned)(a.B * a.K)), block(kMBlock);
     hipError_t e;
-    if (a.tok_slot && a.s_count > 1) {
-        int per_cu = 0, dev = 0, cus = 0;
-        if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kMBlock, 0)) != hipSuccess) return e;
-        if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-        if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-        if ((long)per_cu * cus >= (long)a.B * a.K) {
-            hipLaunchKernelGGL(fn, grid, block, 0, stream, a);
-            return hipGetLastError();
-        }
+    if (a.tok_slot) {
+        hipLaunchKernelGGL(fn, grid, block, 0, stream, a);
+        return hipGetLastError();
     }
-    a.tok_slot = nullptr;
     for (int s = a.s_begin; s < a.s_begin + a.s_count; ++s) {
         a.s = s;
         hipLaunchKernelGGL(fn, grid, block, 0, stream, a);
@@ -867,6 +931,15 @@ hipError_t mpfr_depths(MpfrArgs a, hipStream_t stream) {
 }
 
 }  // namespace
+
+hipError_t mpfr_all_depths_fit(const MpfrArgs& a, bool bf16, bool vec, int layout, bool* fits) {
+    if (bf16) {
+        if (vec) return layout == 0 ? mpfr_fit<true, true, 0>(a, fits) : mpfr_fit<true, true, 1>(a, fits);
+        return layout == 0 ? mpfr_fit<true, false, 0>(a, fits) : mpfr_fit<true, false, 1>(a, fits);
+    }
+    if (vec) return layout == 0 ? mpfr_fit<false, true, 0>(a, fits) : mpfr_fit<false, true, 1>(a, fits);
+    return layout == 0 ? mpfr_fit<false, false, 0>(a, fits) : mpfr_fit<false, false, 1>(a, fits);
+}
 
 hipError_t launch_mpfr_depths(MpfrArgs a, bool bf16, bool vec, int layout, hipStream_t stream) {
     if (bf16) {
@@ -878,7 +951,8 @@ hipError_t launch_mpfr_depths(MpfrArgs a, bool bf16, bool vec, int layout, hipSt
 }
 
 hipError_t launch_mpfr_stream(const MpfrArgs& a, bool bf16, bool vec, hipStream_t stream) {
-    const dim3 grid((unsigned)(a.B * a.K * a.s_count)), block(kMBlock);
+    const int rows = a.B * a.K * a.s_count;
+    const dim3 grid((unsigned)(a.stream_grid > 0 && a.stream_grid < rows ? a.stream_grid : rows)), block(kMBlock);
     if (bf16) {
         if (vec) hipLaunchKernelGGL((mpfr_stream_kernel<true, true>), grid, block, 0, stream, a);
         else hipLaunchKernelGGL((mpfr_stream_kernel<true, false>), grid, block, 0, stream, a);
