@@ -255,3 +255,35 @@ def test_mpfr_draft_calls_of_two_depths(psd, cfg):
     w = workloads.WORKLOADS[cfg]
     assert w.gamma % 2 == 0
     run_mpfr(psd, w, 20 + cfg, 0, mode="draft2", gen_device=DEV, seqs=range(0, w.B, max(1, w.B // 8)))
+
+
+def test_mpfr_epoch_across_sampling_forms(psd):
+    """Two block shapes share one workspace: B K = 600, more workgroups than fit the
+    device together at this kernel's occupancy (512 on MI355X), so one sampling launch
+    per depth follows a streaming launch that records the call's epoch; and B K = 96,
+    where one sampling launch runs every depth beside the streaming launch and waits
+    for its tagged words.  The shapes' tagged words sit at different offsets, so a stale
+    tag would show up as a wrong draft.  Alternating the two, every call equals the same
+    call on a fresh workspace, which matches the oracle."""
+    wa = workloads.custom(2048, 6, 4, 100, dtype="bf16", T_target=0.8, T_draft=0.8)
+    wb = workloads.custom(2048, 6, 4, 16, dtype="bf16", T_target=0.8, T_draft=0.8)
+    blk_a = workloads.make_block(wa, 31, device=DEV)
+    blk_b = workloads.make_block(wb, 32, device=DEV)
+    ref_a, _ = run_mpfr(psd, wa, 31, 0, blk=blk_a, seqs=range(0, wa.B, 25))
+    ref_b, _ = run_mpfr(psd, wb, 32, 0, blk=blk_b, seqs=range(0, wb.B, 4))
+    pa = psd.make_params(wa.key, wa.V, wa.K, wa.m, wa.T_target, wa.T_draft, dtype=wa.torch_dtype,
+                         mode=psd.PSD_MODE_MPFR)
+    pb = psd.make_params(wb.key, wb.V, wb.K, wb.m, wb.T_target, wb.T_draft, dtype=wb.torch_dtype,
+                         mode=psd.PSD_MODE_MPFR)
+    n = max(psd.workspace_bytes(pa, wa.B, wa.gamma), psd.workspace_bytes(pb, wb.B, wb.gamma))
+    ws = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    status = torch.full((1,), -1, dtype=torch.int32, device=DEV)
+    for rep in range(3):
+        for name, p, blk, ref in (("B=100", pa, blk_a, ref_a), ("B=16", pb, blk_b, ref_b)):
+            print(f"[mpfr] shared workspace, round {rep}, {name}", flush=True)
+            out = psd.verify(p, ws, blk["prefix_tokens"], blk["start_pos"], blk["target_logits"],
+                             blk["draft_logits"], want_targets=True, status=status)
+            torch.cuda.synchronize()
+            assert int(status[0]) == 0 and psd.workspace_errors(ws) == 0
+            for k in ("out_tokens", "out_len", "draft_tokens", "target_tokens"):
+                assert torch.equal(out[k], ref[k]), (rep, name, k)
