@@ -240,14 +240,6 @@ psd_status mpfr_prepare(const psd_params* p, const psd_block* b, psd::MpfrArgs& 
     if (e != hipSuccess) return hip_fail(e, "MPFR occupancy query");
     m.tok_slot = fits ? (uint64_t*)((unsigned char*)b->workspace + M.slot) : nullptr;
     m.stream_records_epoch = fits ? 0 : 1;
-    // Beside a sampling launch that runs every depth, half as many streaming workgroups as
-    // rows (two rows each, depth-major) land the first depths' rows sooner (at least 512
-    // or every row): 178 vs 185 us per call with one per row at V=128256, K=4, gamma=4,
-    // B=64 (384: 191 us, 256: 209 us).
-    if (fits) {
-        const int rows = b->batch * p->num_drafts * m.s_count;
-        m.stream_grid = std::max((rows + 1) / 2, std::min(rows, 512));
-    }
     return PSD_OK;
 }
 
@@ -474,6 +466,11 @@ psd_status verify_mpfr_forked(const psd_params* params, const psd_block* block, 
         // target race on the side stream (the streaming launch never waits, and both
         // launches' workgroups fit the device together).  The streaming launch is
         // enqueued first, so a sampling launch never waits for rows that will not come.
+        // Half as many streaming workgroups as rows (two rows each, depth-major; at least
+        // 512 or every row) land the first depths' rows sooner: 178 vs 185 us per call
+        // with one per row at V=128256, K=4, gamma=4, B=64 (384: 191 us, 256: 209 us).
+        const int rows = m.B * m.K * m.s_count;
+        m.stream_grid = std::max((rows + 1) / 2, std::min(rows, 512));
         if ((e = hipEventRecord(f.in, stream)) != hipSuccess) return hip_fail(e, "fork event record");
         if ((e = hipStreamWaitEvent(f.side, f.in, 0)) != hipSuccess) return hip_fail(e, "fork event wait");
         if ((st = mpfr_stream_rows(params, m, f.side)) != PSD_OK) return st;
