@@ -54,10 +54,8 @@ struct MNode {
 };
 
 struct MShared {
-    float gm[kMaxGroups];      // group maxima of the row
     float m3[256];             // 2048-token block maxima
     float m4[16];              // 32768-token node maxima
-    int path_tok[32 * 32];     // draft tokens of the K paths at depths < s ([path][depth])
     int seed_g[kSeeds];
     int seed_tok[kSeeds];
     double pair[kSeeds * 32];  // seed arrival scores (shifted frame)
@@ -67,7 +65,11 @@ struct MShared {
     int cand_v[kMCand];
     float cand_x[kMCand];
     int cand_j[kMCand];
-    double cand_g[kMCand];
+    union {
+        int path_tok[32 * 32];  // draft tokens of the K paths at depths < s ([path][depth]):
+                                // read up to the context key only
+        double cand_g[kMCand];  // the listed tokens' cumulative clocks (arrival phase)
+    };
     double cand_s[kMCand];
     float red_m[kMBlock / 64], red_s[kMBlock / 64], red_x[kMBlock / 64];
     double red_d[kMBlock / 64];
@@ -442,7 +444,7 @@ __device__ __forceinline__ uint32_t row_word(const MpfrArgs& a, const uint64_t* 
 // Depth s of path k of sequence b (every thread of the workgroup calls it; its early
 // returns are uniform).  ep: the launch's epoch when it runs every depth.
 template <bool BF16, bool VEC, int LAYOUT>
-__device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b, int k, int s, uint32_t ep) {
+__device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, float* gm, int b, int k, int s, uint32_t ep) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t V = (uint32_t)a.V;
     const int ng = (a.V + 127) / 128, n3 = (ng + 15) / 16, n4 = (n3 + 15) / 16;
@@ -486,7 +488,7 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
                 if (g < ng) {
                     const uint32_t x = a.tok_slot && (uint32_t)(w[i] >> 32) != ep ? row_word(a, a.row_gm + rid * ng + g, ep)
                                                                                    : (uint32_t)w[i];
-                    sm.gm[g] = __uint_as_float(x);
+                    gm[g] = __uint_as_float(x);
                 }
             }
         }
@@ -499,7 +501,7 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
     } else {
         // ---- stream the row: log-sum-exp, group maxima, row maximum
         __syncthreads();
-        mstream_row<BF16, VEC>(row, a.V, a.invT, sm.gm,
+        mstream_row<BF16, VEC>(row, a.V, a.invT, gm,
                                a.draft_lse ? a.draft_lse + ((size_t)b * a.K + k) * a.gamma + s : nullptr, sm.red_m,
                                sm.red_s, sm.red_x, &sm.rowmax);
     }
@@ -526,17 +528,17 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
         }
         for (int t = tid; t < n3; t += kMBlock) {
             float mx = -INFINITY;
-            for (int g = 16 * t; g < min(ng, 16 * t + 16); ++g) mx = fmaxf(mx, sm.gm[g]);
+            for (int g = 16 * t; g < min(ng, 16 * t + 16); ++g) mx = fmaxf(mx, gm[g]);
             sm.m3[t] = mx;
         }
-        if (!a.row_seed) seed_groups(sm.gm, ng, sm.seed_g);
+        if (!a.row_seed) seed_groups(gm, ng, sm.seed_g);
         __syncthreads();
         for (int t = tid; t < n4; t += kMBlock) {
             float mx = -INFINITY;
             for (int i = 16 * t; i < min(n3, 16 * t + 16); ++i) mx = fmaxf(mx, sm.m3[i]);
             sm.m4[t] = mx;
         }
-        if (!a.row_seed) seed_tokens<BF16, VEC>(row, a.V, sm.gm, sm.seed_g, sm.seed_tok);
+        if (!a.row_seed) seed_tokens<BF16, VEC>(row, a.V, gm, sm.seed_g, sm.seed_tok);
         __syncthreads();
         const uint32_t k0 = sm.kappa0, k1 = sm.kappa1;
         // seed arrivals in float32: E_j for every (seed, j < nu), the cumulative sums in
@@ -562,7 +564,7 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
             const int i = tid >> 5, j = tid & 31, v = sm.seed_tok[i];
             static_assert(kSeeds * 32 == kMBlock, "one seed arrival slot per thread");
             sm.pair[tid] = v >= 0 && j < nu
-                               ? (double)(ln_f32((float)sm.pair[tid]) - (sm.gm[sm.seed_g[i]] - shift) * a.invT)
+                               ? (double)(ln_f32((float)sm.pair[tid]) - (gm[sm.seed_g[i]] - shift) * a.invT)
                                : INFINITY;
         }
         __syncthreads();
@@ -636,11 +638,11 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
                     if (e < nl3 * 16) {
                         const MNode pa = sm.l3[e >> 4];
                         const uint32_t g = pa.i * 16u + (uint32_t)(e & 15);
-                        if ((int)g < ng && ln_f32(pa.m) - (sm.gm[g] - shift) * a.invT <= sm.theta) {
+                        if ((int)g < ng && ln_f32(pa.m) - (gm[g] - shift) * a.invT <= sm.theta) {
                             float m;
                             uint32_t p;
                             child_min_f32(pa.m, pa.p, 2, g, g << kShift2, node_end(kShift2, g, V), 0u, k0, k1, m, p);
-                            if (ln_f32(m) - (sm.gm[g] - shift) * a.invT <= sm.theta)
+                            if (ln_f32(m) - (gm[g] - shift) * a.invT <= sm.theta)
                                 sm.lg[atomicAdd(&sm.n_lg, 1)] = MNode{g, m, p};
                         }
                     }
@@ -661,7 +663,7 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
             } else {
                 for (int g0 = 0; g0 < ng; g0 += 16) {
                     const int g = g0 + (tid >> 4);
-                    if (g < ng && kLnClockFloor - (sm.gm[g] - shift) * a.invT <= sm.theta) {
+                    if (g < ng && kLnClockFloor - (gm[g] - shift) * a.invT <= sm.theta) {
                         const uint32_t chunk = (uint32_t)g * 16u + (uint32_t)(tid & 15);
                         float x[8];
                         mload8<BF16, VEC>(row, a.V, (int)(chunk * 8u), x);
@@ -867,18 +869,19 @@ __device__ __forceinline__ void mpfr_depth(const MpfrArgs& a, MShared& sm, int b
 // the launcher uses this form only when all of them can be resident together.  The
 // last workgroup to leave resets the exit count and records the launch's epoch.
 template <bool BF16, bool VEC, int LAYOUT>
-__global__ __launch_bounds__(kMBlock) void mpfr_draft_kernel(MpfrArgs a) {
+__global__ __launch_bounds__(kMBlock, 3) void mpfr_draft_kernel(MpfrArgs a) {
     __shared__ MShared sm;
+    extern __shared__ __align__(16) float gm[];  // the row's group maxima (dynamic: one per group)
     const int b = (int)blockIdx.x / a.K, k = (int)blockIdx.x % a.K;
     if (!a.tok_slot) {
-        mpfr_depth<BF16, VEC, LAYOUT>(a, sm, b, k, a.s, 0u);
+        mpfr_depth<BF16, VEC, LAYOUT>(a, sm, gm, b, k, a.s, 0u);
         return;
     }
     if (threadIdx.x == 0) sm.epoch = next_epoch(a);
     __syncthreads();
     const uint32_t ep = sm.epoch;
     for (int s = a.s_begin; s < a.s_begin + a.s_count; ++s) {
-        mpfr_depth<BF16, VEC, LAYOUT>(a, sm, b, k, s, ep);
+        mpfr_depth<BF16, VEC, LAYOUT>(a, sm, gm, b, k, s, ep);
         __syncthreads();
     }
     if (threadIdx.x == 0) record_epoch(a, ep);
@@ -896,14 +899,17 @@ __global__ void finish_status_kernel(uint32_t* ctrl, uint32_t* status) {
 
 namespace {
 
+// Dynamic LDS of a sampling launch: the row's group maxima.
+size_t mpfr_draft_smem(const MpfrArgs& a) { return (size_t)(((a.V + 127) / 128 + 3) & ~3) * sizeof(float); }
+
 template <bool BF16, bool VEC, int LAYOUT>
 hipError_t mpfr_fit(const MpfrArgs& a, bool* fits) {
     *fits = false;
     if (!a.row_gm || a.s_count < 2) return hipSuccess;
     int per_cu = 0, dev = 0, cus = 0;
     hipError_t e;
-    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, mpfr_draft_kernel<BF16, VEC, LAYOUT>, kMBlock, 0)) !=
-        hipSuccess)
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, mpfr_draft_kernel<BF16, VEC, LAYOUT>, kMBlock,
+                                                          mpfr_draft_smem(a))) != hipSuccess)
         return e;
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
@@ -917,14 +923,15 @@ template <bool BF16, bool VEC, int LAYOUT>
 hipError_t mpfr_depths(MpfrArgs a, hipStream_t stream) {
     auto fn = mpfr_draft_kernel<BF16, VEC, LAYOUT>;
     const dim3 grid((unsigned)(a.B * a.K)), block(kMBlock);
+    const size_t smem = mpfr_draft_smem(a);
     hipError_t e;
     if (a.tok_slot) {
-        hipLaunchKernelGGL(fn, grid, block, 0, stream, a);
+        hipLaunchKernelGGL(fn, grid, block, smem, stream, a);
         return hipGetLastError();
     }
     for (int s = a.s_begin; s < a.s_begin + a.s_count; ++s) {
         a.s = s;
-        hipLaunchKernelGGL(fn, grid, block, 0, stream, a);
+        hipLaunchKernelGGL(fn, grid, block, smem, stream, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;

@@ -258,15 +258,16 @@ def test_mpfr_draft_calls_of_two_depths(psd, cfg):
 
 
 def test_mpfr_epoch_across_sampling_forms(psd):
-    """Two block shapes share one workspace: B K = 600, more workgroups than fit the
-    device together at this kernel's occupancy (512 on MI355X), so one sampling launch
-    per depth follows a streaming launch that records the call's epoch; and B K = 96,
+    """Two block shapes share one workspace: B K = 1000, more workgroups than fit the
+    device together at this kernel's occupancy (768 on MI355X) but still under the
+    streaming launch's limit, so one sampling launch per depth follows a streaming
+    launch that records the call's epoch; and B K = 128,
     where one sampling launch runs every depth beside the streaming launch and waits
     for its tagged words.  The shapes' tagged words sit at different offsets, so a stale
     tag would show up as a wrong draft.  Alternating the two, every call equals the same
     call on a fresh workspace, which matches the oracle."""
-    wa = workloads.custom(2048, 6, 4, 100, dtype="bf16", T_target=0.8, T_draft=0.8)
-    wb = workloads.custom(2048, 6, 4, 16, dtype="bf16", T_target=0.8, T_draft=0.8)
+    wa = workloads.custom(2048, 8, 4, 125, dtype="bf16", T_target=0.8, T_draft=0.8)
+    wb = workloads.custom(2048, 8, 4, 16, dtype="bf16", T_target=0.8, T_draft=0.8)
     blk_a = workloads.make_block(wa, 31, device=DEV)
     blk_b = workloads.make_block(wb, 32, device=DEV)
     ref_a, _ = run_mpfr(psd, wa, 31, 0, blk=blk_a, seqs=range(0, wa.B, 25))
@@ -279,7 +280,7 @@ def test_mpfr_epoch_across_sampling_forms(psd):
     ws = torch.zeros(n, dtype=torch.uint8, device=DEV)
     status = torch.full((1,), -1, dtype=torch.int32, device=DEV)
     for rep in range(3):
-        for name, p, blk, ref in (("B=100", pa, blk_a, ref_a), ("B=16", pb, blk_b, ref_b)):
+        for name, p, blk, ref in (("B=125", pa, blk_a, ref_a), ("B=16", pb, blk_b, ref_b)):
             print(f"[mpfr] shared workspace, round {rep}, {name}", flush=True)
             out = psd.verify(p, ws, blk["prefix_tokens"], blk["start_pos"], blk["target_logits"],
                              blk["draft_logits"], want_targets=True, status=status)
