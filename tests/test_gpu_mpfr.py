@@ -281,7 +281,7 @@ def test_mpfr_epoch_across_sampling_forms(psd):
     status = torch.full((1,), -1, dtype=torch.int32, device=DEV)
     for rep in range(3):
         for name, p, blk, ref in (("B=125", pa, blk_a, ref_a), ("B=16", pb, blk_b, ref_b)):
-            print(f"[mpfr] shared workspace, round {rep}, {name}", flush=True)
+            print(f"[mpfr] shared workspace, pass {rep}, {name}", flush=True)
             out = psd.verify(p, ws, blk["prefix_tokens"], blk["start_pos"], blk["target_logits"],
                              blk["draft_logits"], want_targets=True, status=status)
             torch.cuda.synchronize()
