@@ -228,7 +228,7 @@ bool mpfr_vec(const psd_params* p, const void* draft_logits) {
 // depth when it fits the device, else one per depth); *streamed tells whether the call
 // has a streaming launch.
 psd_status mpfr_prepare(const psd_params* p, const psd_block* b, psd::MpfrArgs& m, bool* streamed) {
-    *streamed = (long)b->batch * p->num_drafts < 1024;
+    *streamed = (long)b->batch * p->num_drafts < psd::kMpfrStreamBelow;
     if (!*streamed) return PSD_OK;
     const psd::WsLayout L = psd::ws_layout(b->batch, p->num_drafts, b->gamma, p->vocab, p->dtype == PSD_BF16);
     const psd::MpfrLayout M = psd::mpfr_layout(L, b->batch, p->num_drafts, b->gamma);

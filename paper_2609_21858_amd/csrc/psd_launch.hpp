@@ -79,9 +79,15 @@ struct MpfrArgs {
 struct MpfrLayout {
     size_t gm, rmax, seed, slot, ytok, total;
 };
+// Identical-drafter calls with fewer than this many (sequence, path) workgroups per
+// depth stream their draft rows in a launch of their own; larger ones stream each
+// depth's rows in its sampling launch.
+constexpr long kMpfrStreamBelow = 1024;
+
 inline MpfrLayout mpfr_layout(const WsLayout& L, int B, int K, int gamma) {
     MpfrLayout M;
-    const size_t rows = (size_t)B * K * gamma;
+    // the streamed rows' words exist only when the call has a streaming launch
+    const size_t rows = (long)B * K < kMpfrStreamBelow ? (size_t)B * K * gamma : 0;
     M.gm = L.total;
     M.rmax = align256(M.gm + rows * (size_t)L.ng * 8);
     M.seed = align256(M.rmax + rows * 8);
