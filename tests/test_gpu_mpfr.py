@@ -169,6 +169,22 @@ def test_mpfr_config3_all_sequences(psd, layout):
     run_mpfr(psd, workloads.WORKLOADS[3], 3, layout, gen_device=DEV)
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_config4_sampled(psd, layout):
+    """V=151936, K=8, gamma=8, B=128, fp32 logits: B K = 1024, so one sampling launch per
+    depth, each streaming its rows (three workgroups per CU).  Every 16th sequence
+    against the oracle."""
+    run_mpfr(psd, workloads.WORKLOADS[4], 4, layout, gen_device=DEV, seqs=range(0, 128, 16))
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_mpfr_config5_sampled(psd, layout):
+    """V=256000, K=16, gamma=4, B=256, bf16: one sampling launch per depth with 4096
+    workgroups, contexts of up to 16 identical drafters.  Every 32nd sequence against
+    the oracle."""
+    run_mpfr(psd, workloads.WORKLOADS[5], 5, layout, gen_device=DEV, seqs=range(3, 256, 32))
+
+
 def test_mpfr_detection_pivot_is_slot0(psd):
     """Detection in MPFR mode scores the slot-0 clock: it equals the oracle's K = 1 score."""
     w = workloads.WORKLOADS[3]
