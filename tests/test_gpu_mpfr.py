@@ -114,6 +114,8 @@ def test_mpfr_config1(psd, layout):
     dict(V=1, K=2, gamma=2, B=1, dtype="fp32", m=1, T_draft=1.0),      # one token
     dict(V=40000, K=8, gamma=3, B=2, dtype="bf16", m=3, T_draft=0.5),  # several level-4 nodes, nu up to 8
     dict(V=20000, K=16, gamma=2, B=2, dtype="fp32", m=16, T_draft=2.0),  # nu = 16, long window
+    dict(V=500, K=32, gamma=3, B=2, dtype="bf16", m=2, T_draft=1.0),    # the most drafters
+    dict(V=300, K=2, gamma=32, B=2, dtype="fp32", m=4, T_draft=1.0),    # the most depths in one launch
 ])
 def test_mpfr_ragged_and_edge_shapes(psd, layout, case):
     w = workloads.custom(case["V"], case["K"], case["gamma"], case["B"], dtype=case["dtype"], m=case["m"],
@@ -167,6 +169,23 @@ def test_mpfr_config2_full(psd, layout):
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_mpfr_config3_all_sequences(psd, layout):
     run_mpfr(psd, workloads.WORKLOADS[3], 3, layout, gen_device=DEV)
+
+
+def test_mpfr_rows_without_finite_logits(psd):
+    """Rows with no finite logit.  All paths of sequence 0 at depth 1: the context draws
+    -1 for each of them, and the deeper contexts build on those drafts.  Path 2 of
+    sequence 1 at depth 0: its context's proposal row is path 0's, so only its own LSE
+    reads -inf.  A target row of sequence 2: its target is -1 and ends the block there.
+    Everything as the oracle has it."""
+    w = workloads.custom(700, 4, 4, 3, dtype="fp32", m=2, tau=0.7, sigma=2.0, alpha=1.0, T_draft=1.0)
+    blk = workloads.make_block(w, 14)
+    blk["draft_logits"][0, :, 1, :] = -np.inf
+    blk["draft_logits"][1, 2, 0, :] = -np.inf
+    blk["target_logits"][2, 3, :] = -np.inf
+    for layout in LAYOUTS:
+        out, _ = run_mpfr(psd, w, 14, layout, blk=blk)
+        assert (out["draft_tokens"][0, :, 1] == -1).all()
+        assert out["draft_lse"][1, 2, 0] == -np.inf
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
