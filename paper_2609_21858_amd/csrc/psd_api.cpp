@@ -428,7 +428,8 @@ namespace {
 
 // Identical drafters with one shared target chain: the target chain needs no draft
 // until the walk, so the fused kernel races it (without the walk) on the side
-// stream while the drafting launches run on the caller's stream; the walk kernel
+// stream while the drafts are sampled on the caller's stream (the draft rows are
+// streamed on whichever stream lets the sampling start soonest); the walk kernel
 // follows both.  The race kernel's error bits go to a control word that the walk
 // kernel adds to the call's status.
 psd_status verify_mpfr_forked(const psd_params* params, const psd_block* block, const void* target_logits,
