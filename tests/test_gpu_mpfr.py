@@ -323,3 +323,32 @@ def test_mpfr_epoch_across_sampling_forms(psd):
             assert int(status[0]) == 0 and psd.workspace_errors(ws) == 0
             for k in ("out_tokens", "out_len", "draft_tokens", "target_tokens"):
                 assert torch.equal(out[k], ref[k]), (rep, name, k)
+
+
+def test_modes_alternate_on_one_workspace(psd):
+    """Distinct-drafter and identical-drafter calls of one block alternate on one
+    workspace (sized for the larger): the race kernel's epoch and the identical-drafter
+    launches' epoch advance independently, and every call equals the same call on a
+    fresh workspace."""
+    w = workloads.WORKLOADS[2]
+    blk = workloads.make_block(w, 17, device=DEV)
+    ph = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype)
+    pm = psd.make_params(w.key, w.V, w.K, w.m, w.T_target, w.T_draft, dtype=w.torch_dtype, mode=psd.PSD_MODE_MPFR)
+
+    def call(p, ws):
+        out = psd.verify(p, ws, blk["prefix_tokens"], blk["start_pos"], blk["target_logits"], blk["draft_logits"],
+                         want_targets=True)
+        torch.cuda.synchronize()
+        assert psd.workspace_errors(ws) == 0
+        return {k: v.clone() for k, v in out.items()}
+
+    ref = {"het": call(ph, psd.new_workspace(ph, w.B, w.gamma, DEV)),
+           "mpfr": call(pm, psd.new_workspace(pm, w.B, w.gamma, DEV))}
+    n = max(psd.workspace_bytes(ph, w.B, w.gamma), psd.workspace_bytes(pm, w.B, w.gamma))
+    ws = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    for rep in range(3):
+        for name, p in (("het", ph), ("mpfr", pm), ("mpfr", pm), ("het", ph)):
+            print(f"[mpfr] shared workspace, pass {rep}, {name}", flush=True)
+            got = call(p, ws)
+            for k in ("out_tokens", "out_len", "draft_tokens", "target_tokens"):
+                assert torch.equal(got[k], ref[name][k]), (rep, name, k)
